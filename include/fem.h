@@ -1,0 +1,107 @@
+/*
+ * fem.h -- C ABI of the MI355X Free Energy Mixer (FEM) read library (libfem.so).
+ *
+ * The library computes the FEM free-energy read of "Free Energy Mixer"
+ * (Lu & Yang, ICLR 2026): for every batch b, head h, step t and channel j,
+ *
+ *     F[b,h,t,j] = (1 / beta[h,j]) * log  sum_{i <= t}  p_t(i) * exp(beta[h,j] * v[b,h,i,j])
+ *
+ * (Sec. 2.3, free-energy read, eq. fem-free-energy-main), over a causal prior
+ * p_t on the support {0, ..., t} (0-based, diagonal included):
+ *
+ *   fem_softmax_fwd:  p_t(i) = softmax_{i <= t}( q_t . k_i / sqrt(d) )
+ *                     (Sec. 1, masked scores; Appendix "Parameterizations of
+ *                      the Prior Selection", softmax prior, with no bias term)
+ *   fem_linear_fwd:   p_t(i) = <phi(q_t), phi(k_i)> / sum_{r <= t} <phi(q_t), phi(k_r)>,
+ *                     phi = elu + 1  (Appendix "Selection distributions,
+ *                      support, and normalization", linear attention)
+ *
+ * Conventions shared by every entry point:
+ *   - Q, K, V, beta and out are DEVICE pointers (HIP device memory, e.g.
+ *     torch tensors' data_ptr()).  The caller owns every buffer; the library
+ *     keeps no pointer after the call returns.
+ *   - Layout: contiguous row-major [B, H, T, width] (width fastest); Q, K, V
+ *     16-byte aligned.  beta is [H, width_v] float32, shared over B and T.
+ *   - out is always float32 [B, H, T, width_v] and must not alias an input.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; 0 is the null
+ *     stream): they return after enqueueing the kernels.  Launch errors are
+ *     reported as FEM_ERR_HIP; errors of the kernels themselves surface at the
+ *     caller's next synchronisation.
+ *   - Every argument check is made on the host before anything is launched;
+ *     on error nothing is launched and `out` is untouched.  The library never
+ *     aborts, throws or prints.
+ *   - Preconditions that are NOT checked (they would need a device read):
+ *     beta finite and > 0 (the read is defined for beta > 0 only, Sec. 2.3)
+ *     and all inputs finite.  Violations give unspecified values; NaN inputs
+ *     propagate.
+ */
+#ifndef FEM_H
+#define FEM_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of Q, K and V.  beta and out are always float32. */
+typedef enum {
+  FEM_DTYPE_F32 = 0,
+  FEM_DTYPE_BF16 = 1
+} fem_dtype;
+
+typedef enum {
+  FEM_OK = 0,
+  FEM_ERR_NULLPTR = 1,      /* a required pointer is NULL                      */
+  FEM_ERR_SHAPE = 2,        /* B, H or T <= 0, or a size overflows             */
+  FEM_ERR_UNSUPPORTED = 3,  /* width, chunk or dtype outside the supported set */
+  FEM_ERR_ALIGN = 4,        /* Q, K or V not 16-byte aligned                   */
+  FEM_ERR_HIP = 5           /* a HIP call or kernel launch failed              */
+} fem_status;
+
+/*
+ * Causal softmax-prior FEM read (Sec. 2.3 with the softmax prior of Sec. 1).
+ *
+ *   Q, K, V : [B, H, T, d], element type `dtype`
+ *   beta    : [H, d] float32, > 0
+ *   out     : [B, H, T, d] float32
+ *   d       : 32, 64 or 128 for FEM_DTYPE_BF16 (matrix-core path);
+ *             any 1 <= d <= 256 for FEM_DTYPE_F32 (exact vector path)
+ *
+ * Score scale is fixed at 1/sqrt(d).  Returns a fem_status.
+ */
+int fem_softmax_fwd(const void* Q, const void* K, const void* V,
+                    const float* beta, float* out,
+                    int B, int H, int T, int d, int dtype, hipStream_t stream);
+
+/*
+ * Causal linear-prior FEM read, phi = elu + 1, as an O(T) chunked scan
+ * (Appendix "Parameterizations of the Prior Selection": associative-scan
+ * form with a constant channel appended to the values for the normaliser;
+ * no decay and no feature scaling).
+ *
+ *   Q, K    : [B, H, T, d_k], element type `dtype`
+ *   V       : [B, H, T, d_v], element type `dtype`
+ *   beta    : [H, d_v] float32, > 0
+ *   out     : [B, H, T, d_v] float32
+ *   d_k, d_v: 64 (both)
+ *   chunk   : scan chunk length, 16, 32, 64 or 128.  It only schedules the
+ *             work: the result does not depend on it beyond rounding.
+ *   dtype   : FEM_DTYPE_BF16
+ *
+ * Returns a fem_status.
+ */
+int fem_linear_fwd(const void* Q, const void* K, const void* V,
+                   const float* beta, float* out,
+                   int B, int H, int T, int d_k, int d_v, int chunk,
+                   int dtype, hipStream_t stream);
+
+/* Static, NUL-terminated name of a status code (never NULL). */
+const char* fem_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FEM_H */

@@ -1,0 +1,236 @@
+"""Plain float64 oracle of the Free Energy Mixer (FEM) read.
+
+TEST INFRASTRUCTURE.  This module is a slow, obviously-correct CPU statement of
+what the HIP library computes.  It is used only by the tests, the smoke check
+and the CPU-baseline leg of the benchmark; the product path never touches it.
+It shares no code with the HIP path: the only thing the two sides share is the
+seeded input generator, which holds none of the method's arithmetic.
+
+What is computed (paper, Sec. 1 and Sec. 2.3; Appendix "Selection
+distributions, support, and normalization"; Appendix "Parameterizations of the
+Prior Selection", softmax prior):
+
+  prior     p_t(i) = softmax over i <= t of  q_t . k_i / sqrt(d)      (softmax)
+            p_t(i) = <phi(q_t), phi(k_i)> / sum_{r<=t} <phi(q_t), phi(k_r)>
+                     with phi = elu + 1                                (linear)
+  read      F_{t,j} = (1 / beta_j) * log sum_{i<=t} p_t(i) * exp(beta_j v_{i,j})
+                                  (free-energy read, eq. fem-free-energy-main)
+
+Indices are 0-based here; the causal support of row t is {0, ..., t}, diagonal
+included.  The read is exact up to float64 rounding: the only numerical device
+is the per-channel log-sum-exp shift of the paper's "Numerical stability"
+paragraph (Appendix, two-level gated FEM), i.e. a constant c_j subtracted
+inside the exponential and added back after the logarithm, which is an exact
+identity for any constant.
+
+Nothing here is blocked, fused or reordered beyond evaluating the rows of the
+output independently (each row's formula is unchanged) and using a float64
+matrix product for the sum over i.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# Smallest per-(t, j) sum that the shifted matrix-product evaluation accepts;
+# anything smaller is recomputed with a joint per-(t, j) log-sum-exp, which has
+# no underflow at all.  float64's normal range ends near 2.2e-308.
+_TINY = 1e-280
+
+
+def elu_plus_one(x: np.ndarray) -> np.ndarray:
+    """phi(x) = elu(x) + 1: x + 1 for x > 0, exp(x) for x <= 0.
+
+    The paper leaves the nonnegative feature map of the linear prior open
+    (Appendix "Selection distributions ..."); this build fixes phi = elu + 1.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+def softmax_prior_rows(q: np.ndarray, k: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """Causal softmax prior for the requested query rows.
+
+    q: [T, d], k: [T, d] float64; rows: 1-D int array of query indices.
+    Returns P with P[r, i] = p_{rows[r]}(i) for i < n, n = max(rows) + 1,
+    and P[r, i] = 0 for i > rows[r] (causal mask, support {0..t}).
+    Sec. 1 (masked scores s_{t,i} = q_t.k_i / sqrt d, -inf for i > t;
+    alpha = softmax(s)).
+    """
+    d = q.shape[1]
+    n = int(rows.max()) + 1
+    s = (q[rows] @ k[:n].T) / math.sqrt(d)
+    mask = np.arange(n)[None, :] <= rows[:, None]
+    s = np.where(mask, s, -np.inf)
+    s = s - s.max(axis=1, keepdims=True)
+    e = np.exp(s)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def softmax_logprior_rows(q: np.ndarray, k: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """log p_t(i) of the causal softmax prior (-inf off the support)."""
+    d = q.shape[1]
+    n = int(rows.max()) + 1
+    s = (q[rows] @ k[:n].T) / math.sqrt(d)
+    mask = np.arange(n)[None, :] <= rows[:, None]
+    s = np.where(mask, s, -np.inf)
+    m = s.max(axis=1, keepdims=True)
+    return s - (m + np.log(np.exp(s - m).sum(axis=1, keepdims=True)))
+
+
+def linear_prior_rows(q: np.ndarray, k: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """Causal linear-attention prior p_t(i) = <phi q_t, phi k_i> / sum_{r<=t} (...)
+
+    Appendix "Selection distributions, support, and normalization" (linear
+    attention) and the unified interface p_t(i) = s_t(i) / sum_{r<=t} s_t(r)
+    (Appendix "Parameterizations of the Prior Selection").  No 1/sqrt(d)
+    factor: the normalisation makes p invariant to any scaling of phi.
+    """
+    n = int(rows.max()) + 1
+    a = elu_plus_one(q[rows]) @ elu_plus_one(k[:n]).T
+    mask = np.arange(n)[None, :] <= rows[:, None]
+    a = np.where(mask, a, 0.0)
+    return a / a.sum(axis=1, keepdims=True)
+
+
+def free_energy_read(p: np.ndarray, v: np.ndarray, beta: np.ndarray,
+                     logp=None) -> np.ndarray:
+    """F[r, j] = (1/beta_j) log sum_i p[r, i] exp(beta_j v[i, j]).
+
+    p: [R, n] prior rows (zero off the support); v: [n, D]; beta: [D] > 0.
+    Eq. fem-free-energy-main / eq. fem-fixed (Sec. 2.3), evaluated as
+      G = p @ exp(beta*v - c),  F = (log G + c) / beta,
+    with c_j = max_i beta_j v_{i,j} (the paper's per-channel LSE shift).
+    Entries whose G would fall near float64 underflow are recomputed as a
+    joint log-sum-exp of log p + beta v for that single (r, j).
+    ``logp`` (an array shaped like p, or a function returning one) supplies
+    exact log-probabilities for that fallback; if absent, log p is taken
+    from p.
+    """
+    beta = np.asarray(beta, dtype=np.float64)
+    x = v * beta[None, :]
+    c = x.max(axis=0)
+    g = p @ np.exp(x - c[None, :])
+    with np.errstate(divide="ignore"):
+        out = (np.log(g) + c[None, :]) / beta[None, :]
+    bad = ~(g > _TINY)
+    if bad.any():
+        if callable(logp):
+            logp = logp()
+        if logp is None:
+            with np.errstate(divide="ignore"):
+                logp = np.log(p)
+        for r, j in zip(*np.nonzero(bad)):
+            w = logp[r] + x[:, j]
+            w = w[np.isfinite(w)]
+            mw = w.max()
+            out[r, j] = (mw + math.log(np.exp(w - mw).sum())) / beta[j]
+    return out
+
+
+def posterior(p_row: np.ndarray, v_col: np.ndarray, beta: float) -> np.ndarray:
+    """Posterior selector q(i) proportional to p(i) exp(beta v_i) on the support.
+
+    Eq. fem-posterior-main (Sec. 2.3).  Used by the tests to check the
+    reverse-KL identity and the gradient identity of the read.
+    """
+    w = np.full(p_row.shape, -np.inf)
+    sup = p_row > 0
+    w[sup] = np.log(p_row[sup]) + beta * v_col[sup]
+    w = w - w.max()
+    e = np.exp(w)
+    return e / e.sum()
+
+
+def _as64(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64)
+
+
+def _row_blocks(rows: np.ndarray, block: int):
+    for s in range(0, len(rows), block):
+        yield rows[s:s + block]
+
+
+def fem_softmax(q, k, v, beta, rows=None, block: int = 512) -> np.ndarray:
+    """FEM read with the causal softmax prior.
+
+    q, k: [B, H, T, d]; v: [B, H, T, d_v]; beta: [H, d_v] (> 0), shared
+    over batch and time.
+    rows: optional 1-D array of query rows to evaluate (default: all T).
+    Returns float64 [B, H, len(rows), d].
+    """
+    q, k, v, beta = _as64(q), _as64(k), _as64(v), _as64(beta)
+    B, H, T, _ = q.shape
+    dv = v.shape[3]
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = np.empty((B, H, len(rows), dv))
+    for b in range(B):
+        for h in range(H):
+            pos = 0
+            for rb in _row_blocks(rows, block):
+                n = int(rb.max()) + 1
+                p = softmax_prior_rows(q[b, h], k[b, h], rb)
+                lp = (lambda qq=q[b, h], kk=k[b, h], rr=rb:
+                      softmax_logprior_rows(qq, kk, rr))
+                out[b, h, pos:pos + len(rb)] = free_energy_read(
+                    p, v[b, h, :n], beta[h], logp=lp)
+                pos += len(rb)
+    return out
+
+
+def fem_linear(q, k, v, beta, rows=None, block: int = 512) -> np.ndarray:
+    """FEM read with the causal linear-attention prior (phi = elu + 1).
+
+    Quadratic evaluation of the definition: the masked, row-normalised
+    phi(Q) phi(K)^T, then the same free-energy read as the softmax case.
+    q, k: [B, H, T, d_k]; v: [B, H, T, d_v]; beta: [H, d_v].
+    """
+    q, k, v, beta = _as64(q), _as64(k), _as64(v), _as64(beta)
+    B, H, T, _ = q.shape
+    dv = v.shape[3]
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = np.empty((B, H, len(rows), dv))
+    for b in range(B):
+        for h in range(H):
+            pos = 0
+            for rb in _row_blocks(rows, block):
+                n = int(rb.max()) + 1
+                p = linear_prior_rows(q[b, h], k[b, h], rb)
+                out[b, h, pos:pos + len(rb)] = free_energy_read(p, v[b, h, :n], beta[h])
+                pos += len(rb)
+    return out
+
+
+def fem_linear_recurrent(q, k, v, beta) -> np.ndarray:
+    """The linear-prior read as a float64 recurrence over t.
+
+    Streaming form of the linearisable prior (Appendix "Parameterizations of
+    the Prior Selection", GLA prior with no decay; "Streaming compatibility":
+    a constant channel appended to the values gives the normaliser):
+      S_t = S_{t-1} + phi(k_t) exp(beta v_t - c)^T,   z_t = z_{t-1} + phi(k_t)
+      F_t = (log(phi(q_t)^T S_t) - log(phi(q_t)^T z_t) + c) / beta
+    with one global per-channel shift c_j = max_t beta_j v_{t,j}.  Used only as
+    an independent cross-check of ``fem_linear`` on small T.
+    """
+    q, k, v, beta = _as64(q), _as64(k), _as64(v), _as64(beta)
+    B, H, T, dk = q.shape
+    dv = v.shape[3]
+    out = np.empty((B, H, T, dv))
+    for b in range(B):
+        for h in range(H):
+            x = v[b, h] * beta[h][None, :]
+            c = x.max(axis=0)
+            e = np.exp(x - c[None, :])
+            fq = elu_plus_one(q[b, h])
+            fk = elu_plus_one(k[b, h])
+            S = np.zeros((dk, dv))
+            z = np.zeros(dk)
+            for t in range(T):
+                S += np.outer(fk[t], e[t])
+                z += fk[t]
+                num = fq[t] @ S
+                den = fq[t] @ z
+                out[b, h, t] = (np.log(num) - np.log(den) + c) / beta[h]
+    return out
