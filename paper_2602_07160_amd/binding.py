@@ -1,0 +1,128 @@
+"""Python binding of libfem.so (argument marshalling only).
+
+Each function has the name of the C entry point it calls (``include/fem.h``)
+and takes torch tensors for the device buffers: torch provides device memory
+and the stream, every step of the read runs in the library's HIP kernels.
+There is no fallback: if libfem.so is missing or a call fails, an exception
+is raised.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfem.so")
+
+FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
+
+EXPORTS = ("fem_softmax_fwd", "fem_linear_fwd", "fem_status_str")
+
+_lib = None
+
+
+class FemError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+def load() -> ctypes.CDLL:
+    """Load libfem.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2602_07160_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p
+        lib.fem_softmax_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, vp]
+        lib.fem_softmax_fwd.restype = i
+        lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp]
+        lib.fem_linear_fwd.restype = i
+        lib.fem_status_str.argtypes = [i]
+        lib.fem_status_str.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def fem_status_str(status: int) -> str:
+    return load().fem_status_str(int(status)).decode()
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise FemError(rc, fem_status_str(rc))
+
+
+def _dev_tensor(x: torch.Tensor, name: str, dtype=None) -> torch.Tensor:
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and x.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {x.dtype}")
+    return x
+
+
+def _stream_handle(device, stream) -> int:
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    return s.cuda_stream if isinstance(s, torch.cuda.Stream) else int(s)
+
+
+def fem_softmax_fwd(q, k, v, beta, out=None, stream=None) -> torch.Tensor:
+    """Causal softmax-prior FEM read.  q, k, v: [B, H, T, d] bf16 or fp32;
+    beta: [H, d] fp32.  Returns out [B, H, T, d] fp32 (enqueued on ``stream``,
+    default torch's current stream)."""
+    lib = load()
+    if q.dtype not in FEM_DTYPE:
+        raise ValueError(f"unsupported dtype {q.dtype}")
+    for name, x in (("q", q), ("k", k), ("v", v)):
+        _dev_tensor(x, name, q.dtype)
+        if x.dim() != 4 or x.shape != q.shape:
+            raise ValueError(f"{name} must be [B, H, T, d] like q")
+    B, H, T, d = q.shape
+    _dev_tensor(beta, "beta", torch.float32)
+    if tuple(beta.shape) != (H, d):
+        raise ValueError("beta must be [H, d]")
+    if out is None:
+        out = torch.empty((B, H, T, d), device=q.device, dtype=torch.float32)
+    _dev_tensor(out, "out", torch.float32)
+    if tuple(out.shape) != (B, H, T, d):
+        raise ValueError("out must be [B, H, T, d]")
+    with torch.cuda.device(q.device):
+        rc = lib.fem_softmax_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
+                                 out.data_ptr(), B, H, T, d, FEM_DTYPE[q.dtype],
+                                 _stream_handle(q.device, stream))
+    _check(rc)
+    return out
+
+
+def fem_linear_fwd(q, k, v, beta, out=None, chunk: int = 64, stream=None) -> torch.Tensor:
+    """Causal linear-prior (phi = elu + 1) FEM read.  q, k: [B, H, T, d_k];
+    v: [B, H, T, d_v] bf16; beta: [H, d_v] fp32.  Returns [B, H, T, d_v] fp32."""
+    lib = load()
+    if q.dtype not in FEM_DTYPE:
+        raise ValueError(f"unsupported dtype {q.dtype}")
+    _dev_tensor(q, "q", q.dtype)
+    _dev_tensor(k, "k", q.dtype)
+    _dev_tensor(v, "v", q.dtype)
+    if q.dim() != 4 or k.shape != q.shape or v.dim() != 4 or v.shape[:3] != q.shape[:3]:
+        raise ValueError("q, k must be [B, H, T, d_k] and v [B, H, T, d_v]")
+    B, H, T, dk = q.shape
+    dv = v.shape[3]
+    _dev_tensor(beta, "beta", torch.float32)
+    if tuple(beta.shape) != (H, dv):
+        raise ValueError("beta must be [H, d_v]")
+    if out is None:
+        out = torch.empty((B, H, T, dv), device=q.device, dtype=torch.float32)
+    _dev_tensor(out, "out", torch.float32)
+    if tuple(out.shape) != (B, H, T, dv):
+        raise ValueError("out must be [B, H, T, d_v]")
+    with torch.cuda.device(q.device):
+        rc = lib.fem_linear_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
+                                out.data_ptr(), B, H, T, dk, dv, int(chunk),
+                                FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+    _check(rc)
+    return out

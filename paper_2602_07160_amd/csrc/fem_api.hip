@@ -1,0 +1,72 @@
+// C ABI of libfem.so: argument validation and dispatch (declared in fem.h).
+
+#include "fem.h"
+#include "fem_internal.h"
+
+#include <stdint.h>
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Every [B, H, T, w] tensor must be indexable with 64-bit offsets and every
+// grid dimension must fit the launch limits.
+bool sizes_ok(int B, int H, int T, int w) {
+  if (B <= 0 || H <= 0 || T <= 0 || w <= 0) return false;
+  const unsigned long long n = (unsigned long long)B * H * T * w;
+  if (n > (1ull << 46)) return false;
+  if ((unsigned long long)B * H > 65535ull * 1024ull) return false;
+  return true;
+}
+
+int from_hip(hipError_t e) { return e == hipSuccess ? FEM_OK : FEM_ERR_HIP; }
+
+}  // namespace
+
+extern "C" int fem_softmax_fwd(const void* Q, const void* K, const void* V, const float* beta,
+                               float* out, int B, int H, int T, int d, int dtype,
+                               hipStream_t stream) {
+  if (!Q || !K || !V || !beta || !out) return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, T, d)) return FEM_ERR_SHAPE;
+  if (dtype == FEM_DTYPE_BF16) {
+    if (d != 32 && d != 64 && d != 128) return FEM_ERR_UNSUPPORTED;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return FEM_ERR_ALIGN;
+    return from_hip(fem::launch_softmax_bf16(Q, K, V, beta, out, B, H, T, d, stream));
+  }
+  if (dtype == FEM_DTYPE_F32) {
+    if (d > 256) return FEM_ERR_UNSUPPORTED;
+    if ((unsigned long long)B * H > 65535ull) return FEM_ERR_SHAPE;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return FEM_ERR_ALIGN;
+    return from_hip(fem::launch_softmax_f32(static_cast<const float*>(Q),
+                                            static_cast<const float*>(K),
+                                            static_cast<const float*>(V), beta, out, B, H, T,
+                                            d, stream));
+  }
+  return FEM_ERR_UNSUPPORTED;
+}
+
+extern "C" int fem_linear_fwd(const void* Q, const void* K, const void* V, const float* beta,
+                              float* out, int B, int H, int T, int d_k, int d_v, int chunk,
+                              int dtype, hipStream_t stream) {
+  if (!Q || !K || !V || !beta || !out) return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, T, d_k) || !sizes_ok(B, H, T, d_v)) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  if (d_k != 64 || d_v != 64) return FEM_ERR_UNSUPPORTED;
+  if (chunk != 16 && chunk != 32 && chunk != 64 && chunk != 128) return FEM_ERR_UNSUPPORTED;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return FEM_ERR_ALIGN;
+  const hipError_t e = fem::launch_linear_bf16(Q, K, V, beta, out, B, H, T, d_k, d_v, chunk, stream);
+  if (e == hipErrorNotSupported) return FEM_ERR_UNSUPPORTED;
+  return from_hip(e);
+}
+
+extern "C" const char* fem_status_str(int status) {
+  switch (status) {
+    case FEM_OK: return "FEM_OK";
+    case FEM_ERR_NULLPTR: return "FEM_ERR_NULLPTR: a required pointer is NULL";
+    case FEM_ERR_SHAPE: return "FEM_ERR_SHAPE: B, H, T or a width is not positive, or a size overflows";
+    case FEM_ERR_UNSUPPORTED: return "FEM_ERR_UNSUPPORTED: width, chunk or dtype outside the supported set";
+    case FEM_ERR_ALIGN: return "FEM_ERR_ALIGN: Q, K, V or out is not 16-byte aligned";
+    case FEM_ERR_HIP: return "FEM_ERR_HIP: a HIP call or kernel launch failed";
+    default: return "FEM_ERR_UNKNOWN: not a fem_status value";
+  }
+}

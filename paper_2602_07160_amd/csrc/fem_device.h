@@ -1,0 +1,72 @@
+// Device-side types and helpers shared by the FEM kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fem {
+
+typedef __bf16 bf16;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// v_exp_f32 (2^x) and v_log_f32 (log2 x): the hardware transcendental units.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float log2_hw(float x) { return __builtin_amdgcn_logf(x); }
+
+// Round two floats to bf16 (round-to-nearest-even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ bf16x2 to_bf16x2(float a, float b) {
+  f32x2 f = {a, b};
+  return __builtin_convertvector(f, bf16x2);
+}
+
+// a.x*b.x + a.y*b.y + c with bf16 pairs and an fp32 accumulator (v_dot2c_f32_bf16).
+__device__ __forceinline__ float dot2_bf16(bf16x2 a, bf16x2 b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(a, b, c, false);
+}
+
+// Value of lane (l ^ 32) for every lane l (v_permlane32_swap).
+__device__ __forceinline__ float other_half(float x) {
+  unsigned u = __float_as_uint(x);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  // lanes 0..31: r[1] holds lane l+32; lanes 32..63: r[0] holds lane l-32
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+// Streaming log2-sum-exp2 accumulator: value = m + log2(s).
+struct Lse2 {
+  float m = -INFINITY;
+  float s = 0.f;
+  __device__ __forceinline__ void add(float w) {
+    if (w > m) {
+      s = s * exp2_hw(m - w) + 1.f;
+      m = w;
+    } else {
+      s += exp2_hw(w - m);
+    }
+  }
+  // Combine across the 64 lanes of a wave; every lane gets the total.
+  __device__ __forceinline__ float wave_total() const {
+    float M = wave_max(m);
+    float part = (m == -INFINITY) ? 0.f : s * exp2_hw(m - M);
+    float S = wave_sum(part);
+    return M + log2_hw(S);
+  }
+};
+
+}  // namespace fem

@@ -1,0 +1,24 @@
+// Host-side launchers behind the C ABI (internal; not exported).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace fem {
+
+// Fused bf16 matrix-core softmax-prior read, d in {32, 64, 128}.
+hipError_t launch_softmax_bf16(const void* Q, const void* K, const void* V,
+                               const float* beta, float* out,
+                               int B, int H, int T, int d, hipStream_t stream);
+
+// Exact fp32 vector-unit softmax-prior read, 1 <= d <= 256.
+hipError_t launch_softmax_f32(const float* Q, const float* K, const float* V,
+                              const float* beta, float* out,
+                              int B, int H, int T, int d, hipStream_t stream);
+
+// Chunked-scan linear-prior read (phi = elu + 1), bf16, d_k = d_v = 64.
+hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V,
+                              const float* beta, float* out,
+                              int B, int H, int T, int dk, int dv, int chunk,
+                              hipStream_t stream);
+
+}  // namespace fem

@@ -1,0 +1,81 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point
+that include/fem.h declares, and rejects bad arguments before launching
+anything (no GPU needed: every call here fails validation on the host)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2602_07160_amd import binding
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "fem.h")
+
+OK, NULLPTR, SHAPE, UNSUPPORTED, ALIGN, HIPERR = range(6)
+BF16, F32 = 1, 0
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fem_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return binding.load()
+
+
+def test_exports_match_header(lib):
+    names = declared()
+    assert set(names) >= set(binding.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for s in range(6):
+        assert binding.fem_status_str(s).startswith(
+            ["FEM_OK", "FEM_ERR_NULLPTR", "FEM_ERR_SHAPE", "FEM_ERR_UNSUPPORTED",
+             "FEM_ERR_ALIGN", "FEM_ERR_HIP"][s])
+    assert "UNKNOWN" in binding.fem_status_str(99)
+
+
+# fake, never-dereferenced device addresses (validation fails first)
+A = 1 << 20
+
+
+def sm(lib, q=A, k=A, v=A, beta=A, out=A, B=1, H=1, T=8, d=64, dt=BF16):
+    return lib.fem_softmax_fwd(q, k, v, beta, out, B, H, T, d, dt, None)
+
+
+def ln(lib, q=A, k=A, v=A, beta=A, out=A, B=1, H=1, T=8, dk=64, dv=64, chunk=64, dt=BF16):
+    return lib.fem_linear_fwd(q, k, v, beta, out, B, H, T, dk, dv, chunk, dt, None)
+
+
+def test_softmax_validation(lib):
+    assert sm(lib, q=None) == NULLPTR
+    assert sm(lib, beta=None) == NULLPTR
+    assert sm(lib, out=None) == NULLPTR
+    assert sm(lib, T=0) == SHAPE
+    assert sm(lib, B=-1) == SHAPE
+    assert sm(lib, H=0) == SHAPE
+    assert sm(lib, B=1 << 20, H=1 << 20, T=1 << 20) == SHAPE
+    for d in (16, 48, 96, 256):
+        assert sm(lib, d=d) == UNSUPPORTED
+    assert sm(lib, d=300, dt=F32) == UNSUPPORTED
+    assert sm(lib, dt=7) == UNSUPPORTED
+    assert sm(lib, q=A + 2) == ALIGN
+    assert sm(lib, out=A + 4) == ALIGN
+    assert sm(lib, v=A + 8, dt=F32) == ALIGN
+
+
+def test_linear_validation(lib):
+    assert ln(lib, k=None) == NULLPTR
+    assert ln(lib, T=0) == SHAPE
+    assert ln(lib, dk=32) == UNSUPPORTED
+    assert ln(lib, dv=128) == UNSUPPORTED
+    assert ln(lib, chunk=48) == UNSUPPORTED
+    assert ln(lib, dt=F32) == UNSUPPORTED
+    assert ln(lib, v=A + 2) == ALIGN

@@ -1,0 +1,227 @@
+"""GPU parity of fem_softmax_fwd (HIP, through the C ABI) against the float64 oracle.
+
+Tolerances (max abs error, written per test): 1e-4 for fp32 inputs and 2e-2
+for bf16 inputs.  Every case prints its name, shape and seed before touching
+the GPU.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_07160_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL_BF16 = 2e-2
+TOL_F32 = 1e-4
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def run(fem, q, k, v, beta):
+    dev = torch.device("cuda:0")
+    out = fem.fem_softmax_fwd(q.to(dev), k.to(dev), v.to(dev), beta.to(dev))
+    torch.cuda.synchronize()
+    return out.cpu().double().numpy()
+
+
+def ref(q, k, v, beta, rows=None):
+    return oracle.fem_softmax(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                              beta.double().numpy(), rows=rows)
+
+
+def check(got, want, tol, what):
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got - want).max()
+    say(f"{what}: max abs err {err:.3e} (tol {tol})")
+    assert err <= tol, f"{what}: max abs err {err} > {tol}"
+    return err
+
+
+# --------------------------------------------------------------------------
+# the five workloads (softmax ones): full oracle where it is cheap, sampled
+# rows at full size otherwise
+# --------------------------------------------------------------------------
+def test_workload1_fp32_full(fem):
+    say("workload 1: fp32 B1 H1 T128 d32, seed 43")
+    q, k, v, b = inputs.make_inputs(1)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_F32, "w1")
+
+
+def test_workload2_bf16_full(fem):
+    say("workload 2: bf16 B4 H8 T1024 d64, seed 44")
+    q, k, v, b = inputs.make_inputs(2)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, "w2")
+
+
+def _sampled_rows(T, rng, extra=12):
+    fixed = [0, 1, 2, 31, 32, 63, 64, 65, 127, 255, 256, 257, T // 2, T - 2, T - 1]
+    rows = set(x for x in fixed if 0 <= x < T)
+    rows |= set(int(x) for x in rng.integers(0, T, extra))
+    return np.array(sorted(rows))
+
+
+def test_workload3_full_size_sampled(fem):
+    say("workload 3: bf16 B8 H16 T4096 d128, seed 45, sampled rows")
+    q, k, v, b = inputs.make_inputs(3)
+    got = run(fem, q, k, v, b)
+    rng = np.random.default_rng(0)
+    rows = _sampled_rows(4096, rng)
+    for bb, hh in [(0, 0), (3, 7), (7, 15), (5, 2)]:
+        want = oracle.fem_softmax(q[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                  k[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                  v[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                  b[hh:hh + 1].double().numpy(), rows=rows)[0, 0]
+        check(got[bb, hh, rows], want, TOL_BF16, f"w3 b{bb} h{hh}")
+
+
+def test_workload3_reduced_full(fem):
+    say("workload 3 recipe, reduced: B1 H2 T600 d128 (ragged), full oracle")
+    q, k, v, b = inputs.make_inputs(3, B=1, H=2, T=600)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, "w3-reduced")
+
+
+def test_workload4_full_size_sampled(fem):
+    say("workload 4: bf16 B1 H8 T16384 d64 offset/clip, seed 46, sampled rows")
+    q, k, v, b = inputs.make_inputs(4)
+    got = run(fem, q, k, v, b)
+    rows = _sampled_rows(16384, np.random.default_rng(1), extra=20)
+    want = ref(q, k, v, b, rows=rows)
+    check(got[:, :, rows], want, TOL_BF16, "w4")
+
+
+def test_workload4_reduced_full(fem):
+    say("workload 4 recipe, reduced: B1 H8 T2048 d64, full oracle")
+    q, k, v, b = inputs.make_inputs(4, T=2048)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, "w4-reduced")
+
+
+# --------------------------------------------------------------------------
+# shapes: every supported d, ragged T, T=1, tile boundaries, many heads
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("T", [1, 2, 31, 63, 64, 65, 255, 256, 257, 700])
+def test_bf16_shapes(fem, d, T):
+    say(f"bf16 shape B2 H3 T{T} d{d}, seed {1000 + T + d}")
+    q, k, v, b = inputs.draw(1000 + T + d, 2, 3, T, d, dtype="bf16")
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, f"T{T} d{d}")
+
+
+@pytest.mark.parametrize("d", [1, 7, 32, 100, 256])
+@pytest.mark.parametrize("T", [1, 5, 300])
+def test_fp32_shapes(fem, d, T):
+    say(f"fp32 shape B2 H2 T{T} d{d}")
+    q, k, v, b = inputs.draw(2000 + T + d, 2, 2, T, d, dtype="f32", beta_lo=0.25, beta_hi=4.0)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_F32, f"fp32 T{T} d{d}")
+
+
+# --------------------------------------------------------------------------
+# numerics: small and large beta, peaked scores, equal scores, underflow
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("beta", [1e-3, 0.1, 1.0, 16.0, 64.0])
+def test_bf16_beta_extremes(fem, beta):
+    say(f"bf16 constant beta {beta}: B1 H2 T512 d64")
+    q, k, v, _ = inputs.draw(3000, 1, 2, 512, 64, dtype="bf16")
+    b = torch.full((2, 64), beta, dtype=torch.float32)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, f"beta={beta}")
+
+
+def test_bf16_peaked_scores(fem):
+    say("bf16 peaked scores q = 8 k_t: B1 H2 T384 d64")
+    q, k, v, b = inputs.draw(3001, 1, 2, 384, 64, dtype="bf16")
+    q = (8.0 * k.float()).to(torch.bfloat16)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, "peaked")
+
+
+def test_bf16_equal_scores_is_logcumsumexp(fem):
+    say("bf16 Q = 0 (uniform prior) vs torch.logcumsumexp: B2 H2 T300 d64")
+    q, k, v, b = inputs.draw(3002, 2, 2, 300, 64, dtype="bf16")
+    q = torch.zeros_like(q)
+    got = run(fem, q, k, v, b)
+    x = v.double() * b.double()[None, :, None, :]
+    want = (torch.logcumsumexp(x, dim=2) - torch.log(torch.arange(1, 301, dtype=torch.float64))[:, None]) \
+        / b.double()[None, :, None, :]
+    check(got, want.numpy(), TOL_BF16, "uniform prior")
+
+
+def test_bf16_first_tile_underflow(fem):
+    """In-support values 160 nats below a masked value in the same tile: the
+    shared column shift leaves rows 0..31 with an underflowed accumulator,
+    which the exact per-(t, j) path must repair."""
+    say("bf16 forced underflow: B1 H1 T128 d64, v=-5 then +5 at key 32, beta=16")
+    q, k, _, _ = inputs.draw(3003, 1, 1, 128, 64, dtype="bf16")
+    v = torch.full((1, 1, 128, 64), -5.0)
+    v[:, :, 32] = 5.0
+    v[:, :, 40:] = torch.randn(1, 1, 88, 64, generator=torch.Generator().manual_seed(0))
+    v = v.to(torch.bfloat16)
+    b = torch.full((1, 64), 16.0)
+    got = run(fem, q, k, v, b)
+    check(got, ref(q, k, v, b), TOL_BF16, "underflow repair")
+    np.testing.assert_allclose(got[0, 0, :32], -5.0, atol=TOL_BF16)
+
+
+def test_bf16_scale_law(fem):
+    """F(beta; 2v) = 2 F(2beta; v); doubling is exact in bf16."""
+    say("bf16 scale law a=2: B1 H2 T400 d128")
+    q, k, v, b = inputs.draw(3004, 1, 2, 400, 128, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
+    lhs = run(fem, q, k, (2 * v.float()).to(torch.bfloat16), b)
+    rhs = 2 * run(fem, q, k, v, 2 * b)
+    check(lhs, rhs, 2 * TOL_BF16, "scale law")
+
+
+def test_bf16_causality(fem):
+    say("bf16 causality: perturb keys/values after t=300, B1 H2 T640 d64")
+    q, k, v, b = inputs.draw(3005, 1, 2, 640, 64, dtype="bf16")
+    a = run(fem, q, k, v, b)
+    k2, v2 = k.clone(), v.clone()
+    k2[:, :, 301:] = (3 * torch.randn(k2[:, :, 301:].shape)).to(torch.bfloat16)
+    v2[:, :, 301:] = (3 * torch.randn(v2[:, :, 301:].shape)).to(torch.bfloat16)
+    b2 = run(fem, q, k2, v2, b)
+    err = np.abs(a[:, :, :301] - b2[:, :, :301]).max()
+    say(f"causality: rows <= 300 changed by {err:.3e}")
+    assert err <= 1e-5
+    assert np.abs(a[:, :, 301:] - b2[:, :, 301:]).max() > 1e-3
+
+
+def test_bf16_deterministic(fem):
+    say("bf16 determinism: two runs bit-identical, B2 H4 T1000 d128")
+    q, k, v, b = inputs.draw(3006, 2, 4, 1000, 128, dtype="bf16")
+    a = run(fem, q, k, v, b)
+    c = run(fem, q, k, v, b)
+    assert np.array_equal(a, c)
+
+
+def test_nondefault_stream(fem):
+    say("bf16 on a non-default stream: B1 H2 T500 d64")
+    q, k, v, b = inputs.draw(3007, 1, 2, 500, 64, dtype="bf16")
+    dev = torch.device("cuda:0")
+    qd, kd, vd, bd = q.to(dev), k.to(dev), v.to(dev), b.to(dev)
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s):
+        out = fem.fem_softmax_fwd(qd, kd, vd, bd)
+    s.synchronize()
+    check(out.cpu().double().numpy(), ref(q, k, v, b), TOL_BF16, "stream")
+
+
+def test_binding_rejects_bad_arguments(fem):
+    say("binding argument errors")
+    dev = torch.device("cuda:0")
+    q = torch.zeros(1, 1, 8, 48, dtype=torch.bfloat16, device=dev)
+    b = torch.ones(1, 48, device=dev)
+    with pytest.raises(fem.FemError) as e:
+        fem.fem_softmax_fwd(q, q, q, b)
+    assert e.value.status == 3
+    q = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16, device=dev)
+    with pytest.raises(ValueError):
+        fem.fem_softmax_fwd(q, q, q, torch.ones(2, 64, device=dev))
+    with pytest.raises(ValueError):
+        fem.fem_softmax_fwd(q, q.transpose(2, 3).contiguous().transpose(2, 3), q,
+                            torch.ones(1, 64, device=dev))
