@@ -30,8 +30,14 @@
 //     per-(t, j) log-sum-exp in fp32.
 //
 // Work decomposition: one workgroup of NW waves owns BQ = 32*NW query rows of
-// one (b, h); each wave owns 32 rows.  Workgroups are launched longest-first
-// (largest causal extent first); consecutive heads land on consecutive XCDs.
+// one (b, h); each wave owns 32 rows for the products and D/NW channels for
+// the tilt.  Software pipeline, one barrier per 64-key tile: while a wave
+// multiplies tile k (K, E of tile k in LDS buffer k%2) it also tilts its own
+// channels of tile k+1 (V of tile k+1 -> E buffer (k+1)%2; the running column
+// maximum needs no cross-wave reduction because a channel is owned by one
+// wave), and its prefetched global loads for K(k+1) and V(k+2) are parked in
+// the free buffers.  Workgroups run longest causal extent first; workgroup i
+// of a causal level covers head i, so a head's workgroups share an XCD.
 
 #include "fem_device.h"
 #include "fem_internal.h"
@@ -46,6 +52,9 @@ constexpr float kColLag = 16.f;      // column shift raised only past this lag
 constexpr float kRowLag = 8.f;       // row max raised only past this lag (P <= 2^8)
 constexpr float kUnderflow = 0x1p-64f;
 
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+
 template <int D, int NW>
 struct Cfg {
   static constexpr int BQ = NW * 32;      // query rows per workgroup
@@ -53,14 +62,30 @@ struct Cfg {
   static constexpr int NT = NW * 64;      // threads
   static constexpr int NCB = D / 32;      // 32-channel output blocks
   static constexpr int NKS = D / 16;      // 16-wide k-steps of Q K^T
-  static constexpr int KROW = D + 8;      // K tile row stride (bf16), +16 B pad
+  static constexpr int KROW = D + 8;      // K / V tile row stride (bf16): one 16-byte pad slot
   static constexpr int EROW = BK + 8;     // E^T row stride (bf16), +16 B pad
-  static constexpr int NPART = NT / D;    // tilt threads per channel
-  static constexpr int KPP = BK / NPART;  // keys per tilt thread
-  static constexpr size_t LDS =
-      sizeof(bf16) * (BK * KROW + BK * D + 2 * D * EROW) +
-      sizeof(float) * (4 * D + NPART * D + NW * D) + 16;
-  static_assert(NT % D == 0 && BK % NPART == 0, "tilt mapping");
+  static constexpr int CPW = D / NW;      // channels tilted per wave
+  static constexpr int G = 64 / CPW;      // lanes per channel in the tilt
+  static constexpr int RPL = 16 / G;      // 4-key runs per tilt lane
+  // K / V tiles are filled by direct global->LDS loads: each wave instruction
+  // writes 64 consecutive 16-byte slots (1 KiB); a padded row is SPR slots.
+  static constexpr int SPR = KROW / 8;               // slots per padded row
+  static constexpr int BLOCKS = BK * SPR / 64;       // 1 KiB blocks per tile
+  static constexpr int BPW = (BLOCKS + NW - 1) / NW; // blocks per wave
+  // LDS layout (bytes)
+  static constexpr int KB = BK * KROW * 2;
+  static constexpr int EB = D * EROW * 2;
+  static constexpr int OFF_K = 0;                 // 2 buffers
+  static constexpr int OFF_V = OFF_K + 2 * KB;    // 2 buffers
+  static constexpr int OFF_EH = OFF_V + 2 * KB;   // 2 buffers
+  static constexpr int OFF_EL = OFF_EH + 2 * EB;  // 2 buffers
+  static constexpr int OFF_F = OFF_EL + 2 * EB;   // floats
+  static constexpr int NF = D /*bl*/ + D /*inv*/ + 2 * D /*c*/ + 2 * D /*g*/ + NW * D /*cw*/;
+  static constexpr int OFF_R = OFF_F + NF * 4;    // rose flags [2][NW]
+  static constexpr size_t LDS = OFF_R + 2 * NW * 4;
+  static_assert(CPW * NW == D && G * CPW == 64 && RPL * G == 16, "tilt mapping");
+  static_assert(BK * SPR % 64 == 0, "tile = whole 1 KiB blocks");
+  static_assert(LDS <= 160 * 1024, "LDS budget");
 };
 
 // Position of key r (0..63 within a tile) inside an E^T row.  Within each
@@ -98,29 +123,121 @@ __device__ float exact_read(const bf16* __restrict__ Qh, const bf16* __restrict_
 }
 
 template <int D, int NW>
+struct Smem {
+  using C = Cfg<D, NW>;
+  unsigned char* base;
+  __device__ unsigned char* k(int b) const { return base + C::OFF_K + b * C::KB; }
+  __device__ unsigned char* v(int b) const { return base + C::OFF_V + b * C::KB; }
+  __device__ unsigned char* eh(int b) const { return base + C::OFF_EH + b * C::EB; }
+  __device__ unsigned char* el(int b) const { return base + C::OFF_EL + b * C::EB; }
+  __device__ float* bl() const { return reinterpret_cast<float*>(base + C::OFF_F); }
+  __device__ float* inv() const { return bl() + D; }
+  __device__ float* c(int b) const { return bl() + 2 * D + b * D; }
+  __device__ float* g(int b) const { return bl() + 4 * D + b * D; }
+  __device__ float* cw(int w) const { return bl() + 6 * D + w * D; }
+  __device__ int* rose(int b) const { return reinterpret_cast<int*>(base + C::OFF_R) + b * NW; }
+};
+
+// Bits of two floats' upper halves packed into one dword (bf16 truncation).
+__device__ __forceinline__ unsigned pack_hi16(float lo_elem, float hi_elem) {
+  return __builtin_amdgcn_perm(__float_as_uint(hi_elem), __float_as_uint(lo_elem), 0x07060302u);
+}
+
+// Tilt of tile tt (first key k0) for this wave's CPW channels: column max over
+// the tile (in-lane, then across the G lanes of a channel), lazily raised
+// running shift, E = 2^(x - c + bias) split into bf16 hi (truncated) and lo
+// (the rounded remainder) -> E^T buffers.  FULL: every key of the tile is < T.
+template <int D, int NW, bool FULL>
+__device__ __forceinline__ void tilt_tile(const Smem<D, NW>& sm, int tt, int k0, int T, int wave,
+                                          int lane) {
+  using C = Cfg<D, NW>;
+  const int jj = lane % C::CPW, g = lane / C::CPW;
+  const int j = wave * C::CPW + jj;
+  const float bl = sm.bl()[j];
+  const unsigned char* sv = sm.v(tt & 1) + j * 2;
+  float v[C::RPL][4];
+  float vmax = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < C::RPL; ++u) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int key = 4 * (g + C::G * u) + b;
+      v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + key * C::KROW * 2);
+      if (FULL || k0 + key < T) vmax = fmaxf(vmax, v[u][b]);
+    }
+  }
+#pragma unroll
+  for (int o = C::CPW; o < 64; o <<= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
+  const float mx = vmax * bl;  // bl > 0: max of beta*v*log2e
+  const float cold = (tt == 0) ? -INFINITY : sm.c((tt - 1) & 1)[j];
+  const float cnew = (mx > cold + kColLag) ? mx : cold;
+  const float sh = kBias - cnew;
+  unsigned char* eh = sm.eh(tt & 1) + j * C::EROW * 2;
+  unsigned char* el = sm.el(tt & 1) + j * C::EROW * 2;
+#pragma unroll
+  for (int u = 0; u < C::RPL; ++u) {
+    const int key0 = 4 * (g + C::G * u);
+    float e[4], lo[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      e[b] = exp2_hw(fmaf(v[u][b], bl, sh));
+      if (!FULL && k0 + key0 + b >= T) e[b] = 0.f;
+      lo[b] = e[b] - __uint_as_float(__float_as_uint(e[b]) & 0xffff0000u);
+    }
+    const u32x2 hi2 = {pack_hi16(e[0], e[1]), pack_hi16(e[2], e[3])};
+    const bf16x2 l01 = to_bf16x2(lo[0], lo[1]), l23 = to_bf16x2(lo[2], lo[3]);
+    const u32x2 lo2 = {__builtin_bit_cast(unsigned, l01), __builtin_bit_cast(unsigned, l23)};
+    *reinterpret_cast<u32x2*>(eh + e_pos(key0) * 2) = hi2;
+    *reinterpret_cast<u32x2*>(el + e_pos(key0) * 2) = lo2;
+  }
+  if (g == 0) {
+    sm.c(tt & 1)[j] = cnew;
+    sm.g(tt & 1)[j] = exp2_hw(cold - cnew);
+  }
+  const bool rose = __any(cnew != cold);
+  if (lane == 0) sm.rose(tt & 1)[wave] = rose ? 1 : 0;
+}
+
+// Direct global -> LDS copy of one K or V tile (rows k0 .. k0+63, padded rows).
+// Wave w writes 1 KiB blocks w, w+NW, ...; lane l of a block fills slot
+// 64*blk + l, i.e. row slot/SPR, chunk slot%SPR (the pad chunk re-reads chunk
+// 0).  Rows at or past T are clamped to T-1: their keys are masked anyway.
+template <int D, int NW>
+__device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned char* dst, int k0,
+                                          int T, int wave, int lane) {
+  using C = Cfg<D, NW>;
+#pragma unroll
+  for (int u = 0; u < C::BPW; ++u) {
+    const int blk = wave + NW * u;
+    if (C::BLOCKS % NW == 0 || blk < C::BLOCKS) {
+      const int slot = blk * 64 + lane;
+      const int row = slot / C::SPR, chunk = slot % C::SPR;
+      const int r = min(k0 + row, T - 1);
+      const bf16* g = src + (size_t)r * D + (chunk < D / 8 ? chunk * 8 : 0);
+      __builtin_amdgcn_global_load_lds(g, dst + blk * 1024, 16, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ beta, float* __restrict__ out, int H, int T, int nqb,
     int nbh) {
   using C = Cfg<D, NW>;
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16* sK = reinterpret_cast<bf16*>(smem);
-  bf16* sV = sK + C::BK * C::KROW;
-  bf16* sEh = sV + C::BK * D;
-  bf16* sEl = sEh + D * C::EROW;
-  float* sC = reinterpret_cast<float*>(sEl + D * C::EROW);  // running column shift
-  float* sBl = sC + D;                                      // beta * log2(e)
-  float* sInv = sBl + D;                                    // 1 / (beta * log2(e))
-  float* sG = sInv + D;                                     // column rescale, this tile
-  float* sPart = sG + D;                                    // partial column maxima
-  float* sCw = sPart + C::NPART * D;  // column shift each wave's accumulator ends on
-  int* sRose = reinterpret_cast<int*>(sCw + NW * D);
+  const Smem<D, NW> sm{smem};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int n = lane & 31;   // query column of this lane in the 32x32 blocks
   const int hl = lane >> 5;  // lane half
+  // The two waves sharing a SIMD (w and w + NW/2) run their phases in
+  // opposite order so that one's vector work overlaps the other's MFMAs.
+  const bool tilt_first = wave >= NW / 2;
 
   const int bid = blockIdx.x;
   const int qb = nqb - 1 - bid / nbh;  // longest causal extent first
@@ -135,14 +252,23 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
 
   for (int j = tid; j < D; j += C::NT) {
     const float bl = beta[h * D + j] * kLog2e;
-    sBl[j] = bl;
-    sInv[j] = 1.f / bl;
-    sC[j] = -INFINITY;
+    sm.bl()[j] = bl;
+    sm.inv()[j] = 1.f / bl;
   }
 
   const int wq0 = q0 + wave * 32;  // first query row of this wave
   const int tq = wq0 + n;          // this lane's query row
   const bool wave_live = wq0 < T;
+  const int qlast = min(q0 + C::BQ, T) - 1;
+  const int ntiles = qlast / C::BK + 1;
+  // Last tile this wave multiplies into its accumulator.  Later tiles may still
+  // raise the shared column shift; the wave keeps the shift its accumulator
+  // was last rescaled to (cw) instead of rescaling for tiles it skips.
+  const int wlast = min((wq0 + 31) / C::BK, ntiles - 1);
+
+  load_tile<D, NW>(Kh, sm.k(0), 0, T, wave, lane);
+  load_tile<D, NW>(Vh, sm.v(0), 0, T, wave, lane);
+  if (ntiles > 1) load_tile<D, NW>(Vh, sm.v(1), C::BK, T, wave, lane);
 
   bf16x8 qf[C::NKS];
 #pragma unroll
@@ -151,6 +277,11 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     qf[ks] = (tq < T) ? *reinterpret_cast<const bf16x8*>(Qh + (size_t)tq * D + ks * 16 + hl * 8)
                       : z;
   }
+  wait_vmem();
+  __syncthreads();
+  if (C::BK <= T) tilt_tile<D, NW, true>(sm, 0, 0, T, wave, lane);
+  else tilt_tile<D, NW, false>(sm, 0, 0, T, wave, lane);
+  __syncthreads();
 
   f32x16 acc[C::NCB];
 #pragma unroll
@@ -158,97 +289,53 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   float m = -INFINITY;  // running row max (log2 units), shared by the lane pair
   float l = 0.f;        // this lane's half of the row sum
   const float scale2 = kLog2e / sqrtf((float)D);
-
-  const int qlast = min(q0 + C::BQ, T) - 1;
-  const int ntiles = qlast / C::BK + 1;
-  // Last tile this wave multiplies into its accumulator.  Later tiles may still
-  // raise the shared column shift; the wave keeps the shift its accumulator
-  // was last rescaled to (sCw) instead of rescaling for tiles it skips.
-  const int wlast = min((wq0 + 31) / C::BK, ntiles - 1);
+  const bf16x2 ones = to_bf16x2(1.f, 1.f);
+  const int kofs = n * C::KROW * 2 + hl * 16;  // lane part of K fragment addresses
+  const int eofs = n * C::EROW * 2 + hl * 16;  // lane part of E fragment addresses
 
   for (int kt = 0; kt < ntiles; ++kt) {
     const int k0 = kt * C::BK;
+    const int cur = kt & 1;
+    const bool more1 = kt + 1 < ntiles, more2 = kt + 2 < ntiles;
+    if (more1) load_tile<D, NW>(Kh, sm.k(cur ^ 1), k0 + C::BK, T, wave, lane);
+    if (more2) load_tile<D, NW>(Vh, sm.v(cur), k0 + 2 * C::BK, T, wave, lane);
 
-    // ---- K and V tile: HBM -> LDS (16-byte vectors; rows past T are zero)
-    constexpr int CH = D / 8;
-    for (int c = tid; c < C::BK * CH; c += C::NT) {
-      const int r = c / CH, cc = c % CH;
-      bf16x8 kv = {}, vv = {};
-      if (k0 + r < T) {
-        kv = *reinterpret_cast<const bf16x8*>(Kh + (size_t)(k0 + r) * D + cc * 8);
-        vv = *reinterpret_cast<const bf16x8*>(Vh + (size_t)(k0 + r) * D + cc * 8);
-      }
-      *reinterpret_cast<bf16x8*>(sK + r * C::KROW + cc * 8) = kv;
-      *reinterpret_cast<bf16x8*>(sV + r * D + cc * 8) = vv;
+    const bool next_full = k0 + 2 * C::BK <= T;
+    if (tilt_first && more1) {
+      if (next_full) tilt_tile<D, NW, true>(sm, kt + 1, k0 + C::BK, T, wave, lane);
+      else tilt_tile<D, NW, false>(sm, kt + 1, k0 + C::BK, T, wave, lane);
     }
-    if (tid == 0) *sRose = 0;
-    __syncthreads();
 
-    // ---- tilt: column max, running shift, E = 2^(x - c + bias) as bf16 hi/lo
-    {
-      const int j = tid % D, part = tid / D;
-      const float bl = sBl[j];
-      const float cold = sC[j];
-      float xs[C::KPP];
-      float mx = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < C::KPP; ++r) {
-        const int key = part * C::KPP + r;
-        xs[r] = (float)sV[key * D + j] * bl;
-        if (k0 + key < T) mx = fmaxf(mx, xs[r]);
-      }
-      sPart[part * D + j] = mx;
-      __syncthreads();
-      float tmx = sPart[j];
-#pragma unroll
-      for (int p = 1; p < C::NPART; ++p) tmx = fmaxf(tmx, sPart[p * D + j]);
-      const float cnew = (tmx > cold + kColLag) ? tmx : cold;
-      const float sh = kBias - cnew;
-#pragma unroll
-      for (int r = 0; r < C::KPP; ++r) {
-        const int key = part * C::KPP + r;
-        const float e = (k0 + key < T) ? exp2_hw(xs[r] + sh) : 0.f;
-        const bf16 hi = (bf16)e;
-        const bf16 lo = (bf16)(e - (float)hi);
-        sEh[j * C::EROW + e_pos(key)] = hi;
-        sEl[j * C::EROW + e_pos(key)] = lo;
-      }
-      if (part == 0) {
-        sG[j] = exp2_hw(cold - cnew);
-        if (cnew != cold) *sRose = 1;
-        sC[j] = cnew;
-      }
-    }
-    __syncthreads();
-
-    // ---- per wave: scores, online softmax, tilted product
     if (wave_live && k0 <= wq0 + 31) {
-      f32x16 sacc[2] = {f32x16{}, f32x16{}};
+      const unsigned char* sk = sm.k(cur) + kofs;
+      f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int ks = 0; ks < C::NKS; ++ks) {
+        const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(sk + ks * 32);
+        const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(sk + 32 * C::KROW * 2 + ks * 32);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], s1, 0, 0, 0);
+      }
+      f32x16 sacc[2] = {s0, s1};
+      // scores stay raw (q.k); scale2 > 0 so the row max commutes with it
+      const bool need_mask = (k0 + C::BK - 1 > wq0) || (k0 + C::BK > T);
+      if (need_mask) {
 #pragma unroll
-        for (int ks = 0; ks < C::NKS; ++ks) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8*>(sK + (kb * 32 + n) * C::KROW + ks * 16 + hl * 8);
-          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sacc[kb], 0, 0, 0);
+        for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = k0 + kb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
+            if (key > tq || key >= T) sacc[kb][i] = -INFINITY;
+          }
         }
       }
-      const bool need_mask = (k0 + C::BK - 1 > wq0) || (k0 + C::BK > T);
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float s = sacc[kb][i] * scale2;
-          if (need_mask) {
-            const int key = k0 + kb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
-            if (key > tq || key >= T) s = -INFINITY;
-          }
-          sacc[kb][i] = s;
-          mx = fmaxf(mx, s);
-        }
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
       }
-      mx = fmaxf(mx, other_half(mx));
+      mx = fmaxf(mx, other_half(mx)) * scale2;
       const float mnew = (mx > m + kRowLag) ? mx : m;
       if (__any(mnew != m)) {
         const float alpha = exp2_hw(m - mnew);
@@ -259,54 +346,73 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
       }
 
       bf16x8 pf[4];
-      const bf16x2 ones = to_bf16x2(1.f, 1.f);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const int kb = ks >> 1, s0 = (ks & 1) * 8;
+        const int kb = ks >> 1, s0i = (ks & 1) * 8;
 #pragma unroll
         for (int u = 0; u < 8; u += 2) {
-          const bf16x2 p2 = to_bf16x2(exp2_hw(sacc[kb][s0 + u] - m),
-                                      exp2_hw(sacc[kb][s0 + u + 1] - m));
+          const bf16x2 p2 = to_bf16x2(exp2_hw(fmaf(sacc[kb][s0i + u], scale2, -m)),
+                                      exp2_hw(fmaf(sacc[kb][s0i + u + 1], scale2, -m)));
           pf[ks][u] = p2[0];
           pf[ks][u + 1] = p2[1];
           l = dot2_bf16(p2, ones, l);
         }
       }
 
-      if (*sRose) {
+      const i32x4* rf = reinterpret_cast<const i32x4*>(sm.rose(cur));
+      i32x4 any4 = rf[0];
+#pragma unroll
+      for (int w = 1; w < NW / 4; ++w) any4 |= rf[w];
+      if (any4[0] | any4[1] | any4[2] | any4[3]) {
+        const float* gcol = sm.g(cur);
 #pragma unroll
         for (int cb = 0; cb < C::NCB; ++cb) {
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
-            const f32x4 gg = *reinterpret_cast<const f32x4*>(sG + cb * 32 + g * 8 + hl * 4);
+            const f32x4 gg = *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
 #pragma unroll
             for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
           }
         }
       }
 
+      const unsigned char* seh = sm.eh(cur) + eofs;
+      const unsigned char* sel = sm.el(cur) + eofs;
 #pragma unroll
-      for (int cb = 0; cb < C::NCB; ++cb) {
+      for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const int off = (cb * 32 + n) * C::EROW + ks * 16 + hl * 8;
-          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sEh + off);
-          const bf16x8 al = *reinterpret_cast<const bf16x8*>(sEl + off);
+        for (int cb = 0; cb < C::NCB; ++cb) {
+          const int off = cb * 32 * C::EROW * 2 + ks * 32;
+          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(seh + off);
+          const bf16x8 al = *reinterpret_cast<const bf16x8*>(sel + off);
           acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, pf[ks], acc[cb], 0, 0, 0);
           acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, pf[ks], acc[cb], 0, 0, 0);
         }
       }
       if (kt == wlast) {
-        for (int j = lane; j < D; j += 64) sCw[wave * D + j] = sC[j];
+        const float* cc = sm.c(cur);
+        for (int j = lane; j < D; j += 64) sm.cw(wave)[j] = cc[j];
       }
     }
+
+    if (!tilt_first && more1) {
+      if (next_full) tilt_tile<D, NW, true>(sm, kt + 1, k0 + C::BK, T, wave, lane);
+      else tilt_tile<D, NW, false>(sm, kt + 1, k0 + C::BK, T, wave, lane);
+    }
+    wait_vmem();
     __syncthreads();
   }
 
   if (!wave_live) return;
 
-  // ---- epilogue: o = (log2 acc - log2 l + c - bias) / (beta log2 e)
-  const float ll = log2_hw(l + other_half(l));
+  // ---- epilogue: o = (log2 acc - log2 l + c - bias) / (beta log2 e).  The
+  // logarithms are split into exponent and mantissa so the bias and the
+  // integer parts cancel exactly (tiny beta amplifies any error here).
+  const float lt = l + other_half(l);
+  int el;
+  const float fl = log2_hw(frexpf(lt, &el));
+  const float* cw = sm.cw(wave);
+  const float* inv = sm.inv();
   uint64_t flags = 0;
 #pragma unroll
   for (int cb = 0; cb < C::NCB; ++cb) {
@@ -317,7 +423,9 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float a = acc[cb][g * 4 + e];
-        o[e] = ((log2_hw(a) - kBias) - ll + sCw[wave * D + ch0 + e]) * sInv[ch0 + e];
+        int ea;
+        const float fa = log2_hw(frexpf(a, &ea));
+        o[e] = ((float)(ea - el - (int)kBias) + (fa - fl) + cw[ch0 + e]) * inv[ch0 + e];
         if (!(a >= kUnderflow) && tq < T) flags |= 1ull << (cb * 16 + g * 4 + e);
       }
       if (tq < T) *reinterpret_cast<f32x4*>(Oh + (size_t)tq * D + ch0) = o;
@@ -331,12 +439,12 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     const int src = __builtin_ctzll(who);
     const uint32_t flo = __builtin_amdgcn_readlane((uint32_t)flags, src);
     const uint32_t fhi = __builtin_amdgcn_readlane((uint32_t)(flags >> 32), src);
-    const uint64_t fl = ((uint64_t)fhi << 32) | flo;
-    const int e = __builtin_ctzll(fl);
+    const uint64_t fl64 = ((uint64_t)fhi << 32) | flo;
+    const int e = __builtin_ctzll(fl64);
     const int t = __builtin_amdgcn_readlane(tq, src);
     const int cb = e >> 4, i = e & 15;
     const int ch = cb * 32 + (i >> 2) * 8 + (src >> 5) * 4 + (i & 3);
-    const float o = exact_read<D>(Qh, Kh, Vh, t, ch, scale2, sBl[ch]);
+    const float o = exact_read<D>(Qh, Kh, Vh, t, ch, scale2, sm.bl()[ch]);
     if (lane == src) {
       flags &= ~(1ull << e);
       Oh[(size_t)t * D + ch] = o;
