@@ -86,9 +86,14 @@ int fem_softmax_fwd(const void* Q, const void* K, const void* V,
  *   beta    : [H, d_v] float32, > 0
  *   out     : [B, H, T, d_v] float32
  *   d_k, d_v: 64 (both)
- *   chunk   : scan chunk length, 16, 32, 64 or 128.  It only schedules the
- *             work: the result does not depend on it beyond rounding.
+ *   chunk   : length of the intra-chunk (quadratic) block of the scan; 64.
+ *             It only schedules the work: the result does not depend on it
+ *             beyond rounding.  Other values return FEM_ERR_UNSUPPORTED.
  *   dtype   : FEM_DTYPE_BF16
+ *
+ * The scan keeps per-segment states in a stream-ordered workspace
+ * (hipMallocAsync / hipFreeAsync on `stream`, 16.9 KiB per 512 tokens per
+ * (b, h)); an allocation failure returns FEM_ERR_HIP.
  *
  * Returns a fem_status.
  */

@@ -52,7 +52,7 @@ extern "C" int fem_linear_fwd(const void* Q, const void* K, const void* V, const
   if (!sizes_ok(B, H, T, d_k) || !sizes_ok(B, H, T, d_v)) return FEM_ERR_SHAPE;
   if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
   if (d_k != 64 || d_v != 64) return FEM_ERR_UNSUPPORTED;
-  if (chunk != 16 && chunk != 32 && chunk != 64 && chunk != 128) return FEM_ERR_UNSUPPORTED;
+  if (chunk != 64) return FEM_ERR_UNSUPPORTED;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return FEM_ERR_ALIGN;
   const hipError_t e = fem::launch_linear_bf16(Q, K, V, beta, out, B, H, T, d_k, d_v, chunk, stream);
   if (e == hipErrorNotSupported) return FEM_ERR_UNSUPPORTED;

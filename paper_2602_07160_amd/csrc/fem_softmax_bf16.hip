@@ -31,13 +31,17 @@
 //
 // Work decomposition: one workgroup of NW waves owns BQ = 32*NW query rows of
 // one (b, h); each wave owns 32 rows for the products and D/NW channels for
-// the tilt.  Software pipeline, one barrier per 64-key tile: while a wave
-// multiplies tile k (K, E of tile k in LDS buffer k%2) it also tilts its own
-// channels of tile k+1 (V of tile k+1 -> E buffer (k+1)%2; the running column
-// maximum needs no cross-wave reduction because a channel is owned by one
-// wave), and its prefetched global loads for K(k+1) and V(k+2) are parked in
-// the free buffers.  Workgroups run longest causal extent first; workgroup i
-// of a causal level covers head i, so a head's workgroups share an XCD.
+// the tilt (so the running column maximum needs no cross-wave reduction).
+//
+// Schedule.  A wave cannot issue vector instructions while its own MFMAs run,
+// but the two waves sharing a SIMD can overlap each other's.  So every wave
+// alternates a matrix-only block M(k) = {PV(k-1), QK(k)} with a vector-only
+// block {softmax(k) -> P(k), tilt of its channels of tile k}, and the two
+// waves of a SIMD run them in opposite halves of each iteration (two barriers
+// per 64-key tile).  K(k+1) and V(k+1) stream straight into the free LDS
+// buffers (global_load_lds_dwordx4) during iteration k; K, V and E are double
+// buffered.  Workgroups run longest causal extent first; workgroup i of a
+// causal level covers head i, so a head's workgroups share an XCD.
 
 #include "fem_device.h"
 #include "fem_internal.h"
@@ -235,9 +239,11 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const int wave = tid >> 6;
   const int n = lane & 31;   // query column of this lane in the 32x32 blocks
   const int hl = lane >> 5;  // lane half
-  // The two waves sharing a SIMD (w and w + NW/2) run their phases in
-  // opposite order so that one's vector work overlaps the other's MFMAs.
-  const bool tilt_first = wave >= NW / 2;
+  // Waves w and w + NW/2 share a SIMD.  Group A (w < NW/2) runs its matrix
+  // block in the first half of every iteration and its vector block in the
+  // second; group B the other way round, so one wave's vector work overlaps
+  // the other's MFMAs.
+  const bool grpB = wave >= NW / 2;
 
   const int bid = blockIdx.x;
   const int qb = nqb - 1 - bid / nbh;  // longest causal extent first
@@ -264,12 +270,10 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   // Last tile this wave multiplies into its accumulator.  Later tiles may still
   // raise the shared column shift; the wave keeps the shift its accumulator
   // was last rescaled to (cw) instead of rescaling for tiles it skips.
-  const int wlast = min((wq0 + 31) / C::BK, ntiles - 1);
+  const int wlast = wave_live ? min((wq0 + 31) / C::BK, ntiles - 1) : -1;
 
   load_tile<D, NW>(Kh, sm.k(0), 0, T, wave, lane);
   load_tile<D, NW>(Vh, sm.v(0), 0, T, wave, lane);
-  if (ntiles > 1) load_tile<D, NW>(Vh, sm.v(1), C::BK, T, wave, lane);
-
   bf16x8 qf[C::NKS];
 #pragma unroll
   for (int ks = 0; ks < C::NKS; ++ks) {
@@ -279,13 +283,12 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   }
   wait_vmem();
   __syncthreads();
-  if (C::BK <= T) tilt_tile<D, NW, true>(sm, 0, 0, T, wave, lane);
-  else tilt_tile<D, NW, false>(sm, 0, 0, T, wave, lane);
-  __syncthreads();
 
   f32x16 acc[C::NCB];
 #pragma unroll
   for (int cb = 0; cb < C::NCB; ++cb) acc[cb] = f32x16{};
+  f32x16 sacc[2] = {f32x16{}, f32x16{}};  // scores: QK(k) -> softmax(k)
+  bf16x8 pf[4] = {};                      // probabilities: softmax(k) -> PV(k)
   float m = -INFINITY;  // running row max (log2 units), shared by the lane pair
   float l = 0.f;        // this lane's half of the row sum
   const float scale2 = kLog2e / sqrtf((float)D);
@@ -293,21 +296,49 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const int kofs = n * C::KROW * 2 + hl * 16;  // lane part of K fragment addresses
   const int eofs = n * C::EROW * 2 + hl * 16;  // lane part of E fragment addresses
 
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int k0 = kt * C::BK;
-    const int cur = kt & 1;
-    const bool more1 = kt + 1 < ntiles, more2 = kt + 2 < ntiles;
-    if (more1) load_tile<D, NW>(Kh, sm.k(cur ^ 1), k0 + C::BK, T, wave, lane);
-    if (more2) load_tile<D, NW>(Vh, sm.v(cur), k0 + 2 * C::BK, T, wave, lane);
-
-    const bool next_full = k0 + 2 * C::BK <= T;
-    if (tilt_first && more1) {
-      if (next_full) tilt_tile<D, NW, true>(sm, kt + 1, k0 + C::BK, T, wave, lane);
-      else tilt_tile<D, NW, false>(sm, kt + 1, k0 + C::BK, T, wave, lane);
+  // ---- matrix block of iteration k: PV(k-1) then QK(k)
+  auto mblock = [&](int k) {
+    const int j = k - 1;
+    if (j >= 0 && j <= wlast) {
+      const int pb = j & 1;
+      if (j > 0) {  // tile 0 always raises the shift, but the accumulator is still zero
+        const i32x4* rf = reinterpret_cast<const i32x4*>(sm.rose(pb));
+        i32x4 any4 = rf[0];
+#pragma unroll
+        for (int w = 1; w < NW / 4; ++w) any4 |= rf[w];
+        if (any4[0] | any4[1] | any4[2] | any4[3]) {
+          const float* gcol = sm.g(pb);
+#pragma unroll
+          for (int cb = 0; cb < C::NCB; ++cb) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const f32x4 gg = *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
+            }
+          }
+        }
+      }
+      const unsigned char* seh = sm.eh(pb) + eofs;
+      const unsigned char* sel = sm.el(pb) + eofs;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+        for (int cb = 0; cb < C::NCB; ++cb) {
+          const int off = cb * 32 * C::EROW * 2 + ks * 32;
+          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(seh + off);
+          const bf16x8 al = *reinterpret_cast<const bf16x8*>(sel + off);
+          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, pf[ks], acc[cb], 0, 0, 0);
+          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, pf[ks], acc[cb], 0, 0, 0);
+        }
+      }
+      if (j == wlast) {
+        const float* cc = sm.c(pb);
+        for (int c = lane; c < D; c += 64) sm.cw(wave)[c] = cc[c];
+      }
     }
-
-    if (wave_live && k0 <= wq0 + 31) {
-      const unsigned char* sk = sm.k(cur) + kofs;
+    if (k <= wlast) {
+      const unsigned char* sk = sm.k(k & 1) + kofs;
       f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
       for (int ks = 0; ks < C::NKS; ++ks) {
@@ -316,10 +347,17 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
         s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], s0, 0, 0, 0);
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], s1, 0, 0, 0);
       }
-      f32x16 sacc[2] = {s0, s1};
+      sacc[0] = s0;
+      sacc[1] = s1;
+    }
+  };
+
+  // ---- vector block: softmax of tile js (-> P, row rescale), tilt of tile jt
+  auto vblock = [&](int js, int jt) {
+    if (js >= 0 && js <= wlast) {
+      const int k0 = js * C::BK;
       // scores stay raw (q.k); scale2 > 0 so the row max commutes with it
-      const bool need_mask = (k0 + C::BK - 1 > wq0) || (k0 + C::BK > T);
-      if (need_mask) {
+      if ((k0 + C::BK - 1 > wq0) || (k0 + C::BK > T)) {
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -344,8 +382,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
         for (int cb = 0; cb < C::NCB; ++cb) acc[cb] *= alpha;
         m = mnew;
       }
-
-      bf16x8 pf[4];
+      float l2 = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int kb = ks >> 1, s0i = (ks & 1) * 8;
@@ -355,49 +392,31 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
                                       exp2_hw(fmaf(sacc[kb][s0i + u + 1], scale2, -m)));
           pf[ks][u] = p2[0];
           pf[ks][u + 1] = p2[1];
-          l = dot2_bf16(p2, ones, l);
+          if (u & 2) l2 = dot2_bf16(p2, ones, l2);
+          else l = dot2_bf16(p2, ones, l);
         }
       }
-
-      const i32x4* rf = reinterpret_cast<const i32x4*>(sm.rose(cur));
-      i32x4 any4 = rf[0];
-#pragma unroll
-      for (int w = 1; w < NW / 4; ++w) any4 |= rf[w];
-      if (any4[0] | any4[1] | any4[2] | any4[3]) {
-        const float* gcol = sm.g(cur);
-#pragma unroll
-        for (int cb = 0; cb < C::NCB; ++cb) {
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 gg = *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
-          }
-        }
-      }
-
-      const unsigned char* seh = sm.eh(cur) + eofs;
-      const unsigned char* sel = sm.el(cur) + eofs;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-        for (int cb = 0; cb < C::NCB; ++cb) {
-          const int off = cb * 32 * C::EROW * 2 + ks * 32;
-          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(seh + off);
-          const bf16x8 al = *reinterpret_cast<const bf16x8*>(sel + off);
-          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, pf[ks], acc[cb], 0, 0, 0);
-          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, pf[ks], acc[cb], 0, 0, 0);
-        }
-      }
-      if (kt == wlast) {
-        const float* cc = sm.c(cur);
-        for (int j = lane; j < D; j += 64) sm.cw(wave)[j] = cc[j];
-      }
+      l += l2;
     }
+    if (jt < ntiles) {
+      if ((jt + 1) * C::BK <= T) tilt_tile<D, NW, true>(sm, jt, jt * C::BK, T, wave, lane);
+      else tilt_tile<D, NW, false>(sm, jt, jt * C::BK, T, wave, lane);
+    }
+  };
 
-    if (!tilt_first && more1) {
-      if (next_full) tilt_tile<D, NW, true>(sm, kt + 1, k0 + C::BK, T, wave, lane);
-      else tilt_tile<D, NW, false>(sm, kt + 1, k0 + C::BK, T, wave, lane);
+  for (int k = 0; k <= ntiles; ++k) {
+    if (k + 1 < ntiles) {
+      load_tile<D, NW>(Kh, sm.k((k + 1) & 1), (k + 1) * C::BK, T, wave, lane);
+      load_tile<D, NW>(Vh, sm.v((k + 1) & 1), (k + 1) * C::BK, T, wave, lane);
+    }
+    if (!grpB) {
+      mblock(k);
+      __syncthreads();
+      vblock(k, k);
+    } else {
+      vblock(k - 1, k);
+      __syncthreads();
+      mblock(k);
     }
     wait_vmem();
     __syncthreads();

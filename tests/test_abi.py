@@ -77,5 +77,6 @@ def test_linear_validation(lib):
     assert ln(lib, dk=32) == UNSUPPORTED
     assert ln(lib, dv=128) == UNSUPPORTED
     assert ln(lib, chunk=48) == UNSUPPORTED
+    assert ln(lib, chunk=32) == UNSUPPORTED
     assert ln(lib, dt=F32) == UNSUPPORTED
     assert ln(lib, v=A + 2) == ALIGN

@@ -1,0 +1,118 @@
+"""GPU parity of fem_linear_fwd (HIP chunked scan, through the C ABI) against
+the float64 oracle.  Tolerance: max abs error <= 2e-2 (bf16 inputs)."""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_07160_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def run(fem, q, k, v, beta, chunk=64):
+    dev = torch.device("cuda:0")
+    out = fem.fem_linear_fwd(q.to(dev), k.to(dev), v.to(dev), beta.to(dev), chunk=chunk)
+    torch.cuda.synchronize()
+    return out.cpu().double().numpy()
+
+
+def ref(q, k, v, beta, rows=None):
+    return oracle.fem_linear(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                             beta.double().numpy(), rows=rows)
+
+
+def check(got, want, tol, what):
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got - want).max()
+    say(f"{what}: max abs err {err:.3e} (tol {tol})")
+    assert err <= tol, f"{what}: max abs err {err} > {tol}"
+
+
+def test_workload5_full_size_sampled(fem):
+    say("workload 5: linear bf16 B4 H16 T8192 d64 chunk 64, seed 47, sampled rows")
+    q, k, v, b = inputs.make_inputs(5)
+    got = run(fem, q, k, v, b)
+    rng = np.random.default_rng(5)
+    rows = sorted(set([0, 1, 63, 64, 511, 512, 513, 4095, 8190, 8191]) |
+                  set(int(x) for x in rng.integers(0, 8192, 14)))
+    rows = np.array(rows)
+    for bb, hh in [(0, 0), (1, 9), (3, 15)]:
+        want = oracle.fem_linear(q[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                 k[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                 v[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                 b[hh:hh + 1].double().numpy(), rows=rows)[0, 0]
+        check(got[bb, hh, rows], want, TOL, f"w5 b{bb} h{hh}")
+
+
+def test_workload5_reduced_full(fem):
+    say("workload 5 recipe, reduced: B1 H3 T1300 (3 segments, ragged), full oracle")
+    q, k, v, b = inputs.make_inputs(5, B=1, H=3, T=1300)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL, "w5-reduced")
+
+
+@pytest.mark.parametrize("T", [1, 2, 63, 64, 65, 511, 512, 513, 1025])
+def test_linear_shapes(fem, T):
+    say(f"linear shape B2 H2 T{T} d64")
+    q, k, v, b = inputs.draw(4000 + T, 2, 2, T, 64, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL, f"linear T{T}")
+
+
+@pytest.mark.parametrize("beta", [1e-2, 0.1, 1.0, 16.0])
+def test_linear_beta_extremes(fem, beta):
+    say(f"linear constant beta {beta}: B1 H2 T700")
+    q, k, v, _ = inputs.draw(4100, 1, 2, 700, 64, dtype="bf16")
+    b = torch.full((2, 64), beta, dtype=torch.float32)
+    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL, f"linear beta={beta}")
+
+
+def test_linear_equal_keys_is_logcumsumexp(fem):
+    say("linear all keys equal (uniform prior) vs torch.logcumsumexp: B1 H2 T600")
+    q, k, v, b = inputs.draw(4200, 1, 2, 600, 64, dtype="bf16")
+    k = k[:, :, :1].expand(-1, -1, 600, -1).contiguous()
+    got = run(fem, q, k, v, b)
+    x = v.double() * b.double()[None, :, None, :]
+    want = (torch.logcumsumexp(x, dim=2) - torch.log(torch.arange(1, 601, dtype=torch.float64))[:, None]) \
+        / b.double()[None, :, None, :]
+    check(got, want.numpy(), TOL, "linear uniform prior")
+
+
+def test_linear_underflow_repair(fem):
+    say("linear forced underflow: v=-5 then +5 at key 20 in the same chunk, beta=16, T200")
+    q, k, _, _ = inputs.draw(4300, 1, 1, 200, 64, dtype="bf16")
+    v = torch.full((1, 1, 200, 64), -5.0)
+    v[:, :, 20] = 5.0
+    v[:, :, 30:] = torch.randn(1, 1, 170, 64, generator=torch.Generator().manual_seed(1))
+    v = v.to(torch.bfloat16)
+    b = torch.full((1, 64), 16.0)
+    got = run(fem, q, k, v, b)
+    check(got, ref(q, k, v, b), TOL, "linear underflow repair")
+
+
+def test_linear_deterministic(fem):
+    say("linear determinism: B2 H2 T1500")
+    q, k, v, b = inputs.draw(4400, 2, 2, 1500, 64, dtype="bf16")
+    assert np.array_equal(run(fem, q, k, v, b), run(fem, q, k, v, b))
+
+
+def test_linear_rejects_unsupported(fem):
+    say("linear argument errors")
+    dev = torch.device("cuda:0")
+    q = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16, device=dev)
+    b = torch.ones(1, 64, device=dev)
+    with pytest.raises(fem.FemError) as e:
+        fem.fem_linear_fwd(q, q, q, b, chunk=32)
+    assert e.value.status == 3
+    q32 = torch.zeros(1, 1, 8, 32, dtype=torch.bfloat16, device=dev)
+    with pytest.raises(fem.FemError):
+        fem.fem_linear_fwd(q32, q32, q32, torch.ones(1, 32, device=dev))
