@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-linear", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one device-to-device copy of this many MiB (a known-size "
+                         "kernel for calibrating hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the FEM read is benchmarked on a single MI355X "
@@ -113,6 +116,12 @@ def main():
 
     dev = torch.device("cuda:0")
     binding.load()
+    if args.calib_copy_mib > 0:
+        src = torch.ones(args.calib_copy_mib << 18, device=dev, dtype=torch.float32)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     w = inputs.WORKLOADS[3]
     q, k, v, beta = inputs.make_inputs(3)
