@@ -91,9 +91,11 @@ int fem_softmax_fwd(const void* Q, const void* K, const void* V,
  *             beyond rounding.  Other values return FEM_ERR_UNSUPPORTED.
  *   dtype   : FEM_DTYPE_BF16
  *
- * The scan keeps per-segment states in a stream-ordered workspace
- * (hipMallocAsync / hipFreeAsync on `stream`, 16.9 KiB per 512 tokens per
- * (b, h)); an allocation failure returns FEM_ERR_HIP.
+ * The scan keeps per-segment states in a stream-ordered workspace of
+ * 16.9 KiB per 512 tokens per (b, h), taken from and returned to a
+ * library-owned memory pool of the current device on `stream` (the pool keeps
+ * its memory until the process ends, so repeated calls of one size do not
+ * reach the driver's allocator); an allocation failure returns FEM_ERR_HIP.
  *
  * Returns a fem_status.
  */

@@ -21,4 +21,8 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V,
                               int B, int H, int T, int dk, int dv, int chunk,
                               hipStream_t stream);
 
+// Stream-ordered scratch from a library-owned pool (see fem_workspace.hip).
+hipError_t workspace_alloc(void** p, size_t bytes, hipStream_t stream);
+hipError_t workspace_free(void* p, hipStream_t stream);
+
 }  // namespace fem

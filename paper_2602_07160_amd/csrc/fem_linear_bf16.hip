@@ -404,7 +404,7 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const
   const int nbh = B * H;
   float* ws = nullptr;
   const size_t bytes = (size_t)nbh * nseg * STATE * sizeof(float);
-  hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&ws), bytes, stream);
+  hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
   if (e != hipSuccess) return e;
   if (nseg > 1) {
     hipLaunchKernelGGL(linear_kernel<false>, dim3((unsigned)(nbh * nseg)), dim3(NTH), 0, stream,
@@ -418,7 +418,7 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const
                        reinterpret_cast<const bf16*>(V), beta, out, ws, H, T, nseg);
     e = hipGetLastError();
   }
-  const hipError_t f = hipFreeAsync(ws, stream);
+  const hipError_t f = workspace_free(ws, stream);
   return e != hipSuccess ? e : f;
 }
 

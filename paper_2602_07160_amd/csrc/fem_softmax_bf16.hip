@@ -147,31 +147,64 @@ __device__ __forceinline__ unsigned pack_hi16(float lo_elem, float hi_elem) {
   return __builtin_amdgcn_perm(__float_as_uint(hi_elem), __float_as_uint(lo_elem), 0x07060302u);
 }
 
-// Tilt of tile tt (first key k0) for this wave's CPW channels: column max over
-// the tile (in-lane, then across the G lanes of a channel), lazily raised
-// running shift, E = 2^(x - c + bias) split into bf16 hi (truncated) and lo
-// (the rounded remainder) -> E^T buffers.  FULL: every key of the tile is < T.
-template <int D, int NW, bool FULL>
-__device__ __forceinline__ void tilt_tile(const Smem<D, NW>& sm, int tt, int k0, int T, int wave,
-                                          int lane) {
+// max(x, x of lane ^ o) without going through LDS where the hardware has a
+// lane swap for that distance (v_permlane16_swap / v_permlane32_swap).
+__device__ __forceinline__ float max_xor(float x, int o) {
+  const unsigned u = __float_as_uint(x);
+  if (o == 32) {
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  }
+  if (o == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  }
+  return fmaxf(x, __shfl_xor(x, o));
+}
+
+// Tilt of tile tt (first key k0) for this wave's CPW channels, in two steps so
+// that the LDS reads of V can be issued before unrelated vector work:
+//   tilt_read   : this lane's V values (channel jj, 4-key runs g + G*u);
+//   tilt_finish : column max over the tile (in-lane, then across the G lanes
+//                 of a channel), lazily raised running shift, E = 2^(x - c +
+//                 bias) split into bf16 hi (truncated) and lo (the rounded
+//                 remainder) -> E^T buffers.  FULL: every key of the tile < T.
+template <int D, int NW>
+__device__ __forceinline__ void tilt_read(const Smem<D, NW>& sm, int tt, int wave, int lane,
+                                          float (&v)[Cfg<D, NW>::RPL][4]) {
   using C = Cfg<D, NW>;
   const int jj = lane % C::CPW, g = lane / C::CPW;
   const int j = wave * C::CPW + jj;
-  const float bl = sm.bl()[j];
   const unsigned char* sv = sm.v(tt & 1) + j * 2;
-  float v[C::RPL][4];
-  float vmax = -INFINITY;
 #pragma unroll
   for (int u = 0; u < C::RPL; ++u) {
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const int key = 4 * (g + C::G * u) + b;
       v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + key * C::KROW * 2);
+    }
+  }
+}
+
+template <int D, int NW, bool FULL>
+__device__ __forceinline__ void tilt_finish(const Smem<D, NW>& sm, int tt, int k0, int T,
+                                            int wave, int lane,
+                                            const float (&v)[Cfg<D, NW>::RPL][4]) {
+  using C = Cfg<D, NW>;
+  const int jj = lane % C::CPW, g = lane / C::CPW;
+  const int j = wave * C::CPW + jj;
+  const float bl = sm.bl()[j];
+  float vmax = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < C::RPL; ++u) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int key = 4 * (g + C::G * u) + b;
       if (FULL || k0 + key < T) vmax = fmaxf(vmax, v[u][b]);
     }
   }
 #pragma unroll
-  for (int o = C::CPW; o < 64; o <<= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
+  for (int o = C::CPW; o < 64; o <<= 1) vmax = max_xor(vmax, o);
   const float mx = vmax * bl;  // bl > 0: max of beta*v*log2e
   const float cold = (tt == 0) ? -INFINITY : sm.c((tt - 1) & 1)[j];
   const float cnew = (mx > cold + kColLag) ? mx : cold;
@@ -202,6 +235,15 @@ __device__ __forceinline__ void tilt_tile(const Smem<D, NW>& sm, int tt, int k0,
   if (lane == 0) sm.rose(tt & 1)[wave] = rose ? 1 : 0;
 }
 
+// Whole tilt of tile tt (prologue).
+template <int D, int NW, bool FULL>
+__device__ __forceinline__ void tilt_tile(const Smem<D, NW>& sm, int tt, int k0, int T, int wave,
+                                          int lane) {
+  float v[Cfg<D, NW>::RPL][4];
+  tilt_read<D, NW>(sm, tt, wave, lane, v);
+  tilt_finish<D, NW, FULL>(sm, tt, k0, T, wave, lane, v);
+}
+
 // Direct global -> LDS copy of one K or V tile (rows k0 .. k0+63, padded rows).
 // Wave w writes 1 KiB blocks w, w+NW, ...; lane l of a block fills slot
 // 64*blk + l, i.e. row slot/SPR, chunk slot%SPR (the pad chunk re-reads chunk
@@ -224,6 +266,58 @@ __device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned
 }
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Matrix-only block: PV of the previous tile (if PV) then QK^T of this tile
+// (if QK), as one straight run of MFMAs.  Every MFMA takes its A operand
+// (E^T hi/lo or K) from LDS; the fragments are prefetched RING steps ahead so
+// that LDS latency hides behind the MFMAs already issued.  PV steps alternate
+// the output blocks (independent accumulators) within each hi/lo half.
+template <int D, int NW, bool PV, bool QK>
+__device__ __forceinline__ void mfma_block(f32x16 (&acc)[D / 32], f32x16& s0, f32x16& s1,
+                                           const bf16x8 (&pf)[4], const bf16x8 (&qf)[D / 16],
+                                           const unsigned char* eh, const unsigned char* el,
+                                           const unsigned char* kt) {
+  using C = Cfg<D, NW>;
+  constexpr int NPV = PV ? 4 * 2 * C::NCB : 0;
+  constexpr int NQK = QK ? 2 * C::NKS : 0;
+  constexpr int NS = NPV + NQK;
+  constexpr int RING = 6;
+  auto frag = [&](int s) -> bf16x8 {
+    if (s < NPV) {
+      const int ks = s / (2 * C::NCB), rem = s % (2 * C::NCB);
+      const int lo = rem / C::NCB, cb = rem % C::NCB;
+      const unsigned char* b = lo ? el : eh;
+      return *reinterpret_cast<const bf16x8*>(b + cb * 32 * C::EROW * 2 + ks * 32);
+    }
+    const int t = s - NPV, ks = t >> 1, kb = t & 1;
+    return *reinterpret_cast<const bf16x8*>(kt + kb * 32 * C::KROW * 2 + ks * 32);
+  };
+  bf16x8 ring[RING];
+#pragma unroll
+  for (int s = 0; s < RING; ++s)
+    if (s < NS) ring[s] = frag(s);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const bf16x8 a = ring[s % RING];
+    if (s + RING < NS) ring[s % RING] = frag(s + RING);
+    if (s < NPV) {
+      const int ks = s / (2 * C::NCB), cb = (s % (2 * C::NCB)) % C::NCB;
+      acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[ks], acc[cb], 0, 0, 0);
+    } else {
+      const int t = s - NPV, ks = t >> 1;
+      if (t & 1) s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s1, 0, 0, 0);
+      else s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s0, 0, 0, 0);
+    }
+  }
+  // Pin the order: RING fragment reads up front, then one read ahead per MFMA.
+#pragma unroll
+  for (int s = 0; s < RING; ++s) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    if (s + RING < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+}
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
@@ -299,61 +393,50 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   // ---- matrix block of iteration k: PV(k-1) then QK(k)
   auto mblock = [&](int k) {
     const int j = k - 1;
-    if (j >= 0 && j <= wlast) {
-      const int pb = j & 1;
-      if (j > 0) {  // tile 0 always raises the shift, but the accumulator is still zero
-        const i32x4* rf = reinterpret_cast<const i32x4*>(sm.rose(pb));
-        i32x4 any4 = rf[0];
+    const bool do_pv = j >= 0 && j <= wlast;
+    const bool do_qk = k <= wlast;
+    if (!do_pv && !do_qk) return;
+    const int pb = j & 1;
+    if (do_pv && j > 0) {  // tile 0 always raises the shift, but the accumulator is still zero
+      const i32x4* rf = reinterpret_cast<const i32x4*>(sm.rose(pb));
+      i32x4 any4 = rf[0];
 #pragma unroll
-        for (int w = 1; w < NW / 4; ++w) any4 |= rf[w];
-        if (any4[0] | any4[1] | any4[2] | any4[3]) {
-          const float* gcol = sm.g(pb);
+      for (int w = 1; w < NW / 4; ++w) any4 |= rf[w];
+      if (any4[0] | any4[1] | any4[2] | any4[3]) {
+        const float* gcol = sm.g(pb);
 #pragma unroll
-          for (int cb = 0; cb < C::NCB; ++cb) {
+        for (int cb = 0; cb < C::NCB; ++cb) {
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const f32x4 gg = *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 gg = *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
 #pragma unroll
-              for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
-            }
+            for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
           }
         }
       }
-      const unsigned char* seh = sm.eh(pb) + eofs;
-      const unsigned char* sel = sm.el(pb) + eofs;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-        for (int cb = 0; cb < C::NCB; ++cb) {
-          const int off = cb * 32 * C::EROW * 2 + ks * 32;
-          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(seh + off);
-          const bf16x8 al = *reinterpret_cast<const bf16x8*>(sel + off);
-          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, pf[ks], acc[cb], 0, 0, 0);
-          acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, pf[ks], acc[cb], 0, 0, 0);
-        }
-      }
-      if (j == wlast) {
-        const float* cc = sm.c(pb);
-        for (int c = lane; c < D; c += 64) sm.cw(wave)[c] = cc[c];
-      }
     }
-    if (k <= wlast) {
-      const unsigned char* sk = sm.k(k & 1) + kofs;
-      f32x16 s0 = f32x16{}, s1 = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < C::NKS; ++ks) {
-        const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(sk + ks * 32);
-        const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(sk + 32 * C::KROW * 2 + ks * 32);
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], s1, 0, 0, 0);
-      }
+    const unsigned char* seh = sm.eh(pb & 1) + eofs;
+    const unsigned char* sel = sm.el(pb & 1) + eofs;
+    const unsigned char* sk = sm.k(k & 1) + kofs;
+    f32x16 s0 = f32x16{}, s1 = f32x16{};
+    if (do_pv && do_qk) mfma_block<D, NW, true, true>(acc, s0, s1, pf, qf, seh, sel, sk);
+    else if (do_pv) mfma_block<D, NW, true, false>(acc, s0, s1, pf, qf, seh, sel, sk);
+    else mfma_block<D, NW, false, true>(acc, s0, s1, pf, qf, seh, sel, sk);
+    if (do_qk) {
       sacc[0] = s0;
       sacc[1] = s1;
+    }
+    if (do_pv && j == wlast) {
+      const float* cc = sm.c(pb);
+      for (int c = lane; c < D; c += 64) sm.cw(wave)[c] = cc[c];
     }
   };
 
   // ---- vector block: softmax of tile js (-> P, row rescale), tilt of tile jt
   auto vblock = [&](int js, int jt) {
+    float tv[C::RPL][4];
+    const bool do_tilt = jt < ntiles;
+    if (do_tilt) tilt_read<D, NW>(sm, jt, wave, lane, tv);
     if (js >= 0 && js <= wlast) {
       const int k0 = js * C::BK;
       // scores stay raw (q.k); scale2 > 0 so the row max commutes with it
@@ -398,9 +481,9 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
       }
       l += l2;
     }
-    if (jt < ntiles) {
-      if ((jt + 1) * C::BK <= T) tilt_tile<D, NW, true>(sm, jt, jt * C::BK, T, wave, lane);
-      else tilt_tile<D, NW, false>(sm, jt, jt * C::BK, T, wave, lane);
+    if (do_tilt) {
+      if ((jt + 1) * C::BK <= T) tilt_finish<D, NW, true>(sm, jt, jt * C::BK, T, wave, lane, tv);
+      else tilt_finish<D, NW, false>(sm, jt, jt * C::BK, T, wave, lane, tv);
     }
   };
 
@@ -411,11 +494,9 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     }
     if (!grpB) {
       mblock(k);
-      __syncthreads();
       vblock(k, k);
     } else {
       vblock(k - 1, k);
-      __syncthreads();
       mblock(k);
     }
     wait_vmem();
