@@ -218,7 +218,6 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, const bf16* 
     // mask (key > query), round to bf16, normaliser from the rounded values
     bf16x8 pf[4] = {};
     float den = 0.f;
-    const bf16x2 ones = to_bf16x2(1.f, 1.f);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int kb = ks >> 1, s0 = (ks & 1) * 8;
@@ -233,7 +232,7 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, const bf16* 
         const bf16x2 p2 = to_bf16x2(a0, a1);
         pf[ks][u] = p2[0];
         pf[ks][u + 1] = p2[1];
-        den = dot2_bf16(p2, ones, den);
+        den = add_bf16x2(p2, den);
       }
     }
     // inter-chunk normaliser phi(q)^T z, this lane's half of d_k

@@ -12,8 +12,9 @@
 //     need one v_permlane32_swap and no LDS traffic.
 //   * Online row softmax with a running row max m_t (raised lazily, only when
 //     a tile beats it by kRowLag) and a row sum l_t accumulated from the SAME
-//     bf16-rounded probabilities that feed the product (v_dot2 with ones), so
-//     that rounding P cancels between numerator and normaliser.
+//     bf16-rounded probabilities that feed the product (a small MFMA against
+//     a 0/1 selector), so that rounding P cancels between numerator and
+//     normaliser.
 //   * Tilted values E_{i,j} = 2^(x_{i,j} - c_j + kBias), formed once per K/V
 //     tile per workgroup and shared by all its waves through LDS.  c_j is a
 //     running per-channel maximum of x over the tiles seen so far (raised
@@ -248,19 +249,22 @@ __device__ __forceinline__ void tilt_tile(const Smem<D, NW>& sm, int tt, int k0,
 // Wave w writes 1 KiB blocks w, w+NW, ...; lane l of a block fills slot
 // 64*blk + l, i.e. row slot/SPR, chunk slot%SPR (the pad chunk re-reads chunk
 // 0).  Rows at or past T are clamped to T-1: their keys are masked anyway.
+// The address is a uniform tile base plus a 32-bit lane offset, so the loads
+// use scalar-base addressing and no 64-bit lane addresses stay live.
 template <int D, int NW>
 __device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned char* dst, int k0,
                                           int T, int wave, int lane) {
   using C = Cfg<D, NW>;
+  const char* base = reinterpret_cast<const char*>(src + (size_t)k0 * D);
+  const int rmax = T - 1 - k0;
 #pragma unroll
   for (int u = 0; u < C::BPW; ++u) {
     const int blk = wave + NW * u;
     if (C::BLOCKS % NW == 0 || blk < C::BLOCKS) {
       const int slot = blk * 64 + lane;
-      const int row = slot / C::SPR, chunk = slot % C::SPR;
-      const int r = min(k0 + row, T - 1);
-      const bf16* g = src + (size_t)r * D + (chunk < D / 8 ? chunk * 8 : 0);
-      __builtin_amdgcn_global_load_lds(g, dst + blk * 1024, 16, 0, 0);
+      const int row = min(slot / C::SPR, rmax), chunk = slot % C::SPR;
+      const unsigned off = (unsigned)(row * D + (chunk < D / 8 ? chunk * 8 : 0)) * 2u;
+      __builtin_amdgcn_global_load_lds(base + off, dst + blk * 1024, 16, 0, 0);
     }
   }
 }
@@ -272,9 +276,18 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // (E^T hi/lo or K) from LDS; the fragments are prefetched RING steps ahead so
 // that LDS latency hides behind the MFMAs already issued.  PV steps alternate
 // the output blocks (independent accumulators) within each hi/lo half.
+//
+// With PV the block also adds this tile's row sums of P into lacc: a 16x16x32
+// product of a constant 0/1 selector (lsel) with the same P^T fragments.
+// Lane l supplies selector row l%16 over k-block l/16; the B operand's k-block
+// b holds query (l%16) + 16*(b%2), so a one in row m = 4r for the k-blocks
+// with b%2 == r%2 sums query (l%16) + 16*(r%2) into output row 4r, which the
+// 16x16 output layout places in register 0 of lane 16r + l%16.  Hence
+// lacc[0] of every lane is the full row sum of its query l%32.
 template <int D, int NW, bool PV, bool QK>
-__device__ __forceinline__ void mfma_block(f32x16 (&acc)[D / 32], f32x16& s0, f32x16& s1,
-                                           const bf16x8 (&pf)[4], const bf16x8 (&qf)[D / 16],
+__device__ __forceinline__ void mfma_block(f32x16 (&acc)[D / 32], f32x4& lacc, f32x16& s0,
+                                           f32x16& s1, const bf16x8 (&pf)[4],
+                                           const bf16x8 (&qf)[D / 16], const bf16x8& lsel,
                                            const unsigned char* eh, const unsigned char* el,
                                            const unsigned char* kt) {
   using C = Cfg<D, NW>;
@@ -296,6 +309,12 @@ __device__ __forceinline__ void mfma_block(f32x16 (&acc)[D / 32], f32x16& s0, f3
 #pragma unroll
   for (int s = 0; s < RING; ++s)
     if (s < NS) ring[s] = frag(s);
+  // Row sums of P on the matrix pipe while the first fragments are in flight.
+  if (PV) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lsel, pf[ks], lacc, 0, 0, 0);
+  }
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     const bf16x8 a = ring[s % RING];
@@ -309,9 +328,11 @@ __device__ __forceinline__ void mfma_block(f32x16 (&acc)[D / 32], f32x16& s0, f3
       else s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s0, 0, 0, 0);
     }
   }
-  // Pin the order: RING fragment reads up front, then one read ahead per MFMA.
+  // Pin the order: RING fragment reads up front, the row-sum MFMAs, then one
+  // read ahead per MFMA.
 #pragma unroll
   for (int s = 0; s < RING; ++s) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  if (PV) __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     if (s + RING < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
@@ -384,9 +405,15 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   f32x16 sacc[2] = {f32x16{}, f32x16{}};  // scores: QK(k) -> softmax(k)
   bf16x8 pf[4] = {};                      // probabilities: softmax(k) -> PV(k)
   float m = -INFINITY;  // running row max (log2 units), shared by the lane pair
-  float l = 0.f;        // this lane's half of the row sum
+  f32x4 lacc = {};      // lacc[0]: row sum of the rounded P (see mfma_block)
+  bf16x8 lsel;
+  {
+    const int r = lane & 15, b = lane >> 4;
+    const __bf16 one = ((r & 3) == 0 && ((r >> 2) & 1) == (b & 1)) ? (__bf16)1.f : (__bf16)0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) lsel[e] = one;
+  }
   const float scale2 = kLog2e / sqrtf((float)D);
-  const bf16x2 ones = to_bf16x2(1.f, 1.f);
   const int kofs = n * C::KROW * 2 + hl * 16;  // lane part of K fragment addresses
   const int eofs = n * C::EROW * 2 + hl * 16;  // lane part of E fragment addresses
 
@@ -419,9 +446,12 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     const unsigned char* sel = sm.el(pb & 1) + eofs;
     const unsigned char* sk = sm.k(k & 1) + kofs;
     f32x16 s0 = f32x16{}, s1 = f32x16{};
-    if (do_pv && do_qk) mfma_block<D, NW, true, true>(acc, s0, s1, pf, qf, seh, sel, sk);
-    else if (do_pv) mfma_block<D, NW, true, false>(acc, s0, s1, pf, qf, seh, sel, sk);
-    else mfma_block<D, NW, false, true>(acc, s0, s1, pf, qf, seh, sel, sk);
+    if (do_pv && do_qk)
+      mfma_block<D, NW, true, true>(acc, lacc, s0, s1, pf, qf, lsel, seh, sel, sk);
+    else if (do_pv)
+      mfma_block<D, NW, true, false>(acc, lacc, s0, s1, pf, qf, lsel, seh, sel, sk);
+    else
+      mfma_block<D, NW, false, true>(acc, lacc, s0, s1, pf, qf, lsel, seh, sel, sk);
     if (do_qk) {
       sacc[0] = s0;
       sacc[1] = s1;
@@ -460,12 +490,11 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
       const float mnew = (mx > m + kRowLag) ? mx : m;
       if (__any(mnew != m)) {
         const float alpha = exp2_hw(m - mnew);
-        l *= alpha;
+        lacc[0] *= alpha;
 #pragma unroll
         for (int cb = 0; cb < C::NCB; ++cb) acc[cb] *= alpha;
         m = mnew;
       }
-      float l2 = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int kb = ks >> 1, s0i = (ks & 1) * 8;
@@ -475,11 +504,8 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
                                       exp2_hw(fmaf(sacc[kb][s0i + u + 1], scale2, -m)));
           pf[ks][u] = p2[0];
           pf[ks][u + 1] = p2[1];
-          if (u & 2) l2 = dot2_bf16(p2, ones, l2);
-          else l = dot2_bf16(p2, ones, l);
         }
       }
-      l += l2;
     }
     if (do_tilt) {
       if ((jt + 1) * C::BK <= T) tilt_finish<D, NW, true>(sm, jt, jt * C::BK, T, wave, lane, tv);
@@ -508,7 +534,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   // ---- epilogue: o = (log2 acc - log2 l + c - bias) / (beta log2 e).  The
   // logarithms are split into exponent and mantissa so the bias and the
   // integer parts cancel exactly (tiny beta amplifies any error here).
-  const float lt = l + other_half(l);
+  const float lt = lacc[0];
   int el;
   const float fl = log2_hw(frexpf(lt, &el));
   const float* cw = sm.cw(wave);
