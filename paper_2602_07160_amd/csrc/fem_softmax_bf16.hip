@@ -8,8 +8,8 @@
 //   * log2 domain throughout: scores are scaled by log2(e)/sqrt(d) and the
 //     tilt exponent is x_{i,j} = beta_j log2(e) v_{i,j}.
 //   * S^T = K Q^T per 64-key tile on MFMA (v_mfma_f32_32x32x16_bf16); the
-//     transposed product leaves one query per lane pair, so row max / row sum
-//     need one v_permlane32_swap and no LDS traffic.
+//     transposed product leaves one query per lane pair, so the row max needs
+//     one v_permlane32_swap and no LDS traffic.
 //   * Online row softmax with a running row max m_t (raised lazily, only when
 //     a tile beats it by kRowLag) and a row sum l_t accumulated from the SAME
 //     bf16-rounded probabilities that feed the product (a small MFMA against
@@ -30,19 +30,27 @@
 //     shared column shift) is recomputed exactly by the wave with a joint
 //     per-(t, j) log-sum-exp in fp32.
 //
-// Work decomposition: one workgroup of NW waves owns BQ = 32*NW query rows of
-// one (b, h); each wave owns 32 rows for the products and D/NW channels for
-// the tilt (so the running column maximum needs no cross-wave reduction).
+// Work decomposition: one workgroup of NW = 4 waves (one per SIMD) owns
+// BQ = 64*NW query rows of one (b, h); each wave owns 64 rows (two 32-row
+// blocks, so every LDS operand fragment feeds two MFMAs) for the products and
+// D/NW channels for the tilt (so the running column maximum needs no
+// cross-wave reduction).  One wave per SIMD leaves it the whole register file.
 //
-// Schedule.  A wave cannot issue vector instructions while its own MFMAs run,
-// but the two waves sharing a SIMD can overlap each other's.  So every wave
-// alternates a matrix-only block M(k) = {PV(k-1), QK(k)} with a vector-only
-// block {softmax(k) -> P(k), tilt of its channels of tile k}, and the two
-// waves of a SIMD run them in opposite halves of each iteration (two barriers
-// per 64-key tile).  K(k+1) and V(k+1) stream straight into the free LDS
-// buffers (global_load_lds_dwordx4) during iteration k; K, V and E are double
-// buffered.  Workgroups run longest causal extent first; workgroup i of a
-// causal level covers head i, so a head's workgroups share an XCD.
+// Schedule.  A wave keeps issuing independent vector instructions while its
+// own MFMAs run (about four per 32x32x16 MFMA come for free), so each
+// iteration k (one barrier) is two interleaved phases per wave:
+//   phase 1: QK^T(k) on the matrix pipe  ||  tilt of the wave's channels of
+//            tile k on the vector pipe;
+//   phase 2: PV(k-1) (hi, lo and the row-sum product)  ||  softmax of tile k
+//            (the scores phase 1 just produced).
+// The instruction mix of each phase is pinned with scheduling groups.  Row
+// and column rescales of the accumulator are rare; they are deferred to just
+// before the next PV so that neither phase needs a branch.  softmax(k)
+// overwrites the P registers behind PV(k-1) as it issues.  K(k+1) and
+// V(k+1) stream straight into the free LDS buffers (global_load_lds_dwordx4)
+// during iteration k; K, V and E are double buffered.  Workgroups run longest
+// causal extent first; workgroup i of a causal level covers head i, so a
+// head's workgroups share an XCD.
 
 #include "fem_device.h"
 #include "fem_internal.h"
@@ -56,6 +64,11 @@ constexpr float kBias = 64.f;        // E = 2^(x - c + kBias) <= 2^(kBias + kCol
 constexpr float kColLag = 16.f;      // column shift raised only past this lag
 constexpr float kRowLag = 8.f;       // row max raised only past this lag (P <= 2^8)
 constexpr float kUnderflow = 0x1p-64f;
+
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSgVALU = 0x002 | 0x400;  // vector ALU, transcendental included
+constexpr int kSgMFMA = 0x008;
+constexpr int kSgDSRead = 0x100;
 
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
@@ -85,21 +98,43 @@ struct Cfg {
   static constexpr int OFF_EH = OFF_V + 2 * KB;   // 2 buffers
   static constexpr int OFF_EL = OFF_EH + 2 * EB;  // 2 buffers
   static constexpr int OFF_F = OFF_EL + 2 * EB;   // floats
-  static constexpr int NF = D /*bl*/ + D /*inv*/ + 2 * D /*c*/ + 2 * D /*g*/ + NW * D /*cw*/;
-  static constexpr int OFF_R = OFF_F + NF * 4;    // rose flags [2][NW]
-  static constexpr size_t LDS = OFF_R + 2 * NW * 4;
+  static constexpr int NF = D /*bl*/ + D /*inv*/ + 2 * D /*c*/ + 2 * D /*g*/ + 64 /*sink*/;
+  static constexpr int OFF_R = OFF_F + NF * 4;    // column-update flags [2][NW]
+  static constexpr int OFF_T = OFF_R + 2 * NW * 4;  // tile-load lane offsets [NW][64][TW]
+  static constexpr int TW = (BPW + 3) / 4 * 4;
+  static constexpr size_t LDS = OFF_T + NW * 64 * TW * 4;
   static_assert(CPW * NW == D && G * CPW == 64 && RPL * G == 16, "tilt mapping");
   static_assert(BK * SPR % 64 == 0, "tile = whole 1 KiB blocks");
+  static_assert(NW % 4 == 0, "flags are read as int4");
   static_assert(LDS <= 160 * 1024, "LDS budget");
+  static_assert(OFF_EL - OFF_EH + D * EROW * 2 < 65536, "hi and lo share a base register");
 };
 
 // Position of key r (0..63 within a tile) inside an E^T row.  Within each
 // 16-key group the keys are stored in the order the MFMA B operand (P^T,
 // taken straight from the S^T accumulator layout) consumes them: lane half h
 // holds keys {4h..4h+3, 8+4h..8+4h+3} as its 8 consecutive k-slots.
-__device__ __forceinline__ int e_pos(int r) {
-  const int g = r & 15;
-  return (r & ~15) + (((g >> 2) & 1) << 3) + (((g >> 3) & 1) << 2) + (g & 3);
+__host__ __device__ constexpr int e_pos(int r) {
+  return (r & ~15) + ((((r & 15) >> 2) & 1) << 3) + ((((r & 15) >> 3) & 1) << 2) + (r & 3);
+}
+
+// The tilt lane with group index g writes keys 4(g + G u): their positions
+// split into a lane part and a part that is a compile-time constant.
+constexpr bool e_pos_splits(int G) {
+  for (int g = 0; g < G; ++g)
+    for (int u = 0; u < 16 / G; ++u)
+      if (e_pos(4 * (g + G * u)) != e_pos(4 * g) + e_pos(4 * G * u)) return false;
+  return true;
+}
+
+// An LDS byte offset kept in one register exactly as computed at this point:
+// the compiler neither folds parts of it into per-access immediates (the
+// 16-bit DS offset field cannot hold buffer bases past 64 KiB, which costs a
+// register per access) nor hoists it out of the loop.  Accesses then take
+// the form base + small immediate.
+__device__ __forceinline__ unsigned pin(unsigned x) {
+  asm volatile("" : "+v"(x));
+  return x;
 }
 
 // Exact fp32 read of one (t, j) by the whole wave: joint log-sum-exp of
@@ -139,8 +174,12 @@ struct Smem {
   __device__ float* inv() const { return bl() + D; }
   __device__ float* c(int b) const { return bl() + 2 * D + b * D; }
   __device__ float* g(int b) const { return bl() + 4 * D + b * D; }
-  __device__ float* cw(int w) const { return bl() + 6 * D + w * D; }
-  __device__ int* rose(int b) const { return reinterpret_cast<int*>(base + C::OFF_R) + b * NW; }
+  // Write-only slots for lanes whose store would otherwise need a branch.
+  __device__ float* sink() const { return bl() + 6 * D; }
+  __device__ int* upd(int b) const { return reinterpret_cast<int*>(base + C::OFF_R) + b * NW; }
+  __device__ unsigned* ltab(int w, int l) const {
+    return reinterpret_cast<unsigned*>(base + C::OFF_T) + (w * 64 + l) * C::TW;
+  }
 };
 
 // Bits of two floats' upper halves packed into one dword (bf16 truncation).
@@ -163,180 +202,341 @@ __device__ __forceinline__ float max_xor(float x, int o) {
   return fmaxf(x, __shfl_xor(x, o));
 }
 
-// Tilt of tile tt (first key k0) for this wave's CPW channels, in two steps so
-// that the LDS reads of V can be issued before unrelated vector work:
-//   tilt_read   : this lane's V values (channel jj, 4-key runs g + G*u);
-//   tilt_finish : column max over the tile (in-lane, then across the G lanes
-//                 of a channel), lazily raised running shift, E = 2^(x - c +
-//                 bias) split into bf16 hi (truncated) and lo (the rounded
-//                 remainder) -> E^T buffers.  FULL: every key of the tile < T.
+// Tilt of tile tt for this wave's CPW channels, as separately placeable steps
+// (the phases interleave them with MFMAs):
+//   read    : this lane's V values (channel jj, 4-key runs g + G*u), beta and
+//             the previous column shift, all from LDS;
+//   colmax  : column max over the tile (a tree in-lane, then across the G
+//             lanes of a channel);
+//   shift   : lazily raised running shift c_j; stores c, the rescale factor
+//             g = 2^(c_old - c_new) and the wave's "some c rose" flag;
+//   value(u, b), store(u) : E = 2^(x - c + bias) of key 4(g + G u) + b split
+//             into bf16 hi (truncated) and lo (the rounded remainder), and the
+//             store of run u into the E^T buffers.
+// Keys at or past T (last tile only) hold copies of row T-1 (see load_tile):
+// they leave the column max unchanged and give finite E, which meet P = 0
+// (the causal mask), so the tilt treats every tile as full.
+// Stores that only one lane of a group should make go to a sink slot from the
+// other lanes, so the code has no branches.
 template <int D, int NW>
-__device__ __forceinline__ void tilt_read(const Smem<D, NW>& sm, int tt, int wave, int lane,
-                                          float (&v)[Cfg<D, NW>::RPL][4]) {
+struct Tilt {
   using C = Cfg<D, NW>;
-  const int jj = lane % C::CPW, g = lane / C::CPW;
-  const int j = wave * C::CPW + jj;
-  const unsigned char* sv = sm.v(tt & 1) + j * 2;
-#pragma unroll
-  for (int u = 0; u < C::RPL; ++u) {
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int key = 4 * (g + C::G * u) + b;
-      v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + key * C::KROW * 2);
-    }
-  }
-}
+  float v[C::RPL][4];
+  float e[C::RPL][4];
+  float bl, cold, cnew, sh;
+  unsigned char* eh;
 
-template <int D, int NW, bool FULL>
-__device__ __forceinline__ void tilt_finish(const Smem<D, NW>& sm, int tt, int k0, int T,
-                                            int wave, int lane,
-                                            const float (&v)[Cfg<D, NW>::RPL][4]) {
-  using C = Cfg<D, NW>;
-  const int jj = lane % C::CPW, g = lane / C::CPW;
-  const int j = wave * C::CPW + jj;
-  const float bl = sm.bl()[j];
-  float vmax = -INFINITY;
+  __device__ __forceinline__ void read(const Smem<D, NW>& sm, int tt, int wave, int lane) {
+    const int jj = lane % C::CPW, g = lane / C::CPW;
+    const int j = wave * C::CPW + jj;
+    const unsigned char* sv =
+        sm.base + pin(C::OFF_V + (tt & 1) * C::KB + j * 2 + 4 * g * C::KROW * 2);
 #pragma unroll
-  for (int u = 0; u < C::RPL; ++u) {
+    for (int u = 0; u < C::RPL; ++u) {
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int key = 4 * (g + C::G * u) + b;
-      if (FULL || k0 + key < T) vmax = fmaxf(vmax, v[u][b]);
+      for (int b = 0; b < 4; ++b)
+        v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + (4 * C::G * u + b) * C::KROW * 2);
     }
+    bl = sm.bl()[j];
+    cold = (tt == 0) ? -INFINITY : sm.c((tt - 1) & 1)[j];
   }
+
+  __device__ __forceinline__ float colmax() const {
+    float t[C::RPL];
 #pragma unroll
-  for (int o = C::CPW; o < 64; o <<= 1) vmax = max_xor(vmax, o);
-  const float mx = vmax * bl;  // bl > 0: max of beta*v*log2e
-  const float cold = (tt == 0) ? -INFINITY : sm.c((tt - 1) & 1)[j];
-  const float cnew = (mx > cold + kColLag) ? mx : cold;
-  const float sh = kBias - cnew;
-  unsigned char* eh = sm.eh(tt & 1) + j * C::EROW * 2;
-  unsigned char* el = sm.el(tt & 1) + j * C::EROW * 2;
+    for (int u = 0; u < C::RPL; ++u)
+      t[u] = fmaxf(fmaxf(v[u][0], v[u][1]), fmaxf(v[u][2], v[u][3]));
 #pragma unroll
-  for (int u = 0; u < C::RPL; ++u) {
-    const int key0 = 4 * (g + C::G * u);
-    float e[4], lo[4];
+    for (int w = 1; w < C::RPL; w <<= 1) {
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      e[b] = exp2_hw(fmaf(v[u][b], bl, sh));
-      if (!FULL && k0 + key0 + b >= T) e[b] = 0.f;
-      lo[b] = e[b] - __uint_as_float(__float_as_uint(e[b]) & 0xffff0000u);
+      for (int u = 0; u + w < C::RPL; u += 2 * w) t[u] = fmaxf(t[u], t[u + w]);
     }
-    const u32x2 hi2 = {pack_hi16(e[0], e[1]), pack_hi16(e[2], e[3])};
+    float x = t[0];
+#pragma unroll
+    for (int o = C::CPW; o < 64; o <<= 1) x = max_xor(x, o);
+    return x;
+  }
+
+  __device__ __forceinline__ void shift(const Smem<D, NW>& sm, int tt, int wave, int lane,
+                                        float vmax) {
+    const int jj = lane % C::CPW, g = lane / C::CPW;
+    const int j = wave * C::CPW + jj;
+    const float mx = vmax * bl;  // bl > 0: max of beta*v*log2e
+    cnew = (mx > cold + kColLag) ? mx : cold;
+    sh = kBias - cnew;
+    eh = sm.base + pin(C::OFF_EH + (tt & 1) * C::EB + j * C::EROW * 2 + e_pos(4 * g) * 2);
+    float* sink = sm.sink() + lane;
+    *(g == 0 ? sm.c(tt & 1) + j : sink) = cnew;
+    *(g == 0 ? sm.g(tt & 1) + j : sink) = exp2_hw(cold - cnew);
+    const int rose = __any(cnew != cold) ? 1 : 0;
+    *(lane == 0 ? sm.upd(tt & 1) + wave : reinterpret_cast<int*>(sink)) = rose;
+  }
+
+  __device__ __forceinline__ void value(int u, int b) {
+    e[u][b] = exp2_hw(fmaf(v[u][b], bl, sh));
+  }
+
+  __device__ __forceinline__ void store(int u) {
+    static_assert(e_pos_splits(C::G), "tilt write positions");
+    float lo[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      lo[b] = e[u][b] - __uint_as_float(__float_as_uint(e[u][b]) & 0xffff0000u);
+    const u32x2 hi2 = {pack_hi16(e[u][0], e[u][1]), pack_hi16(e[u][2], e[u][3])};
     const bf16x2 l01 = to_bf16x2(lo[0], lo[1]), l23 = to_bf16x2(lo[2], lo[3]);
     const u32x2 lo2 = {__builtin_bit_cast(unsigned, l01), __builtin_bit_cast(unsigned, l23)};
-    *reinterpret_cast<u32x2*>(eh + e_pos(key0) * 2) = hi2;
-    *reinterpret_cast<u32x2*>(el + e_pos(key0) * 2) = lo2;
+    *reinterpret_cast<u32x2*>(eh + e_pos(4 * C::G * u) * 2) = hi2;
+    *reinterpret_cast<u32x2*>(eh + (C::OFF_EL - C::OFF_EH) + e_pos(4 * C::G * u) * 2) = lo2;
   }
-  if (g == 0) {
-    sm.c(tt & 1)[j] = cnew;
-    sm.g(tt & 1)[j] = exp2_hw(cold - cnew);
-  }
-  const bool rose = __any(cnew != cold);
-  if (lane == 0) sm.rose(tt & 1)[wave] = rose ? 1 : 0;
-}
+};
 
-// Whole tilt of tile tt (prologue).
-template <int D, int NW, bool FULL>
-__device__ __forceinline__ void tilt_tile(const Smem<D, NW>& sm, int tt, int k0, int T, int wave,
-                                          int lane) {
-  float v[Cfg<D, NW>::RPL][4];
-  tilt_read<D, NW>(sm, tt, wave, lane, v);
-  tilt_finish<D, NW, FULL>(sm, tt, k0, T, wave, lane, v);
-}
+// Online softmax of one tile's scores (entry (kb, i) of sc holds key
+// k0 + kb*32 + (i>>2)*8 + hl*4 + (i&3) of this lane's row), as placeable
+// steps: mask (diagonal tile only), a three-level max tree, the lazy row-max
+// update, and the probabilities of one pair of entries of k-step ks into the
+// MFMA B-operand registers.
+struct Softmax {
+  float t1[11], t2[4], mx;
+
+  template <bool MASK>
+  __device__ __forceinline__ void mask(f32x16 (&sc)[2], int k0, int tq, int hl) {
+    if (MASK) {
+      // entry (kb, i) holds key k0 + hl*4 + r(kb, i); it is in the past of
+      // row tq iff r <= lim.  Keys at or past T are past every row below T.
+      const int lim = tq - k0 - hl * 4;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = kb * 32 + (i >> 2) * 8 + (i & 3);
+          if (r > lim) sc[kb][i] = -INFINITY;
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ static float at(const f32x16 (&sc)[2], int e) {
+    return sc[e >> 4][e & 15];
+  }
+  // level 1, entries [0, 15) or [15, 32) of the 32
+  __device__ __forceinline__ void max1(const f32x16 (&sc)[2], int half) {
+    if (half == 0) {
+#pragma unroll
+      for (int q = 0; q < 5; ++q)
+        t1[q] = fmaxf(fmaxf(at(sc, 3 * q), at(sc, 3 * q + 1)), at(sc, 3 * q + 2));
+    } else {
+#pragma unroll
+      for (int q = 5; q < 10; ++q)
+        t1[q] = fmaxf(fmaxf(at(sc, 3 * q), at(sc, 3 * q + 1)), at(sc, 3 * q + 2));
+      t1[10] = fmaxf(at(sc, 30), at(sc, 31));
+    }
+  }
+  __device__ __forceinline__ void max2() {
+    t2[0] = fmaxf(fmaxf(t1[0], t1[1]), t1[2]);
+    t2[1] = fmaxf(fmaxf(t1[3], t1[4]), t1[5]);
+    t2[2] = fmaxf(fmaxf(t1[6], t1[7]), t1[8]);
+    t2[3] = fmaxf(t1[9], t1[10]);
+    mx = fmaxf(fmaxf(t2[0], t2[1]), fmaxf(t2[2], t2[3]));
+  }
+  // scores stay raw (q.k) up to here; scale2 > 0 so the max commutes with it
+  __device__ __forceinline__ void update(float& m, float& apend, float scale2) {
+    const float x = fmaxf(mx, other_half(mx)) * scale2;
+    const float mnew = (x > m + kRowLag) ? x : m;
+    apend = (mnew == m) ? 1.f : exp2_hw(m - mnew);
+    m = mnew;
+  }
+  __device__ __forceinline__ static void probs(const f32x16 (&sc)[2], bf16x8& p, int ks, int u,
+                                               float m, float scale2) {
+    const int kb = ks >> 1, s0 = (ks & 1) * 8;
+    const bf16x2 p2 = to_bf16x2(exp2_hw(fmaf(sc[kb][s0 + u], scale2, -m)),
+                                exp2_hw(fmaf(sc[kb][s0 + u + 1], scale2, -m)));
+    p[u] = p2[0];
+    p[u + 1] = p2[1];
+  }
+};
 
 // Direct global -> LDS copy of one K or V tile (rows k0 .. k0+63, padded rows).
 // Wave w writes 1 KiB blocks w, w+NW, ...; lane l of a block fills slot
 // 64*blk + l, i.e. row slot/SPR, chunk slot%SPR (the pad chunk re-reads chunk
 // 0).  Rows at or past T are clamped to T-1: their keys are masked anyway.
 // The address is a uniform tile base plus a 32-bit lane offset, so the loads
-// use scalar-base addressing and no 64-bit lane addresses stay live.
+// use scalar-base addressing.  The lane offsets of a whole tile (no clamping)
+// are computed once into an LDS table (tile_offsets) and read back per tile,
+// rather than held in registers across the loop.
+template <int D, int NW>
+__device__ __forceinline__ unsigned tile_offset(int u, int k0, int T, int wave, int lane) {
+  using C = Cfg<D, NW>;
+  const int slot = (wave + NW * u) * 64 + lane;
+  const int row = min(slot / C::SPR, T - 1 - k0), chunk = slot % C::SPR;
+  return (unsigned)(row * D + (chunk < D / 8 ? chunk * 8 : 0)) * 2u;
+}
+
+template <int D, int NW>
+__device__ __forceinline__ void tile_offsets(const Smem<D, NW>& sm, int wave, int lane,
+                                             unsigned (&off)[Cfg<D, NW>::BPW]) {
+  using C = Cfg<D, NW>;
+  const unsigned* t = sm.ltab(wave, lane);
+#pragma unroll
+  for (int u = 0; u < C::BPW; ++u) off[u] = t[u];
+}
+
 template <int D, int NW>
 __device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned char* dst, int k0,
-                                          int T, int wave, int lane) {
+                                          int wave, const unsigned (&off)[Cfg<D, NW>::BPW]) {
   using C = Cfg<D, NW>;
   const char* base = reinterpret_cast<const char*>(src + (size_t)k0 * D);
-  const int rmax = T - 1 - k0;
 #pragma unroll
   for (int u = 0; u < C::BPW; ++u) {
     const int blk = wave + NW * u;
-    if (C::BLOCKS % NW == 0 || blk < C::BLOCKS) {
-      const int slot = blk * 64 + lane;
-      const int row = min(slot / C::SPR, rmax), chunk = slot % C::SPR;
-      const unsigned off = (unsigned)(row * D + (chunk < D / 8 ? chunk * 8 : 0)) * 2u;
-      __builtin_amdgcn_global_load_lds(base + off, dst + blk * 1024, 16, 0, 0);
-    }
+    if (C::BLOCKS % NW == 0 || blk < C::BLOCKS)
+      __builtin_amdgcn_global_load_lds(base + off[u], dst + blk * 1024, 16, 0, 0);
   }
 }
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Matrix-only block: PV of the previous tile (if PV) then QK^T of this tile
-// (if QK), as one straight run of MFMAs.  Every MFMA takes its A operand
-// (E^T hi/lo or K) from LDS; the fragments are prefetched RING steps ahead so
-// that LDS latency hides behind the MFMAs already issued.  PV steps alternate
-// the output blocks (independent accumulators) within each hi/lo half.
+// Phase 1 of an iteration, interleaved by hand with the tilt of tile k (QKT):
+// on the matrix pipe, the row-sum products and k-step 0 of PV(k-1) (PVA),
+// then S^T = K Q^T of tile k into s (QKT).  Slot st issues MFMA st, the LDS
+// read of the operand fragment RING steps ahead and a fixed slice of the
+// tilt; a scheduling barrier after every slot keeps this order.
 //
-// With PV the block also adds this tile's row sums of P into lacc: a 16x16x32
-// product of a constant 0/1 selector (lsel) with the same P^T fragments.
-// Lane l supplies selector row l%16 over k-block l/16; the B operand's k-block
-// b holds query (l%16) + 16*(b%2), so a one in row m = 4r for the k-blocks
-// with b%2 == r%2 sums query (l%16) + 16*(r%2) into output row 4r, which the
-// 16x16 output layout places in register 0 of lane 16r + l%16.  Hence
-// lacc[0] of every lane is the full row sum of its query l%32.
-template <int D, int NW, bool PV, bool QK>
-__device__ __forceinline__ void mfma_block(f32x16 (&acc)[D / 32], f32x4& lacc, f32x16& s0,
-                                           f32x16& s1, const bf16x8 (&pf)[4],
-                                           const bf16x8 (&qf)[D / 16], const bf16x8& lsel,
-                                           const unsigned char* eh, const unsigned char* el,
-                                           const unsigned char* kt) {
+// Row sums: a 16x16x32 product of a constant 0/1 selector (lsel) with the
+// same P^T fragments.  Lane l supplies selector row l%16 over k-block l/16;
+// the B operand's k-block b holds query (l%16) + 16*(b%2), so a one in row
+// m = 4r for the k-blocks with b%2 == r%2 sums query (l%16) + 16*(r%2) into
+// output row 4r, which the 16x16 output layout places in register 0 of lane
+// 16r + l%16.  Hence lacc[0] of every lane is the row sum of its query l%32.
+template <int D, int NW, bool PVA, bool QKT>
+__device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW>& tl, int k, int wave,
+                                       int lane, int kofs, int eofs, const bf16x8 (&qf)[D / 16],
+                                       f32x16 (&s)[2], f32x16 (&acc)[D / 32], f32x4& lacc,
+                                       const bf16x8 (&pp)[4], const bf16x8& lsel) {
   using C = Cfg<D, NW>;
-  constexpr int NPV = PV ? 4 * 2 * C::NCB : 0;
-  constexpr int NQK = QK ? 2 * C::NKS : 0;
-  constexpr int NS = NPV + NQK;
-  constexpr int RING = 6;
-  auto frag = [&](int s) -> bf16x8 {
-    if (s < NPV) {
-      const int ks = s / (2 * C::NCB), rem = s % (2 * C::NCB);
-      const int lo = rem / C::NCB, cb = rem % C::NCB;
-      const unsigned char* b = lo ? el : eh;
-      return *reinterpret_cast<const bf16x8*>(b + cb * 32 * C::EROW * 2 + ks * 32);
+  constexpr int NL = PVA ? 4 : 0;             // row-sum MFMAs
+  constexpr int NE = PVA ? 2 * C::NCB : 0;    // PV k-step 0: hi and lo per output block
+  constexpr int NQ = QKT ? 2 * C::NKS : 0;    // QK MFMAs
+  constexpr int NF = NE + NQ;                 // LDS operand fragments
+  constexpr int NS = NL + NF;
+  constexpr int RING = 4;
+  constexpr int NV = QKT ? C::RPL * 4 : 0;    // tilt values of the lane
+  constexpr int C0 = PVA ? 2 : 0;             // slot of the column max
+  constexpr int NSLOT = NS > C0 + 2 + NV ? NS : C0 + 2 + NV;
+  auto vslot = [&](int x) { return C0 + 2 + (x * (NSLOT - C0 - 2)) / NV; };
+  if (QKT) tl.read(sm, k, wave, lane);
+  const unsigned char* kt = sm.base + pin(C::OFF_K + (k & 1) * C::KB + kofs);
+  const unsigned char* eb = sm.base + (PVA ? pin(C::OFF_EH + ((k - 1) & 1) * C::EB + eofs) : 0u);
+  auto frag = [&](int f) -> bf16x8 {
+    if (f < NE) {
+      const int lo = f / C::NCB, cb = f % C::NCB;
+      return *reinterpret_cast<const bf16x8*>(eb + lo * (C::OFF_EL - C::OFF_EH) +
+                                              cb * 32 * C::EROW * 2);
     }
-    const int t = s - NPV, ks = t >> 1, kb = t & 1;
-    return *reinterpret_cast<const bf16x8*>(kt + kb * 32 * C::KROW * 2 + ks * 32);
+    const int st = f - NE;
+    return *reinterpret_cast<const bf16x8*>(kt + (st & 1) * 32 * C::KROW * 2 + (st >> 1) * 32);
   };
   bf16x8 ring[RING];
 #pragma unroll
-  for (int s = 0; s < RING; ++s)
-    if (s < NS) ring[s] = frag(s);
-  // Row sums of P on the matrix pipe while the first fragments are in flight.
-  if (PV) {
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-      lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lsel, pf[ks], lacc, 0, 0, 0);
+  for (int f = 0; f < RING; ++f)
+    if (f < NF) ring[f] = frag(f);
+  if (QKT) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
   }
+  __builtin_amdgcn_sched_barrier(0);
+  float vmax = 0.f;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    const bf16x8 a = ring[s % RING];
-    if (s + RING < NS) ring[s % RING] = frag(s + RING);
-    if (s < NPV) {
-      const int ks = s / (2 * C::NCB), cb = (s % (2 * C::NCB)) % C::NCB;
-      acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[ks], acc[cb], 0, 0, 0);
-    } else {
-      const int t = s - NPV, ks = t >> 1;
-      if (t & 1) s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s1, 0, 0, 0);
-      else s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s0, 0, 0, 0);
+  for (int st = 0; st < NSLOT; ++st) {
+    if (st < NL) {
+      lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lsel, pp[st], lacc, 0, 0, 0);
+    } else if (st < NS) {
+      const int f = st - NL;
+      const bf16x8 a = ring[f % RING];
+      if (f + RING < NF) ring[f % RING] = frag(f + RING);
+      if (f < NE) {
+        const int cb = f % C::NCB;
+        acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pp[0], acc[cb], 0, 0, 0);
+      } else {
+        const int q = f - NE;
+        s[q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[q >> 1], s[q & 1], 0, 0, 0);
+      }
     }
+    if (QKT) {
+      if (st == C0) vmax = tl.colmax();
+      if (st == C0 + 1) tl.shift(sm, k, wave, lane, vmax);
+#pragma unroll
+      for (int x = 0; x < NV; ++x) {
+        if (vslot(x) == st) {
+          tl.value(x >> 2, x & 3);
+          if ((x & 3) == 3) tl.store(x >> 2);
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
-  // Pin the order: RING fragment reads up front, the row-sum MFMAs, then one
-  // read ahead per MFMA.
+}
+
+// Phase 2 of an iteration: k-steps 1..3 of PV(k-1) (PVB), interleaved by hand
+// with the softmax of this tile (SM; MASK on the wave's diagonal tile and the
+// tiles after it).  One P buffer serves both products: an MFMA reads its
+// operands when it issues, so the softmax writes the new P of k-step ks only
+// in slots after the last MFMA that reads ks (k-step 0 was read in phase 1).
+template <int D, int NW, bool PVB, bool SM, bool MASK>
+__device__ __forceinline__ void phase2(const Smem<D, NW>& sm, f32x16 (&acc)[D / 32],
+                                       bf16x8 (&pp)[4], f32x16 (&sc)[2], float& m, float& apend,
+                                       int j, int eofs, int k0, int tq, int hl, float scale2) {
+  using C = Cfg<D, NW>;
+  constexpr int NF = PVB ? 6 * C::NCB : 0;            // k-steps 1..3, hi and lo
+  constexpr int RING = 4;
+  constexpr int NSLOT = NF > 8 ? NF : 8;
+  // first slot free of reads of P k-step ks, then spread the 4 pairs
+  auto pslot = [&](int ks, int u) {
+    const int first = PVB ? 2 * C::NCB * ks : 0;
+    const int sl = first + (u / 2) * (C::NCB > 1 ? C::NCB / 2 : 1);
+    return sl < 4 ? 4 + sl : sl;
+  };
+  const unsigned char* eb = sm.base + (PVB ? pin(C::OFF_EH + (j & 1) * C::EB + eofs) : 0u);
+  auto frag = [&](int f) -> bf16x8 {
+    const int ks = 1 + f / (2 * C::NCB), rem = f % (2 * C::NCB);
+    const int lo = rem / C::NCB, cb = rem % C::NCB;
+    return *reinterpret_cast<const bf16x8*>(eb + lo * (C::OFF_EL - C::OFF_EH) +
+                                            cb * 32 * C::EROW * 2 + ks * 32);
+  };
+  bf16x8 ring[RING];
 #pragma unroll
-  for (int s = 0; s < RING; ++s) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  if (PV) __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  for (int f = 0; f < RING; ++f)
+    if (f < NF) ring[f] = frag(f);
+  Softmax smx;
+  if (SM) smx.mask<MASK>(sc, k0, tq, hl);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    if (s + RING < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  for (int st = 0; st < NSLOT; ++st) {
+    if (st < NF) {
+      const bf16x8 a = ring[st % RING];
+      if (st + RING < NF) ring[st % RING] = frag(st + RING);
+      const int ks = 1 + st / (2 * C::NCB), cb = (st % (2 * C::NCB)) % C::NCB;
+      acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pp[ks], acc[cb], 0, 0, 0);
+    }
+    if (SM) {
+      if (st == 0) smx.max1(sc, 0);
+      if (st == 1) smx.max1(sc, 1);
+      if (st == 2) smx.max2();
+      if (st == 3) smx.update(m, apend, scale2);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+        for (int u = 0; u < 8; u += 2)
+          if (pslot(ks, u) == st) Softmax::probs(sc, pp[ks], ks, u, m, scale2);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (SM) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int u = 0; u < 8; u += 2)
+        if (pslot(ks, u) >= NSLOT) Softmax::probs(sc, pp[ks], ks, u, m, scale2);
+    }
   }
 }
 
@@ -354,17 +554,12 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const int wave = tid >> 6;
   const int n = lane & 31;   // query column of this lane in the 32x32 blocks
   const int hl = lane >> 5;  // lane half
-  // Waves w and w + NW/2 share a SIMD.  Group A (w < NW/2) runs its matrix
-  // block in the first half of every iteration and its vector block in the
-  // second; group B the other way round, so one wave's vector work overlaps
-  // the other's MFMAs.
-  const bool grpB = wave >= NW / 2;
 
   const int bid = blockIdx.x;
-  const int qb = nqb - 1 - bid / nbh;  // longest causal extent first
+  const int qblk = nqb - 1 - bid / nbh;  // longest causal extent first
   const int bh = bid % nbh;
   const int h = bh % H;
-  const int q0 = qb * C::BQ;
+  const int q0 = qblk * C::BQ;
   const size_t base = (size_t)bh * T * D;
   const bf16* Qh = Q + base;
   const bf16* Kh = K + base;
@@ -382,13 +577,21 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const bool wave_live = wq0 < T;
   const int qlast = min(q0 + C::BQ, T) - 1;
   const int ntiles = qlast / C::BK + 1;
-  // Last tile this wave multiplies into its accumulator.  Later tiles may still
-  // raise the shared column shift; the wave keeps the shift its accumulator
-  // was last rescaled to (cw) instead of rescaling for tiles it skips.
+  // The tile holding the wave's diagonal.  The wave's first row is a multiple
+  // of 32, which divides the tile size, so earlier tiles lie wholly below the
+  // wave's rows and need no causal mask; this and later tiles are masked.
   const int wlast = wave_live ? min((wq0 + 31) / C::BK, ntiles - 1) : -1;
 
-  load_tile<D, NW>(Kh, sm.k(0), 0, T, wave, lane);
-  load_tile<D, NW>(Vh, sm.v(0), 0, T, wave, lane);
+  {
+    unsigned off[C::BPW];
+#pragma unroll
+    for (int u = 0; u < C::BPW; ++u) {
+      off[u] = tile_offset<D, NW>(u, 0, T, wave, lane);
+      sm.ltab(wave, lane)[u] = tile_offset<D, NW>(u, 0, 1 << 30, wave, lane);
+    }
+    load_tile<D, NW>(Kh, sm.k(0), 0, wave, off);
+    load_tile<D, NW>(Vh, sm.v(0), 0, wave, off);
+  }
   bf16x8 qf[C::NKS];
 #pragma unroll
   for (int ks = 0; ks < C::NKS; ++ks) {
@@ -402,10 +605,11 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   f32x16 acc[C::NCB];
 #pragma unroll
   for (int cb = 0; cb < C::NCB; ++cb) acc[cb] = f32x16{};
-  f32x16 sacc[2] = {f32x16{}, f32x16{}};  // scores: QK(k) -> softmax(k)
-  bf16x8 pf[4] = {};                      // probabilities: softmax(k) -> PV(k)
+  f32x16 sacc[2] = {f32x16{}, f32x16{}};  // scores of the current tile
+  bf16x8 pp[4] = {};                      // probabilities: softmax(k) -> PV(k)
   float m = -INFINITY;  // running row max (log2 units), shared by the lane pair
-  f32x4 lacc = {};      // lacc[0]: row sum of the rounded P (see mfma_block)
+  float apend = 1.f;    // row rescale owed to the accumulator before the next PV
+  f32x4 lacc = {};      // lacc[0]: row sum of the rounded P (see phase2)
   bf16x8 lsel;
   {
     const int r = lane & 15, b = lane >> 4;
@@ -417,117 +621,98 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const int kofs = n * C::KROW * 2 + hl * 16;  // lane part of K fragment addresses
   const int eofs = n * C::EROW * 2 + hl * 16;  // lane part of E fragment addresses
 
-  // ---- matrix block of iteration k: PV(k-1) then QK(k)
-  auto mblock = [&](int k) {
-    const int j = k - 1;
-    const bool do_pv = j >= 0 && j <= wlast;
-    const bool do_qk = k <= wlast;
-    if (!do_pv && !do_qk) return;
-    const int pb = j & 1;
-    if (do_pv && j > 0) {  // tile 0 always raises the shift, but the accumulator is still zero
-      const i32x4* rf = reinterpret_cast<const i32x4*>(sm.rose(pb));
-      i32x4 any4 = rf[0];
+  // The lane offsets of the next tile's loads: the table, or clamped rows for
+  // the last tile.
+  auto next_offsets = [&](int k, unsigned (&off)[C::BPW]) {
+    const int kn = (k + 1) * C::BK;
+    if (kn + C::BK <= T) {
+      tile_offsets<D, NW>(sm, wave, lane, off);
+    } else {  // last tile: rows at or past T read row T-1
 #pragma unroll
-      for (int w = 1; w < NW / 4; ++w) any4 |= rf[w];
-      if (any4[0] | any4[1] | any4[2] | any4[3]) {
-        const float* gcol = sm.g(pb);
-#pragma unroll
-        for (int cb = 0; cb < C::NCB; ++cb) {
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 gg = *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
-          }
-        }
-      }
-    }
-    const unsigned char* seh = sm.eh(pb & 1) + eofs;
-    const unsigned char* sel = sm.el(pb & 1) + eofs;
-    const unsigned char* sk = sm.k(k & 1) + kofs;
-    f32x16 s0 = f32x16{}, s1 = f32x16{};
-    if (do_pv && do_qk)
-      mfma_block<D, NW, true, true>(acc, lacc, s0, s1, pf, qf, lsel, seh, sel, sk);
-    else if (do_pv)
-      mfma_block<D, NW, true, false>(acc, lacc, s0, s1, pf, qf, lsel, seh, sel, sk);
-    else
-      mfma_block<D, NW, false, true>(acc, lacc, s0, s1, pf, qf, lsel, seh, sel, sk);
-    if (do_qk) {
-      sacc[0] = s0;
-      sacc[1] = s1;
-    }
-    if (do_pv && j == wlast) {
-      const float* cc = sm.c(pb);
-      for (int c = lane; c < D; c += 64) sm.cw(wave)[c] = cc[c];
+      for (int u = 0; u < C::BPW; ++u) off[u] = tile_offset<D, NW>(u, kn, T, wave, lane);
     }
   };
-
-  // ---- vector block: softmax of tile js (-> P, row rescale), tilt of tile jt
-  auto vblock = [&](int js, int jt) {
-    float tv[C::RPL][4];
-    const bool do_tilt = jt < ntiles;
-    if (do_tilt) tilt_read<D, NW>(sm, jt, wave, lane, tv);
-    if (js >= 0 && js <= wlast) {
-      const int k0 = js * C::BK;
-      // scores stay raw (q.k); scale2 > 0 so the row max commutes with it
-      if ((k0 + C::BK - 1 > wq0) || (k0 + C::BK > T)) {
+  auto load_next = [&](int k, const unsigned (&off)[C::BPW]) {
+    const int kn = (k + 1) * C::BK;
+    load_tile<D, NW>(Kh, sm.k((k + 1) & 1), kn, wave, off);
+    load_tile<D, NW>(Vh, sm.v((k + 1) & 1), kn, wave, off);
+  };
+  // Deferred rescales owed before PV(j): the row factor of softmax(j) and the
+  // column factors of tilt(j) (flag word from upd(j)).
+  auto rescale = [&](int j, const i32x4& any4) {
+    const bool col = (any4[0] | any4[1] | any4[2] | any4[3]) != 0;
+    if (col || __any(apend != 1.f)) {
+      const float* gcol = sm.g(j & 1);
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+      for (int cb = 0; cb < C::NCB; ++cb) {
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = k0 + kb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
-            if (key > tq || key >= T) sacc[kb][i] = -INFINITY;
-          }
+        for (int g = 0; g < 4; ++g) {
+          f32x4 gg = {apend, apend, apend, apend};
+          if (col) gg *= *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
         }
       }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
-      }
-      mx = fmaxf(mx, other_half(mx)) * scale2;
-      const float mnew = (mx > m + kRowLag) ? mx : m;
-      if (__any(mnew != m)) {
-        const float alpha = exp2_hw(m - mnew);
-        lacc[0] *= alpha;
-#pragma unroll
-        for (int cb = 0; cb < C::NCB; ++cb) acc[cb] *= alpha;
-        m = mnew;
-      }
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int kb = ks >> 1, s0i = (ks & 1) * 8;
-#pragma unroll
-        for (int u = 0; u < 8; u += 2) {
-          const bf16x2 p2 = to_bf16x2(exp2_hw(fmaf(sacc[kb][s0i + u], scale2, -m)),
-                                      exp2_hw(fmaf(sacc[kb][s0i + u + 1], scale2, -m)));
-          pf[ks][u] = p2[0];
-          pf[ks][u + 1] = p2[1];
-        }
-      }
-    }
-    if (do_tilt) {
-      if ((jt + 1) * C::BK <= T) tilt_finish<D, NW, true>(sm, jt, jt * C::BK, T, wave, lane, tv);
-      else tilt_finish<D, NW, false>(sm, jt, jt * C::BK, T, wave, lane, tv);
+      lacc[0] *= apend;
     }
   };
+  auto flags_of = [&](int j) {
+    const i32x4* uf = reinterpret_cast<const i32x4*>(sm.upd(j & 1));
+    i32x4 any4 = uf[0];
+#pragma unroll
+    for (int w = 1; w < NW / 4; ++w) any4 |= uf[w];
+    return any4;
+  };
+#define FEM_PHASE1(PVA, QKT) \
+  phase1<D, NW, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, pp, lsel)
+#define FEM_PHASE2(PVB, SM, MK) \
+  phase2<D, NW, PVB, SM, MK>(sm, acc, pp, sacc, m, apend, k - 1, eofs, k * C::BK, tq, hl, scale2)
 
-  for (int k = 0; k <= ntiles; ++k) {
+  // Every wave runs the same steps on every tile: past its diagonal tile the
+  // softmax masks every key, so P = 0 and PV adds nothing, while the
+  // accumulator keeps following the shared column shift to the last tile.
+  // Iteration k: loads of tile k+1; rescales owed before PV(k-1); phase 1:
+  // row sums + PV(k-1) k-step 0 + QK(k) || tilt(k); phase 2: PV(k-1) k-steps
+  // 1..3 || softmax(k); one barrier.
+  {
+    const int k = 0;
     if (k + 1 < ntiles) {
-      load_tile<D, NW>(Kh, sm.k((k + 1) & 1), (k + 1) * C::BK, T, wave, lane);
-      load_tile<D, NW>(Vh, sm.v((k + 1) & 1), (k + 1) * C::BK, T, wave, lane);
+      unsigned off[C::BPW];
+      next_offsets(k, off);
+      load_next(k, off);
     }
-    if (!grpB) {
-      mblock(k);
-      vblock(k, k);
-    } else {
-      vblock(k - 1, k);
-      mblock(k);
-    }
+    Tilt<D, NW> tl;
+    FEM_PHASE1(false, true);
+    if (wlast <= 0) FEM_PHASE2(false, true, true);
+    else FEM_PHASE2(false, true, false);
     wait_vmem();
     __syncthreads();
   }
+  for (int k = 1; k < ntiles; ++k) {
+    // LDS reads of the flag words and the load offsets go out together
+    const i32x4 any4 = flags_of(k - 1);
+    if (k + 1 < ntiles) {
+      unsigned off[C::BPW];
+      next_offsets(k, off);
+      load_next(k, off);
+    }
+    if (k > 1) rescale(k - 1, any4);
+    Tilt<D, NW> tl;
+    FEM_PHASE1(true, true);
+    if (k >= wlast) FEM_PHASE2(true, true, true);
+    else FEM_PHASE2(true, true, false);
+    wait_vmem();
+    __syncthreads();
+  }
+  {
+    const int k = ntiles;
+    if (k > 1) rescale(k - 1, flags_of(k - 1));
+    Tilt<D, NW> tl;
+    FEM_PHASE1(true, false);
+    FEM_PHASE2(true, false, false);
+  }
+#undef FEM_PHASE1
+#undef FEM_PHASE2
 
   if (!wave_live) return;
 
@@ -537,7 +722,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const float lt = lacc[0];
   int el;
   const float fl = log2_hw(frexpf(lt, &el));
-  const float* cw = sm.cw(wave);
+  const float* cw = sm.c((ntiles - 1) & 1);  // the accumulator's final column frame
   const float* inv = sm.inv();
   uint64_t flags = 0;
 #pragma unroll
