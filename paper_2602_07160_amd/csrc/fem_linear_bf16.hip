@@ -19,10 +19,14 @@
 // Chunking: 64-token chunks inside 512-token segments.
 //   kernel 1 (state):  one workgroup per (b, h, segment): the segment's own
 //                      state [S | z] and shift c, starting from zero.
-//   kernel 2 (read):   one workgroup per (b, h, segment): combines the states
-//                      of all earlier segments into its entering state, then
-//                      scans its chunks: intra-chunk (phi Q phi K^T masked) E,
-//                      inter-chunk phi Q S, and the state update phi K^T E.
+//   kernel 2 (prefix): per (b, h), the exclusive prefix of the segment states
+//                      (the state entering each segment), one thread per
+//                      state entry, in place.
+//   kernel 3 (read):   one workgroup per (b, h, segment): loads its entering
+//                      state, then scans its chunks: intra-chunk (phi Q phi
+//                      K^T masked) E, inter-chunk phi Q S, and the state update
+//                      phi K^T E.  The next chunk's Q, K, V are fetched into
+//                      registers while the current one is processed.
 // All products run on v_mfma_f32_32x32x16_bf16 in transposed form (outputs
 // are [channel][token]); E and S enter as bf16 hi + lo pairs, the masked
 // intra-chunk scores A enter as bf16 and the normaliser is summed from the
@@ -66,7 +70,7 @@ struct LinSmem {
   float bl[DV];         // beta log2 e
   float inv[DV];
   float z[DK];          // sum of phi(k) over earlier chunks
-  float zc[DK];         // sum of phi(k) over this chunk
+  float zc[4 * DK];     // partial sums of phi(k) over this chunk (four row quarters)
   int rose;
 };
 
@@ -78,7 +82,19 @@ __device__ __forceinline__ int e_pos(int r) {
   return (r & ~15) + (((g >> 2) & 1) << 3) + (((g >> 3) & 1) << 2) + (g & 3);
 }
 
-__device__ __forceinline__ float phi(float x) { return x > 0.f ? x + 1.f : exp2_hw(x * kLog2e); }
+// Workgroup barrier that orders LDS only: every wave's LDS accesses complete
+// before it, while global loads in flight (the next chunk's prefetch) keep
+// running.  (__syncthreads() would also wait for those.)
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// elu(x) + 1, without a branch: the exponential is evaluated for every x (at
+// min(x, 0), so it stays finite) and selected.
+__device__ __forceinline__ float phi(float x) {
+  const float e = exp2_hw(fminf(x, 0.f) * kLog2e);
+  return x > 0.f ? x + 1.f : e;
+}
 
 // Exact fp32 read of one (t, j) of the linear prior by the whole wave.
 __device__ float exact_read_linear(const bf16* __restrict__ Qh, const bf16* __restrict__ Kh,
@@ -97,41 +113,62 @@ __device__ float exact_read_linear(const bf16* __restrict__ Qh, const bf16* __re
   return (num.wave_total() - den.wave_total()) / bl;
 }
 
-// One chunk of the scan.  Loads tokens [t0, t0 + CH) (rows past T are zero and
-// masked), tilts V, rescales the state, produces outputs (OUT) and updates S.
+// Raw Q, K, V of one chunk held in registers: thread tid covers the 16-byte
+// slots e = tid + NTH*i (row e >> 3, columns (e & 7)*8 ..).
+constexpr int SLOTS = CH * 8 / NTH;
+struct ChunkRegs {
+  bf16x8 q[SLOTS], k[SLOTS], v[SLOTS];
+};
+
+template <bool OUT>
+__device__ __forceinline__ void fetch_chunk(ChunkRegs& cr, const bf16* Qh, const bf16* Kh,
+                                            const bf16* Vh, int t0, int T) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < SLOTS; ++i) {
+    const int e = tid + NTH * i, r = e >> 3, c8 = (e & 7) * 8;
+    bf16x8 z = {};
+    const bool ok = t0 + r < T;
+    cr.k[i] = ok ? *reinterpret_cast<const bf16x8*>(Kh + (size_t)(t0 + r) * DK + c8) : z;
+    cr.v[i] = ok ? *reinterpret_cast<const bf16x8*>(Vh + (size_t)(t0 + r) * DV + c8) : z;
+    if (OUT) cr.q[i] = ok ? *reinterpret_cast<const bf16x8*>(Qh + (size_t)(t0 + r) * DK + c8) : z;
+  }
+}
+
+// One chunk of the scan.  Stages tokens [t0, t0 + CH) from cr (rows past T
+// are zero and masked), starts fetching the next chunk into cr, tilts V,
+// rescales the state, produces outputs (OUT) and updates S.
 // Wave w owns S^T block (dvb = w >> 1, dkb = w & 1) and output block
 // (dvb = w >> 1, qb = w & 1).
 template <bool OUT>
-__device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, const bf16* Qh,
-                                           const bf16* Kh, const bf16* Vh, float* Oh, int t0,
-                                           int T) {
+__device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, ChunkRegs& cr,
+                                           const bf16* Qh, const bf16* Kh, const bf16* Vh,
+                                           float* Oh, int t0, int tnext, int T) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, hl = lane >> 5;
   const int dvb = wave >> 1, sub = wave & 1;
 
   // ---- stage Q, K, V of the chunk; phi in fp32, rounded to bf16
-  for (int e = tid; e < CH * 8; e += NTH) {
-    const int r = e >> 3, c8 = (e & 7) * 8;
-    const bool ok = t0 + r < T;
-    bf16x8 kq = {}, kk = {}, kv = {};
-    if (ok) {
-      kk = *reinterpret_cast<const bf16x8*>(Kh + (size_t)(t0 + r) * DK + c8);
-      kv = *reinterpret_cast<const bf16x8*>(Vh + (size_t)(t0 + r) * DV + c8);
-      if (OUT) kq = *reinterpret_cast<const bf16x8*>(Qh + (size_t)(t0 + r) * DK + c8);
-    }
+#pragma unroll
+  for (int i = 0; i < SLOTS; ++i) {
+    const int e = tid + NTH * i, r = e >> 3, c8 = (e & 7) * 8;
+    // rows past T: phi of the zeros fetched there, times 0 (no branch)
+    const float okf = t0 + r < T ? 1.f : 0.f;
     bf16x8 pk, pq;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      pk[u] = ok ? (bf16)phi((float)kk[u]) : (bf16)0.f;
-      pq[u] = ok ? (bf16)phi((float)kq[u]) : (bf16)0.f;
+      pk[u] = (bf16)(phi((float)cr.k[i][u]) * okf);
+      if (OUT) pq[u] = (bf16)(phi((float)cr.q[i][u]) * okf);
       sm.fkt[(c8 + u) * ROW + e_pos(r)] = pk[u];
     }
     *reinterpret_cast<bf16x8*>(sm.fk + r * ROW + c8) = pk;
-    *reinterpret_cast<bf16x8*>(sm.v + r * ROW + c8) = kv;
+    *reinterpret_cast<bf16x8*>(sm.v + r * ROW + c8) = cr.v[i];
     if (OUT) *reinterpret_cast<bf16x8*>(sm.fq + r * ROW + c8) = pq;
   }
   if (tid == 0) sm.rose = 0;
-  __syncthreads();
+  // the next chunk's loads run while this one is processed
+  if (tnext < T) fetch_chunk<OUT>(cr, Qh, Kh, Vh, tnext, T);
+  lds_barrier();
 
   // ---- tilt: wave w owns channels 16w .. 16w+15; lane = channel + 16 * key group
   {
@@ -168,21 +205,23 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, const bf16* 
       *reinterpret_cast<bf16x4*>(sm.eh + j * ROW + e_pos(key0)) = hi;
       *reinterpret_cast<bf16x4*>(sm.el + j * ROW + e_pos(key0)) = lo;
     }
-    __syncthreads();  // every lane has read sm.c before it changes
+    lds_barrier();  // every lane has read sm.c before it changes
     if (g == 0) {
       sm.g[j] = exp2_hw(cold - cnew);
       sm.c[j] = cnew;
       if (cnew != cold) sm.rose = 1;
     }
-    // chunk sum of phi(k): wave 0..3 each sum 16 d_k columns
-    if (g == 0) {
-      const int dkc = wave * 16 + jj;
+    // chunk sum of phi(k): thread (column tid & 63, quarter tid >> 6) sums 16
+    // rows; the four partial sums meet in LDS
+    {
+      const int dkc = tid & 63, q4 = tid >> 6;
       float s = 0.f;
-      for (int r = 0; r < CH; ++r) s += (float)sm.fk[r * ROW + dkc];
-      sm.zc[dkc] = s;
+#pragma unroll
+      for (int r = 0; r < CH / 4; ++r) s += (float)sm.fk[(q4 * (CH / 4) + r) * ROW + dkc];
+      sm.zc[q4 * DK + dkc] = s;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- rescale the state rows (d_v) when the shift rose, publish S^T hi/lo
   if (sm.rose) {
@@ -198,7 +237,7 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, const bf16* 
       sm.sh[row * SROW + col] = hi;
       sm.sl[row * SROW + col] = (bf16)(st[i] - (float)hi);
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- outputs of query block qb = sub, channel block dvb
     const int qb = sub;
@@ -235,39 +274,40 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, const bf16* 
         den = add_bf16x2(p2, den);
       }
     }
-    // inter-chunk normaliser phi(q)^T z, this lane's half of d_k
-    {
-      const bf16* fqr = sm.fq + (qb * 32 + n) * ROW;
-#pragma unroll
-      for (int ks = 0; ks < DK / 16; ++ks) {
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int dk = ks * 16 + hl * 8 + u;
-          den = fmaf((float)fqr[dk], sm.z[dk], den);
-        }
-      }
-    }
-    den += other_half(den);
-    // numerator: E^T A^T (intra) + S^T phi(Q)^T (inter)
-    f32x16 num = f32x16{};
+    // numerator: E^T A^T (intra) + S^T phi(Q)^T (inter), in independent
+    // accumulators so the MFMAs do not wait on each other; the inter-chunk
+    // normaliser phi(q)^T z (this lane's half of d_k) reuses the phi(Q)
+    // fragments, with four partial sums
+    f32x16 nacc[4] = {f32x16{}, f32x16{}, f32x16{}, f32x16{}};
     const int eoff = (dvb * 32 + n) * ROW + hl * 8;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       if ((ks >> 1) > qb) continue;
       const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.eh + eoff + ks * 16);
       const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.el + eoff + ks * 16);
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, pf[ks], num, 0, 0, 0);
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, pf[ks], num, 0, 0, 0);
+      nacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, pf[ks], nacc[0], 0, 0, 0);
+      nacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, pf[ks], nacc[1], 0, 0, 0);
     }
     const int soff = (dvb * 32 + n) * SROW + hl * 8;
+    float dz[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < DK / 16; ++ks) {
       const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.sh + soff + ks * 16);
       const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.sl + soff + ks * 16);
       const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + (qb * 32 + n) * ROW + ks * 16 + hl * 8);
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, num, 0, 0, 0);
+      nacc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, nacc[2], 0, 0, 0);
+      nacc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, nacc[3], 0, 0, 0);
+      const f32x4 z0 = *reinterpret_cast<const f32x4*>(sm.z + ks * 16 + hl * 8);
+      const f32x4 z1 = *reinterpret_cast<const f32x4*>(sm.z + ks * 16 + hl * 8 + 4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        dz[u] = fmaf((float)b[u], z0[u], dz[u]);
+        dz[u] = fmaf((float)b[u + 4], z1[u], dz[u]);
+      }
     }
+    den += (dz[0] + dz[1]) + (dz[2] + dz[3]);
+    den += other_half(den);
+    const f32x16 num = (nacc[0] + nacc[1]) + (nacc[2] + nacc[3]);
     // epilogue
     int ed;
     const float fd = log2_hw(frexpf(den, &ed));
@@ -315,9 +355,39 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, const bf16* 
       st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, st, 0, 0, 0);
     }
   }
-  __syncthreads();
-  if (tid < DK) sm.z[tid] += sm.zc[tid];
-  __syncthreads();
+  lds_barrier();
+  if (tid < DK) sm.z[tid] += (sm.zc[tid] + sm.zc[DK + tid]) + (sm.zc[2 * DK + tid] + sm.zc[3 * DK + tid]);
+  lds_barrier();
+}
+
+// Exclusive prefix of the segment states of one (b, h) (blockIdx.y): slot s
+// of `pre` receives the state entering segment s, combined from the own states
+// of segments 0 .. s-1 in `own`, each relative to its own shift.  One thread
+// per state entry: S[j][*] carries row shift c_j, z needs none, c is the max.
+__global__ __launch_bounds__(NTH) void prefix_kernel(const float* __restrict__ own,
+                                                     float* __restrict__ pre, int nseg) {
+  const int e = blockIdx.x * NTH + threadIdx.x;
+  if (e >= STATE) return;
+  const size_t base = (size_t)blockIdx.y * nseg * STATE;
+  const float* ob = own + base;
+  float* pb = pre + base;
+  const int j = e < DV * DK ? e / DK : (e >= DV * DK + DK ? e - DV * DK - DK : -1);
+  float acc = 0.f, C = -INFINITY;
+  for (int sg = 0; sg + 1 < nseg; ++sg) {
+    const float val = ob[(size_t)sg * STATE + e];
+    if (e < DV * DK) {
+      const float cs = ob[(size_t)sg * STATE + DV * DK + DK + j];
+      const float Cn = fmaxf(C, cs);
+      acc = acc * exp2_hw(C - Cn) + val * exp2_hw(cs - Cn);
+      C = Cn;
+    } else if (e < DV * DK + DK) {
+      acc += val;
+    } else {
+      acc = fmaxf(C, val);
+      C = acc;
+    }
+    pb[(size_t)(sg + 1) * STATE + e] = acc;
+  }
 }
 
 template <bool OUT>
@@ -338,7 +408,7 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   const bf16* Kh = K + (size_t)bh * T * DK;
   const bf16* Vh = V + (size_t)bh * T * DV;
   float* Oh = out + (size_t)bh * T * DV;
-  float* wsh = ws + (size_t)bh * nseg * STATE;
+  float* wsh = ws + (size_t)bh * nseg * STATE;  // own states; entering states follow gridDim.x slots on
   const int dvb = wave >> 1, sub = wave & 1;
 
   if (tid < DV) {
@@ -351,34 +421,27 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   f32x16 st = f32x16{};
   __syncthreads();
 
-  if (OUT && seg > 0) {
-    // entering state: all earlier segments, each relative to its own shift
-    if (tid < DV) {
-      float C = -INFINITY;
-      for (int s = 0; s < seg; ++s) C = fmaxf(C, wsh[(size_t)s * STATE + DV * DK + DK + tid]);
-      sm.c[tid] = C;
-    }
-    if (tid < DK) {
-      float z = 0.f;
-      for (int s = 0; s < seg; ++s) z += wsh[(size_t)s * STATE + DV * DK + tid];
-      sm.z[tid] = z;
-    }
-    __syncthreads();
-    for (int s = 0; s < seg; ++s) {
-      const float* S = wsh + (size_t)s * STATE;
-      const float* cs = S + DV * DK + DK;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
-        const int col = sub * 32 + (lane & 31);
-        st[i] = fmaf(S[row * DK + col], exp2_hw(cs[row] - sm.c[row]), st[i]);
-      }
-    }
-  }
-
   const int tbeg = seg * SEG;
   const int tend = min(tbeg + SEG, T);
-  for (int t0 = tbeg; t0 < tend; t0 += CH) scan_chunk<OUT>(sm, st, Qh, Kh, Vh, Oh, t0, T);
+  ChunkRegs cr;
+  fetch_chunk<OUT>(cr, Qh, Kh, Vh, tbeg, T);
+
+  if (OUT && seg > 0) {
+    // entering state, left by the prefix kernel in the second half of ws
+    const float* S = wsh + (size_t)gridDim.x * STATE + (size_t)seg * STATE;
+    if (tid < DK) sm.z[tid] = S[DV * DK + tid];
+    if (tid < DV) sm.c[tid] = S[DV * DK + DK + tid];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
+      const int col = sub * 32 + (lane & 31);
+      st[i] = S[row * DK + col];
+    }
+    __syncthreads();
+  }
+
+  for (int t0 = tbeg; t0 < tend; t0 += CH)
+    scan_chunk<OUT>(sm, st, cr, Qh, Kh, Vh, Oh, t0, t0 + CH < tend ? t0 + CH : T, T);
 
   if (!OUT) {
     float* S = wsh + (size_t)seg * STATE;
@@ -402,7 +465,8 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const
   const int nseg = (T + SEG - 1) / SEG;
   const int nbh = B * H;
   float* ws = nullptr;
-  const size_t bytes = (size_t)nbh * nseg * STATE * sizeof(float);
+  // own segment states, then the entering (prefix) states
+  const size_t bytes = 2 * (size_t)nbh * nseg * STATE * sizeof(float);
   hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
   if (e != hipSuccess) return e;
   if (nseg > 1) {
@@ -410,6 +474,11 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const
                        reinterpret_cast<const bf16*>(Q), reinterpret_cast<const bf16*>(K),
                        reinterpret_cast<const bf16*>(V), beta, out, ws, H, T, nseg);
     e = hipGetLastError();
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)((STATE + NTH - 1) / NTH), (unsigned)nbh),
+                         dim3(NTH), 0, stream, ws, ws + (size_t)nbh * nseg * STATE, nseg);
+      e = hipGetLastError();
+    }
   }
   if (e == hipSuccess) {
     hipLaunchKernelGGL(linear_kernel<true>, dim3((unsigned)(nbh * nseg)), dim3(NTH), 0, stream,
