@@ -25,4 +25,7 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V,
 hipError_t workspace_alloc(void** p, size_t bytes, hipStream_t stream);
 hipError_t workspace_free(void* p, hipStream_t stream);
 
+// Compute units of the current device (0 if the query fails); cached.
+int device_cus();
+
 }  // namespace fem

@@ -1,4 +1,5 @@
-// Stream-ordered scratch memory for the kernels' intermediate results.
+// Stream-ordered scratch memory for the kernels' intermediate results, and
+// the device facts the launchers size their grids by.
 //
 // Allocations come from a library-owned memory pool per device whose release
 // threshold is unbounded, so after the first call a workspace of the same
@@ -55,5 +56,18 @@ hipError_t workspace_alloc(void** p, size_t bytes, hipStream_t stream) {
 }
 
 hipError_t workspace_free(void* p, hipStream_t stream) { return hipFreeAsync(p, stream); }
+
+int device_cus() {
+  static int cus[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
 
 }  // namespace fem
