@@ -11,6 +11,9 @@ from .fem_oracle import (  # noqa: F401
     softmax_prior_rows,
     linear_prior_rows,
     free_energy_read,
+    expectation_read,
+    ltl_read,
+    fem_softmax_ltl,
     fem_softmax,
     fem_linear,
     fem_linear_recurrent,

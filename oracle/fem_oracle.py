@@ -15,6 +15,10 @@ Prior Selection", softmax prior):
                      with phi = elu + 1                                (linear)
   read      F_{t,j} = (1 / beta_j) * log sum_{i<=t} p_t(i) * exp(beta_j v_{i,j})
                                   (free-energy read, eq. fem-free-energy-main)
+  gated     o_{t,j} = g_{t,j} * ((1 - lam_{t,j}) * mu_{t,j} + lam_{t,j} * F_{t,j}(beta_max))
+            mu_{t,j} = sum_{i<=t} p_t(i) v_{i,j}
+                                  (two-level gated read, eqs. ltl-final,
+                                   inner-gate-main, fem-two-gates-main)
 
 Indices are 0-based here; the causal support of row t is {0, ..., t}, diagonal
 included.  The read is exact up to float64 rounding: the only numerical device
@@ -130,6 +134,30 @@ def free_energy_read(p: np.ndarray, v: np.ndarray, beta: np.ndarray,
     return out
 
 
+def expectation_read(p: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """mu[r, j] = sum_i p[r, i] v[i, j], the prior's expectation of the values.
+
+    The expectation baseline of the linearized temperature learning (Sec.
+    "Linearized Temperature Learning": mu_{t,j} = E_{i ~ p_t}[v_{i,j}]).
+    """
+    return p @ v
+
+
+def ltl_read(p: np.ndarray, v: np.ndarray, beta_max: np.ndarray, lam: np.ndarray,
+             gate=None, logp=None) -> np.ndarray:
+    """Two-level gated read o = g * ((1 - lam) * mu + lam * F(beta_max)).
+
+    Eq. ltl-final (one expectation and one log-sum-exp at beta_max per
+    channel), eq. inner-gate-main (the inner temperature gate lam in [0, 1])
+    and eq. fem-two-gates-main (the outer gate g > 0).  p: [R, n]; v: [n, D];
+    beta_max: [D]; lam, gate: [R, D] (gate None means g = 1).
+    """
+    mu = expectation_read(p, v)
+    fmax = free_energy_read(p, v, beta_max, logp=logp)
+    o = (1.0 - lam) * mu + lam * fmax
+    return o if gate is None else gate * o
+
+
 def posterior(p_row: np.ndarray, v_col: np.ndarray, beta: float) -> np.ndarray:
     """Posterior selector q(i) proportional to p(i) exp(beta v_i) on the support.
 
@@ -176,6 +204,36 @@ def fem_softmax(q, k, v, beta, rows=None, block: int = 512) -> np.ndarray:
                       softmax_logprior_rows(qq, kk, rr))
                 out[b, h, pos:pos + len(rb)] = free_energy_read(
                     p, v[b, h, :n], beta[h], logp=lp)
+                pos += len(rb)
+    return out
+
+
+def fem_softmax_ltl(q, k, v, beta_max, lam, gate=None, rows=None,
+                    block: int = 512) -> np.ndarray:
+    """Two-level gated FEM read with the causal softmax prior.
+
+    q, k: [B, H, T, d]; v: [B, H, T, d_v]; beta_max: [H, d_v] (> 0);
+    lam: [B, H, T, d_v] in [0, 1]; gate: [B, H, T, d_v] (> 0) or None (= 1).
+    rows: optional query rows (default all T).  Returns float64
+    [B, H, len(rows), d_v].
+    """
+    q, k, v, beta_max, lam = _as64(q), _as64(k), _as64(v), _as64(beta_max), _as64(lam)
+    gate = None if gate is None else _as64(gate)
+    B, H, T, _ = q.shape
+    dv = v.shape[3]
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = np.empty((B, H, len(rows), dv))
+    for b in range(B):
+        for h in range(H):
+            pos = 0
+            for rb in _row_blocks(rows, block):
+                n = int(rb.max()) + 1
+                p = softmax_prior_rows(q[b, h], k[b, h], rb)
+                lp = (lambda qq=q[b, h], kk=k[b, h], rr=rb:
+                      softmax_logprior_rows(qq, kk, rr))
+                g = None if gate is None else gate[b, h, rb]
+                out[b, h, pos:pos + len(rb)] = ltl_read(
+                    p, v[b, h, :n], beta_max[h], lam[b, h, rb], g, logp=lp)
                 pos += len(rb)
     return out
 
