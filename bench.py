@@ -10,7 +10,9 @@ synthetic data resident in HBM before the timed region.  Prints ONE JSON line.
 Throughput is algorithmic: FLOP = 2*B*H*T*(T+1)*d per call (Q K^T and P E
 multiply-adds over the causal triangle, diagonal included; exponentials not
 counted).  The linear-prior read (fem_linear_fwd, B=4, H=16, T=8192,
-d_k=d_v=64, chunk 64) is timed too and reported under "linear".
+d_k=d_v=64, chunk 64) is timed too and reported under "linear", and the
+two-level gated read (fem_softmax_gated_fwd) on the headline shape under
+"gated" (FLOP = 3*B*H*T*(T+1)*d: Q K^T, P E and P V).
 """
 
 from __future__ import annotations
@@ -102,6 +104,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-linear", action="store_true")
+    ap.add_argument("--no-gated", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a known-size "
                          "kernel for calibrating hardware byte counters)")
@@ -158,9 +161,25 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
             "traffic": measured_traffic("fem_softmax_bf16.hip"),
-            "kernel": "softmax_bf16_kernel<128,8>",
+            "kernel": "softmax_bf16_kernel<128,8,kFem>",
         },
     }
+    if not args.no_gated:
+        lam, g = inputs.draw_gates(inputs.BASE_SEED + 103, B, H, T, d)
+        lamd, gd = lam.to(dev), g.to(dev)
+        fng = lambda: binding.fem_softmax_gated_fwd(qd, kd, vd, bd, lamd, gd, out=out)
+        msg = time_calls(fng, args.steps, args.warmup)
+        flop_g = 3.0 * B * H * T * (T + 1) * d
+        result["gated"] = {
+            "workload": w.name + "_gated", "ms": round(msg, 4),
+            "tokens_per_s": round(B * T / (msg * 1e-3), 1),
+            "flop_per_call": flop_g,
+            "achieved_TFLOPs": round(flop_g / (msg * 1e-3) / 1e12, 2),
+            "peak_TFLOPs": PEAK_BF16_TFLOPS,
+            "frac": round(flop_g / (msg * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "kernels": ["softmax_bf16_kernel<128,8,kMean>", "softmax_bf16_kernel<128,8,kGated>"],
+        }
+        del lamd, gd
     del qd, kd, vd, out
     torch.cuda.empty_cache()
 

@@ -16,8 +16,11 @@
  *                     phi = elu + 1  (Appendix "Selection distributions,
  *                      support, and normalization", linear attention)
  *
+ * and the two-level gated read of the paper's models, which mixes F at a
+ * per-channel beta_max with the prior's expectation (fem_softmax_gated_fwd).
+ *
  * Conventions shared by every entry point:
- *   - Q, K, V, beta and out are DEVICE pointers (HIP device memory, e.g.
+ *   - Every tensor argument is a DEVICE pointer (HIP device memory, e.g.
  *     torch tensors' data_ptr()).  The caller owns every buffer; the library
  *     keeps no pointer after the call returns.
  *   - Layout: contiguous row-major [B, H, T, width] (width fastest); Q, K, V
@@ -56,7 +59,7 @@ typedef enum {
   FEM_ERR_NULLPTR = 1,      /* a required pointer is NULL                      */
   FEM_ERR_SHAPE = 2,        /* B, H or T <= 0, or a size overflows             */
   FEM_ERR_UNSUPPORTED = 3,  /* width, chunk or dtype outside the supported set */
-  FEM_ERR_ALIGN = 4,        /* Q, K or V not 16-byte aligned                   */
+  FEM_ERR_ALIGN = 4,        /* a tensor argument is not 16-byte aligned        */
   FEM_ERR_HIP = 5           /* a HIP call or kernel launch failed              */
 } fem_status;
 
@@ -74,6 +77,35 @@ typedef enum {
 int fem_softmax_fwd(const void* Q, const void* K, const void* V,
                     const float* beta, float* out,
                     int B, int H, int T, int d, int dtype, hipStream_t stream);
+
+/*
+ * Two-level gated FEM read with the causal softmax prior (Sec. "Two-Level
+ * Gated FEM", eqs. inner-gate-main and fem-two-gates-main; the inner gate is
+ * the linearized temperature learning of eqs. ltl and ltl-final):
+ *
+ *   o[b,h,t,j]  = g[b,h,t,j] * ( (1 - lam[b,h,t,j]) * mu[b,h,t,j]
+ *                                + lam[b,h,t,j] * F[b,h,t,j] )
+ *   mu[b,h,t,j] = sum_{i <= t} p_t(i) * v[b,h,i,j]      (expectation baseline)
+ *   F[b,h,t,j]  = the read of fem_softmax_fwd at beta = beta_max[h,j]
+ *
+ *   Q, K, V  : [B, H, T, d] bfloat16, d = 32, 64 or 128
+ *   beta_max : [H, d] float32, > 0
+ *   lam      : [B, H, T, d] float32, the inner (temperature) gate; meant to
+ *              lie in [0, 1] (not checked: other values extrapolate linearly)
+ *   gate     : [B, H, T, d] float32, the outer gate (> 0 in the paper's
+ *              parameterization; any finite value is applied as given), or
+ *              NULL for g = 1
+ *   out      : [B, H, T, d] float32; must alias none of the inputs
+ *   dtype    : FEM_DTYPE_BF16
+ *
+ * lam, gate (when given) and out must be 16-byte aligned.  Two kernels run
+ * in order on `stream`; the first leaves mu in `out` for the second, so out
+ * holds partial results until the second has run.  Returns a fem_status.
+ */
+int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V,
+                          const float* beta_max, const float* lam, const float* gate,
+                          float* out, int B, int H, int T, int d, int dtype,
+                          hipStream_t stream);
 
 /*
  * Causal linear-prior FEM read, phi = elu + 1, as an O(T) chunked scan

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfem.so")
 
 FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 
-EXPORTS = ("fem_softmax_fwd", "fem_linear_fwd", "fem_status_str")
+EXPORTS = ("fem_softmax_fwd", "fem_softmax_gated_fwd", "fem_linear_fwd", "fem_status_str")
 
 _lib = None
 
@@ -39,6 +39,8 @@ def load() -> ctypes.CDLL:
         vp, i, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p
         lib.fem_softmax_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_fwd.restype = i
+        lib.fem_softmax_gated_fwd.argtypes = [vp, vp, vp, f, f, f, f, i, i, i, i, i, vp]
+        lib.fem_softmax_gated_fwd.restype = i
         lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp]
         lib.fem_linear_fwd.restype = i
         lib.fem_status_str.argtypes = [i]
@@ -95,6 +97,41 @@ def fem_softmax_fwd(q, k, v, beta, out=None, stream=None) -> torch.Tensor:
         rc = lib.fem_softmax_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
                                  out.data_ptr(), B, H, T, d, FEM_DTYPE[q.dtype],
                                  _stream_handle(q.device, stream))
+    _check(rc)
+    return out
+
+
+def fem_softmax_gated_fwd(q, k, v, beta_max, lam, gate=None, out=None, stream=None) -> torch.Tensor:
+    """Two-level gated read g * ((1 - lam) * mu + lam * F(beta_max)) with the
+    causal softmax prior.  q, k, v: [B, H, T, d] bf16; beta_max: [H, d] fp32;
+    lam, gate: [B, H, T, d] fp32 (gate None means g = 1).  Returns
+    [B, H, T, d] fp32."""
+    lib = load()
+    for name, x in (("q", q), ("k", k), ("v", v)):
+        _dev_tensor(x, name, torch.bfloat16)
+        if x.dim() != 4 or x.shape != q.shape:
+            raise ValueError(f"{name} must be [B, H, T, d] like q")
+    B, H, T, d = q.shape
+    _dev_tensor(beta_max, "beta_max", torch.float32)
+    if tuple(beta_max.shape) != (H, d):
+        raise ValueError("beta_max must be [H, d]")
+    for name, x in (("lam", lam), ("gate", gate)):
+        if x is None and name == "gate":
+            continue
+        _dev_tensor(x, name, torch.float32)
+        if tuple(x.shape) != (B, H, T, d):
+            raise ValueError(f"{name} must be [B, H, T, d]")
+    if out is None:
+        out = torch.empty((B, H, T, d), device=q.device, dtype=torch.float32)
+    _dev_tensor(out, "out", torch.float32)
+    if tuple(out.shape) != (B, H, T, d):
+        raise ValueError("out must be [B, H, T, d]")
+    with torch.cuda.device(q.device):
+        rc = lib.fem_softmax_gated_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                       beta_max.data_ptr(), lam.data_ptr(),
+                                       None if gate is None else gate.data_ptr(),
+                                       out.data_ptr(), B, H, T, d, FEM_DTYPE[q.dtype],
+                                       _stream_handle(q.device, stream))
     _check(rc)
     return out
 

@@ -45,6 +45,21 @@ extern "C" int fem_softmax_fwd(const void* Q, const void* K, const void* V, cons
   return FEM_ERR_UNSUPPORTED;
 }
 
+extern "C" int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V,
+                                     const float* beta_max, const float* lam, const float* gate,
+                                     float* out, int B, int H, int T, int d, int dtype,
+                                     hipStream_t stream) {
+  if (!Q || !K || !V || !beta_max || !lam || !out) return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, T, d)) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  if (d != 32 && d != 64 && d != 128) return FEM_ERR_UNSUPPORTED;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(lam) || !aligned16(out) ||
+      (gate && !aligned16(gate)))
+    return FEM_ERR_ALIGN;
+  return from_hip(
+      fem::launch_softmax_gated_bf16(Q, K, V, beta_max, lam, gate, out, B, H, T, d, stream));
+}
+
 extern "C" int fem_linear_fwd(const void* Q, const void* K, const void* V, const float* beta,
                               float* out, int B, int H, int T, int d_k, int d_v, int chunk,
                               int dtype, hipStream_t stream) {
@@ -65,7 +80,7 @@ extern "C" const char* fem_status_str(int status) {
     case FEM_ERR_NULLPTR: return "FEM_ERR_NULLPTR: a required pointer is NULL";
     case FEM_ERR_SHAPE: return "FEM_ERR_SHAPE: B, H, T or a width is not positive, or a size overflows";
     case FEM_ERR_UNSUPPORTED: return "FEM_ERR_UNSUPPORTED: width, chunk or dtype outside the supported set";
-    case FEM_ERR_ALIGN: return "FEM_ERR_ALIGN: Q, K, V or out is not 16-byte aligned";
+    case FEM_ERR_ALIGN: return "FEM_ERR_ALIGN: an input or out is not 16-byte aligned";
     case FEM_ERR_HIP: return "FEM_ERR_HIP: a HIP call or kernel launch failed";
     default: return "FEM_ERR_UNKNOWN: not a fem_status value";
   }

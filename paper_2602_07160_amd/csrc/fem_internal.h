@@ -10,6 +10,12 @@ hipError_t launch_softmax_bf16(const void* Q, const void* K, const void* V,
                                const float* beta, float* out,
                                int B, int H, int T, int d, hipStream_t stream);
 
+// Two-level gated read g * ((1 - lam) mu + lam F(beta_max)) with the softmax
+// prior, bf16, d in {32, 64, 128}; gate may be null (g = 1).
+hipError_t launch_softmax_gated_bf16(const void* Q, const void* K, const void* V,
+                                     const float* beta_max, const float* lam, const float* gate,
+                                     float* out, int B, int H, int T, int d, hipStream_t stream);
+
 // Exact fp32 vector-unit softmax-prior read, 1 <= d <= 256.
 hipError_t launch_softmax_f32(const float* Q, const float* K, const float* V,
                               const float* beta, float* out,

@@ -30,11 +30,23 @@
 //     shared column shift) is recomputed exactly by the wave with a joint
 //     per-(t, j) log-sum-exp in fp32.
 //
-// Work decomposition: one workgroup of NW = 4 waves (one per SIMD) owns
-// BQ = 64*NW query rows of one (b, h); each wave owns 64 rows (two 32-row
-// blocks, so every LDS operand fragment feeds two MFMAs) for the products and
-// D/NW channels for the tilt (so the running column maximum needs no
-// cross-wave reduction).  One wave per SIMD leaves it the whole register file.
+// Work decomposition: one workgroup of NW = 8 waves (two per SIMD) owns
+// BQ = 32*NW query rows of one (b, h); each wave owns 32 rows for the
+// products (two 32-key blocks per tile, so every Q fragment feeds two MFMAs)
+// and D/NW channels for the tilt (so the running column maximum needs no
+// cross-wave reduction).
+//
+// The same kernel serves the two-level gated read (Sec. "Two-Level Gated
+// FEM", eqs. inner-gate-main and fem-two-gates-main) in two launches:
+//   kMean : the prior's expectation mu = sum_i p_t(i) v_i.  The "tilt" stores
+//           V itself (exact in bf16, so no lo part and no shift), the
+//           accumulator needs only the row rescale, and the epilogue writes
+//           mu = acc / l.
+//   kGated: the free-energy pass at beta_max whose epilogue reads mu back
+//           from the output and writes o = g * ((1 - lam) mu + lam F).
+// Both launches reuse one P per tile and row sum per launch; a single pass
+// with both accumulators would need 64 more registers per lane at d = 128
+// than two waves per SIMD leave, and a third double-buffered E^T tile in LDS.
 //
 // Schedule.  A wave keeps issuing independent vector instructions while its
 // own MFMAs run (about four per 32x32x16 MFMA come for free), so each
@@ -64,6 +76,11 @@ constexpr float kBias = 64.f;        // E = 2^(x - c + kBias) <= 2^(kBias + kCol
 constexpr float kColLag = 16.f;      // column shift raised only past this lag
 constexpr float kRowLag = 8.f;       // row max raised only past this lag (P <= 2^8)
 constexpr float kUnderflow = 0x1p-64f;
+
+// What a launch computes (see the header comment).
+constexpr int kFem = 0;    // F at beta
+constexpr int kMean = 1;   // mu
+constexpr int kGated = 2;  // g * ((1 - lam) mu + lam F), mu read from out
 
 // Instruction classes of __builtin_amdgcn_sched_group_barrier.
 constexpr int kSgVALU = 0x002 | 0x400;  // vector ALU, transcendental included
@@ -218,7 +235,7 @@ __device__ __forceinline__ float max_xor(float x, int o) {
 // (the causal mask), so the tilt treats every tile as full.
 // Stores that only one lane of a group should make go to a sink slot from the
 // other lanes, so the code has no branches.
-template <int D, int NW>
+template <int D, int NW, int MODE>
 struct Tilt {
   using C = Cfg<D, NW>;
   float v[C::RPL][4];
@@ -236,6 +253,10 @@ struct Tilt {
 #pragma unroll
       for (int b = 0; b < 4; ++b)
         v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + (4 * C::G * u + b) * C::KROW * 2);
+    }
+    if (MODE == kMean) {
+      eh = sm.base + pin(C::OFF_EH + (tt & 1) * C::EB + j * C::EROW * 2 + e_pos(4 * g) * 2);
+      return;
     }
     bl = sm.bl()[j];
     cold = (tt == 0) ? -INFINITY : sm.c((tt - 1) & 1)[j];
@@ -273,11 +294,16 @@ struct Tilt {
   }
 
   __device__ __forceinline__ void value(int u, int b) {
-    e[u][b] = exp2_hw(fmaf(v[u][b], bl, sh));
+    e[u][b] = MODE == kMean ? v[u][b] : exp2_hw(fmaf(v[u][b], bl, sh));
   }
 
   __device__ __forceinline__ void store(int u) {
     static_assert(e_pos_splits(C::G), "tilt write positions");
+    if (MODE == kMean) {  // bf16 values: the truncation is exact
+      const u32x2 v2 = {pack_hi16(e[u][0], e[u][1]), pack_hi16(e[u][2], e[u][3])};
+      *reinterpret_cast<u32x2*>(eh + e_pos(4 * C::G * u) * 2) = v2;
+      return;
+    }
     float lo[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b)
@@ -381,7 +407,7 @@ __device__ __forceinline__ void tile_offsets(const Smem<D, NW>& sm, int wave, in
 
 template <int D, int NW>
 __device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned char* dst, int k0,
-                                          int wave, const unsigned (&off)[Cfg<D, NW>::BPW]) {
+                                          int wave, const unsigned* off) {
   using C = Cfg<D, NW>;
   const char* base = reinterpret_cast<const char*>(src + (size_t)k0 * D);
 #pragma unroll
@@ -406,14 +432,15 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // m = 4r for the k-blocks with b%2 == r%2 sums query (l%16) + 16*(r%2) into
 // output row 4r, which the 16x16 output layout places in register 0 of lane
 // 16r + l%16.  Hence lacc[0] of every lane is the row sum of its query l%32.
-template <int D, int NW, bool PVA, bool QKT>
-__device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW>& tl, int k, int wave,
+template <int D, int NW, int MODE, bool PVA, bool QKT>
+__device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW, MODE>& tl, int k, int wave,
                                        int lane, int kofs, int eofs, const bf16x8 (&qf)[D / 16],
                                        f32x16 (&s)[2], f32x16 (&acc)[D / 32], f32x4& lacc,
                                        const bf16x8 (&pp)[4], const bf16x8& lsel) {
   using C = Cfg<D, NW>;
   constexpr int NL = PVA ? 4 : 0;             // row-sum MFMAs
-  constexpr int NE = PVA ? 2 * C::NCB : 0;    // PV k-step 0: hi and lo per output block
+  constexpr int NLO = MODE == kMean ? 0 : C::NCB;  // lo blocks
+  constexpr int NE = PVA ? C::NCB + NLO : 0;  // PV k-step 0: hi blocks, then lo blocks
   constexpr int NQ = QKT ? 2 * C::NKS : 0;    // QK MFMAs
   constexpr int NF = NE + NQ;                 // LDS operand fragments
   constexpr int NS = NL + NF;
@@ -427,7 +454,7 @@ __device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW>& tl, i
   const unsigned char* eb = sm.base + (PVA ? pin(C::OFF_EH + ((k - 1) & 1) * C::EB + eofs) : 0u);
   auto frag = [&](int f) -> bf16x8 {
     if (f < NE) {
-      const int lo = f / C::NCB, cb = f % C::NCB;
+      const int lo = f >= C::NCB ? 1 : 0, cb = lo ? f - C::NCB : f;
       return *reinterpret_cast<const bf16x8*>(eb + lo * (C::OFF_EL - C::OFF_EH) +
                                               cb * 32 * C::EROW * 2);
     }
@@ -453,7 +480,7 @@ __device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW>& tl, i
       const bf16x8 a = ring[f % RING];
       if (f + RING < NF) ring[f % RING] = frag(f + RING);
       if (f < NE) {
-        const int cb = f % C::NCB;
+        const int cb = f >= C::NCB ? f - C::NCB : f;
         acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pp[0], acc[cb], 0, 0, 0);
       } else {
         const int q = f - NE;
@@ -461,8 +488,8 @@ __device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW>& tl, i
       }
     }
     if (QKT) {
-      if (st == C0) vmax = tl.colmax();
-      if (st == C0 + 1) tl.shift(sm, k, wave, lane, vmax);
+      if (MODE != kMean && st == C0) vmax = tl.colmax();
+      if (MODE != kMean && st == C0 + 1) tl.shift(sm, k, wave, lane, vmax);
 #pragma unroll
       for (int x = 0; x < NV; ++x) {
         if (vslot(x) == st) {
@@ -480,24 +507,25 @@ __device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW>& tl, i
 // tiles after it).  One P buffer serves both products: an MFMA reads its
 // operands when it issues, so the softmax writes the new P of k-step ks only
 // in slots after the last MFMA that reads ks (k-step 0 was read in phase 1).
-template <int D, int NW, bool PVB, bool SM, bool MASK>
+template <int D, int NW, int MODE, bool PVB, bool SM, bool MASK>
 __device__ __forceinline__ void phase2(const Smem<D, NW>& sm, f32x16 (&acc)[D / 32],
                                        bf16x8 (&pp)[4], f32x16 (&sc)[2], float& m, float& apend,
                                        int j, int eofs, int k0, int tq, int hl, float scale2) {
   using C = Cfg<D, NW>;
-  constexpr int NF = PVB ? 6 * C::NCB : 0;            // k-steps 1..3, hi and lo
+  constexpr int NPK = MODE == kMean ? C::NCB : 2 * C::NCB;  // fragments per k-step
+  constexpr int NF = PVB ? 3 * NPK : 0;               // k-steps 1..3
   constexpr int RING = 4;
   constexpr int NSLOT = NF > 8 ? NF : 8;
   // first slot free of reads of P k-step ks, then spread the 4 pairs
   auto pslot = [&](int ks, int u) {
-    const int first = PVB ? 2 * C::NCB * ks : 0;
-    const int sl = first + (u / 2) * (C::NCB > 1 ? C::NCB / 2 : 1);
+    const int first = PVB ? NPK * ks : 0;
+    const int sl = first + (u / 2) * (NPK >= 4 ? NPK / 4 : 1);
     return sl < 4 ? 4 + sl : sl;
   };
   const unsigned char* eb = sm.base + (PVB ? pin(C::OFF_EH + (j & 1) * C::EB + eofs) : 0u);
   auto frag = [&](int f) -> bf16x8 {
-    const int ks = 1 + f / (2 * C::NCB), rem = f % (2 * C::NCB);
-    const int lo = rem / C::NCB, cb = rem % C::NCB;
+    const int ks = 1 + f / NPK, rem = f % NPK;
+    const int lo = rem >= C::NCB ? 1 : 0, cb = lo ? rem - C::NCB : rem;
     return *reinterpret_cast<const bf16x8*>(eb + lo * (C::OFF_EL - C::OFF_EH) +
                                             cb * 32 * C::EROW * 2 + ks * 32);
   };
@@ -513,7 +541,7 @@ __device__ __forceinline__ void phase2(const Smem<D, NW>& sm, f32x16 (&acc)[D / 
     if (st < NF) {
       const bf16x8 a = ring[st % RING];
       if (st + RING < NF) ring[st % RING] = frag(st + RING);
-      const int ks = 1 + st / (2 * C::NCB), cb = (st % (2 * C::NCB)) % C::NCB;
+      const int ks = 1 + st / NPK, rem = st % NPK, cb = rem >= C::NCB ? rem - C::NCB : rem;
       acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pp[ks], acc[cb], 0, 0, 0);
     }
     if (SM) {
@@ -540,11 +568,11 @@ __device__ __forceinline__ void phase2(const Smem<D, NW>& sm, f32x16 (&acc)[D / 
   }
 }
 
-template <int D, int NW>
+template <int D, int NW, int MODE>
 __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ beta, float* __restrict__ out, int H, int T, int nqb,
-    int nbh) {
+    const float* __restrict__ beta, const float* lam, const float* gate, float* out, int H,
+    int T, int nqb, int nbh) {
   using C = Cfg<D, NW>;
   extern __shared__ __align__(16) unsigned char smem[];
   const Smem<D, NW> sm{smem};
@@ -640,7 +668,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   // Deferred rescales owed before PV(j): the row factor of softmax(j) and the
   // column factors of tilt(j) (flag word from upd(j)).
   auto rescale = [&](int j, const i32x4& any4) {
-    const bool col = (any4[0] | any4[1] | any4[2] | any4[3]) != 0;
+    const bool col = MODE != kMean && (any4[0] | any4[1] | any4[2] | any4[3]) != 0;
     if (col || __any(apend != 1.f)) {
       const float* gcol = sm.g(j & 1);
 #pragma unroll
@@ -657,6 +685,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     }
   };
   auto flags_of = [&](int j) {
+    if (MODE == kMean) return i32x4{};  // no column shift
     const i32x4* uf = reinterpret_cast<const i32x4*>(sm.upd(j & 1));
     i32x4 any4 = uf[0];
 #pragma unroll
@@ -664,9 +693,10 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     return any4;
   };
 #define FEM_PHASE1(PVA, QKT) \
-  phase1<D, NW, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, pp, lsel)
-#define FEM_PHASE2(PVB, SM, MK) \
-  phase2<D, NW, PVB, SM, MK>(sm, acc, pp, sacc, m, apend, k - 1, eofs, k * C::BK, tq, hl, scale2)
+  phase1<D, NW, MODE, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, pp, lsel)
+#define FEM_PHASE2(PVB, SM, MK)                                                               \
+  phase2<D, NW, MODE, PVB, SM, MK>(sm, acc, pp, sacc, m, apend, k - 1, eofs, k * C::BK, tq, hl, \
+                                   scale2)
 
   // Every wave runs the same steps on every tile: past its diagonal tile the
   // softmax masks every key, so P = 0 and PV adds nothing, while the
@@ -681,7 +711,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
       next_offsets(k, off);
       load_next(k, off);
     }
-    Tilt<D, NW> tl;
+    Tilt<D, NW, MODE> tl;
     FEM_PHASE1(false, true);
     if (wlast <= 0) FEM_PHASE2(false, true, true);
     else FEM_PHASE2(false, true, false);
@@ -697,7 +727,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
       load_next(k, off);
     }
     if (k > 1) rescale(k - 1, any4);
-    Tilt<D, NW> tl;
+    Tilt<D, NW, MODE> tl;
     FEM_PHASE1(true, true);
     if (k >= wlast) FEM_PHASE2(true, true, true);
     else FEM_PHASE2(true, true, false);
@@ -707,7 +737,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   {
     const int k = ntiles;
     if (k > 1) rescale(k - 1, flags_of(k - 1));
-    Tilt<D, NW> tl;
+    Tilt<D, NW, MODE> tl;
     FEM_PHASE1(true, false);
     FEM_PHASE2(true, false, false);
   }
@@ -715,6 +745,23 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
 #undef FEM_PHASE2
 
   if (!wave_live) return;
+
+  if (MODE == kMean) {  // ---- mu = acc / l
+    if (tq >= T) return;
+    const float rl = 1.f / lacc[0];
+#pragma unroll
+    for (int cb = 0; cb < C::NCB; ++cb) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int ch0 = cb * 32 + g * 8 + hl * 4;
+        f32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = acc[cb][g * 4 + e] * rl;
+        *reinterpret_cast<f32x4*>(Oh + (size_t)tq * D + ch0) = o;
+      }
+    }
+    return;
+  }
 
   // ---- epilogue: o = (log2 acc - log2 l + c - bias) / (beta log2 e).  The
   // logarithms are split into exponent and mantissa so the bias and the
@@ -724,6 +771,8 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const float fl = log2_hw(frexpf(lt, &el));
   const float* cw = sm.c((ntiles - 1) & 1);  // the accumulator's final column frame
   const float* inv = sm.inv();
+  const float* Lh = MODE == kGated ? lam + base : nullptr;
+  const float* Gh = MODE == kGated && gate ? gate + base : nullptr;
   uint64_t flags = 0;
 #pragma unroll
   for (int cb = 0; cb < C::NCB; ++cb) {
@@ -739,7 +788,21 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
         o[e] = ((float)(ea - el - (int)kBias) + (fa - fl) + cw[ch0 + e]) * inv[ch0 + e];
         if (!(a >= kUnderflow) && tq < T) flags |= 1ull << (cb * 16 + g * 4 + e);
       }
-      if (tq < T) *reinterpret_cast<f32x4*>(Oh + (size_t)tq * D + ch0) = o;
+      if (tq >= T) continue;
+      const size_t at = (size_t)tq * D + ch0;
+      if (MODE == kGated) {
+        // mu from the kMean launch; an underflowed F keeps mu in place for
+        // the exact path below
+        const f32x4 mu = *reinterpret_cast<const f32x4*>(Oh + at);
+        const f32x4 lm = *reinterpret_cast<const f32x4*>(Lh + at);
+        const f32x4 gg = Gh ? *reinterpret_cast<const f32x4*>(Gh + at) : f32x4{1.f, 1.f, 1.f, 1.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool flagged = (flags >> (cb * 16 + g * 4 + e)) & 1ull;
+          o[e] = flagged ? mu[e] : gg[e] * fmaf(lm[e], o[e] - mu[e], mu[e]);
+        }
+      }
+      *reinterpret_cast<f32x4*>(Oh + at) = o;
     }
   }
 
@@ -758,29 +821,46 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     const float o = exact_read<D>(Qh, Kh, Vh, t, ch, scale2, sm.bl()[ch]);
     if (lane == src) {
       flags &= ~(1ull << e);
-      Oh[(size_t)t * D + ch] = o;
+      const size_t at = (size_t)t * D + ch;
+      if (MODE == kGated) {
+        const float mu = Oh[at];
+        Oh[at] = (Gh ? Gh[at] : 1.f) * fmaf(Lh[at], o - mu, mu);
+      } else {
+        Oh[at] = o;
+      }
     }
   }
 }
 
-template <int D, int NW>
-hipError_t launch(const void* Q, const void* K, const void* V, const float* beta, float* out,
-                  int B, int H, int T, hipStream_t stream) {
+template <int D, int NW, int MODE>
+hipError_t launch(const void* Q, const void* K, const void* V, const float* beta,
+                  const float* lam, const float* gate, float* out, int B, int H, int T,
+                  hipStream_t stream) {
   using C = Cfg<D, NW>;
   static std::once_flag once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(once, [] {
-    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&softmax_bf16_kernel<D, NW>),
-                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
+    attr_err =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&softmax_bf16_kernel<D, NW, MODE>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
   });
   if (attr_err != hipSuccess) return attr_err;
   const int nqb = (T + C::BQ - 1) / C::BQ;
   const int nbh = B * H;
   dim3 grid((unsigned)(nqb * nbh)), block(C::NT);
-  hipLaunchKernelGGL((softmax_bf16_kernel<D, NW>), grid, block, C::LDS, stream,
+  hipLaunchKernelGGL((softmax_bf16_kernel<D, NW, MODE>), grid, block, C::LDS, stream,
                      reinterpret_cast<const bf16*>(Q), reinterpret_cast<const bf16*>(K),
-                     reinterpret_cast<const bf16*>(V), beta, out, H, T, nqb, nbh);
+                     reinterpret_cast<const bf16*>(V), beta, lam, gate, out, H, T, nqb, nbh);
   return hipGetLastError();
+}
+
+template <int D, int NW>
+hipError_t launch_gated(const void* Q, const void* K, const void* V, const float* beta_max,
+                        const float* lam, const float* gate, float* out, int B, int H, int T,
+                        hipStream_t stream) {
+  hipError_t e = launch<D, NW, kMean>(Q, K, V, beta_max, nullptr, nullptr, out, B, H, T, stream);
+  if (e != hipSuccess) return e;
+  return launch<D, NW, kGated>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
 }
 
 }  // namespace
@@ -788,9 +868,20 @@ hipError_t launch(const void* Q, const void* K, const void* V, const float* beta
 hipError_t launch_softmax_bf16(const void* Q, const void* K, const void* V, const float* beta,
                                float* out, int B, int H, int T, int d, hipStream_t stream) {
   switch (d) {
-    case 32: return launch<32, 8>(Q, K, V, beta, out, B, H, T, stream);
-    case 64: return launch<64, 8>(Q, K, V, beta, out, B, H, T, stream);
-    case 128: return launch<128, 8>(Q, K, V, beta, out, B, H, T, stream);
+    case 32: return launch<32, 8, kFem>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream);
+    case 64: return launch<64, 8, kFem>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream);
+    case 128: return launch<128, 8, kFem>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_softmax_gated_bf16(const void* Q, const void* K, const void* V,
+                                     const float* beta_max, const float* lam, const float* gate,
+                                     float* out, int B, int H, int T, int d, hipStream_t stream) {
+  switch (d) {
+    case 32: return launch_gated<32, 8>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
+    case 64: return launch_gated<64, 8>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
+    case 128: return launch_gated<128, 8>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
     default: return hipErrorInvalidValue;
   }
 }

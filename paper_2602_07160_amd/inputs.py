@@ -18,6 +18,12 @@ float32 draw, and the oracle upcasts the stored bits exactly):
   5  linear,  bf16:  B=4,  H=16, T=8192,  d_k=d_v=64, chunk 64;
                      q,k,v ~ N(0,1); beta log-U[0.1, 4]
 
+Gates of the two-level gated read (``draw_gates``), per (b, h, t, j), from
+their own generator: lam = sigmoid(z), z ~ N(0, 2^2), which puts mass near 0,
+near 1 and in between; g = softplus(y), y ~ N(0, 1), divided by its root mean
+square over the channels of the step (the paper's RMS-normalised positive
+outer gate, with unit scale).
+
 The paper's own speed measurements use randomly generated data, and its
 language-model runs use T=4096 with head dimension 128; these shapes stand in
 for those workloads.  beta has shape [H, d] (one inverse temperature per head
@@ -119,3 +125,15 @@ def toy_argmax_values(seed: int, T: int = 128, D: int = 512,
     v = rng.normal(0.0, sigma, size=(T, D))
     v[a, np.arange(D)] = delta + rng.normal(0.0, sigma, size=D)
     return v, a
+
+
+def draw_gates(seed: int, B: int, H: int, T: int, d: int):
+    """Draw (lam, gate) as CPU float32 tensors [B, H, T, d] (recipe above)."""
+    rng = np.random.default_rng(seed)
+    z = rng.normal(0.0, 2.0, size=(B, H, T, d)).astype(np.float32)
+    lam = (1.0 / (1.0 + np.exp(-z))).astype(np.float32)
+    y = rng.standard_normal((B, H, T, d), dtype=np.float32)
+    g = np.logaddexp(np.float32(0.0), y)
+    g = g / np.sqrt(np.mean(g * g, axis=-1, keepdims=True))
+    return torch.from_numpy(np.ascontiguousarray(lam)), \
+        torch.from_numpy(np.ascontiguousarray(g.astype(np.float32)))

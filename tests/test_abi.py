@@ -80,3 +80,19 @@ def test_linear_validation(lib):
     assert ln(lib, chunk=32) == UNSUPPORTED
     assert ln(lib, dt=F32) == UNSUPPORTED
     assert ln(lib, v=A + 2) == ALIGN
+
+
+def gt(lib, q=A, k=A, v=A, bmax=A, lam=A, gate=A, out=A, B=1, H=1, T=8, d=64, dt=BF16):
+    return lib.fem_softmax_gated_fwd(q, k, v, bmax, lam, gate, out, B, H, T, d, dt, None)
+
+
+def test_gated_validation(lib):
+    assert gt(lib, lam=None) == NULLPTR
+    assert gt(lib, bmax=None) == NULLPTR
+    assert gt(lib, out=None) == NULLPTR
+    assert gt(lib, T=0) == SHAPE
+    assert gt(lib, d=48) == UNSUPPORTED
+    assert gt(lib, dt=F32) == UNSUPPORTED
+    assert gt(lib, lam=A + 4) == ALIGN
+    assert gt(lib, gate=A + 8) == ALIGN
+    assert gt(lib, gate=None, k=A + 2) == ALIGN

@@ -177,17 +177,26 @@ def test_bf16_scale_law(fem):
 
 
 def test_bf16_causality(fem):
-    say("bf16 causality: perturb keys/values after t=300, B1 H2 T640 d64")
+    """Keys and values after t = 300 must not enter rows t <= 300.  Exactly,
+    the perturbed run's rows <= 300 match the oracle of the unperturbed
+    inputs.  In rounding, they may move: the column shift is shared by the
+    256 rows of a workgroup, so a larger later value re-scales the earlier
+    terms (and can send an element to the exact path), which changes the
+    result by rounding only -- far below any leak of probability mass."""
+    say("bf16 causality: perturb keys/values after t=300, B1 H2 T640 d64, seed 3005/77")
     q, k, v, b = inputs.draw(3005, 1, 2, 640, 64, dtype="bf16")
     a = run(fem, q, k, v, b)
+    gen = torch.Generator().manual_seed(77)
     k2, v2 = k.clone(), v.clone()
-    k2[:, :, 301:] = (3 * torch.randn(k2[:, :, 301:].shape)).to(torch.bfloat16)
-    v2[:, :, 301:] = (3 * torch.randn(v2[:, :, 301:].shape)).to(torch.bfloat16)
+    k2[:, :, 301:] = (3 * torch.randn(k2[:, :, 301:].shape, generator=gen)).to(torch.bfloat16)
+    v2[:, :, 301:] = (3 * torch.randn(v2[:, :, 301:].shape, generator=gen)).to(torch.bfloat16)
     b2 = run(fem, q, k2, v2, b)
+    want = ref(q, k, v, b, rows=np.arange(301))
+    check(b2[:, :, :301], want, TOL_BF16, "perturbed run, rows <= 300")
     err = np.abs(a[:, :, :301] - b2[:, :, :301]).max()
     say(f"causality: rows <= 300 changed by {err:.3e}")
-    assert err <= 1e-5
-    assert np.abs(a[:, :, 301:] - b2[:, :, 301:]).max() > 1e-3
+    assert err <= 2e-3
+    assert np.abs(a[:, :, 301:] - b2[:, :, 301:]).max() > 1e-1
 
 
 def test_bf16_deterministic(fem):
