@@ -15,6 +15,8 @@ from .fem_oracle import (  # noqa: F401
     ltl_read,
     fem_softmax_ltl,
     fem_softmax,
+    fem_softmax_encoder,
+    softmax_prior_all,
     fem_linear,
     fem_linear_recurrent,
     posterior,

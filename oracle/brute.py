@@ -6,6 +6,8 @@ inputs (T up to a few dozen).  It pins the float64 oracle:
 
   s_{t,i} = q_t . k_i / sqrt(d)                     (Sec. 1, masked scores)
   alpha_{t,i} = exp(s_{t,i}) / sum_{r<=t} exp(s_{t,r})
+                 (encoder read: every key r < T, since encoder-only use
+                  removes the mask, Sec. "Empirical Evaluation")
   p_t(i) = <phi q_t, phi k_i> / sum_{r<=t} <phi q_t, phi k_r>, phi = elu + 1
   F_{t,j} = log( sum_{i<=t} p_t(i) exp(beta_j v_{i,j}) ) / beta_j
                                    (Sec. 2.3, eq. fem-free-energy-main)
@@ -21,7 +23,8 @@ def _phi(x):
 
 
 def brute_read(prior_rows, v, beta, dps=50):
-    """prior_rows[t] = list of p_t(i) for i <= t (mpf); v: T x D; beta: D."""
+    """prior_rows[t] = list of p_t(i) over the support (i <= t, or every i
+    for the encoder read) as mpf; v: T x D; beta: D."""
     with mpmath.workdps(dps):
         T = len(v)
         D = len(v[0])
@@ -31,21 +34,21 @@ def brute_read(prior_rows, v, beta, dps=50):
             for j in range(D):
                 b = mpmath.mpf(beta[j])
                 acc = mpmath.mpf(0)
-                for i in range(t + 1):
+                for i in range(len(prior_rows[t])):
                     acc += prior_rows[t][i] * mpmath.exp(b * mpmath.mpf(v[i][j]))
                 row.append(mpmath.log(acc) / b)
             out.append(row)
         return out
 
 
-def brute_softmax_prior(q, k, dps=50):
+def brute_softmax_prior(q, k, dps=50, causal=True):
     with mpmath.workdps(dps):
         T = len(q)
         d = len(q[0])
         rows = []
         for t in range(T):
             s = []
-            for i in range(t + 1):
+            for i in range(t + 1 if causal else T):
                 dot = mpmath.mpf(0)
                 for c in range(d):
                     dot += mpmath.mpf(q[t][c]) * mpmath.mpf(k[i][c])
@@ -75,6 +78,11 @@ def brute_linear_prior(q, k, dps=50):
 def brute_fem_softmax(q, k, v, beta, dps=50):
     """One head: q, k: T x d; v: T x D; beta: D (nested lists or arrays)."""
     return brute_read(brute_softmax_prior(q, k, dps), v, beta, dps)
+
+
+def brute_fem_softmax_encoder(q, k, v, beta, dps=50):
+    """Encoder (unmasked) read of one head."""
+    return brute_read(brute_softmax_prior(q, k, dps, causal=False), v, beta, dps)
 
 
 def brute_fem_linear(q, k, v, beta, dps=50):

@@ -13,6 +13,7 @@ Prior Selection", softmax prior):
   prior     p_t(i) = softmax over i <= t of  q_t . k_i / sqrt(d)      (softmax)
             p_t(i) = <phi(q_t), phi(k_i)> / sum_{r<=t} <phi(q_t), phi(k_r)>
                      with phi = elu + 1                                (linear)
+            p_t(i) = softmax over every i < T                  (encoder: no mask)
   read      F_{t,j} = (1 / beta_j) * log sum_{i<=t} p_t(i) * exp(beta_j v_{i,j})
                                   (free-energy read, eq. fem-free-energy-main)
   gated     o_{t,j} = g_{t,j} * ((1 - lam_{t,j}) * mu_{t,j} + lam_{t,j} * F_{t,j}(beta_max))
@@ -80,6 +81,25 @@ def softmax_logprior_rows(q: np.ndarray, k: np.ndarray, rows: np.ndarray) -> np.
     s = (q[rows] @ k[:n].T) / math.sqrt(d)
     mask = np.arange(n)[None, :] <= rows[:, None]
     s = np.where(mask, s, -np.inf)
+    m = s.max(axis=1, keepdims=True)
+    return s - (m + np.log(np.exp(s - m).sum(axis=1, keepdims=True)))
+
+
+def softmax_prior_all(q: np.ndarray, k: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """Encoder (unmasked) softmax prior: p_t(i) = softmax_i(q_t.k_i / sqrt d)
+    over every key i < T.  Encoder-only use removes the causal mask (opening of
+    Sec. "Empirical Evaluation"); otherwise as softmax_prior_rows."""
+    d = q.shape[1]
+    s = (q[rows] @ k.T) / math.sqrt(d)
+    s = s - s.max(axis=1, keepdims=True)
+    e = np.exp(s)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def softmax_logprior_all(q: np.ndarray, k: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """log p_t(i) of the encoder softmax prior."""
+    d = q.shape[1]
+    s = (q[rows] @ k.T) / math.sqrt(d)
     m = s.max(axis=1, keepdims=True)
     return s - (m + np.log(np.exp(s - m).sum(axis=1, keepdims=True)))
 
@@ -204,6 +224,26 @@ def fem_softmax(q, k, v, beta, rows=None, block: int = 512) -> np.ndarray:
                       softmax_logprior_rows(qq, kk, rr))
                 out[b, h, pos:pos + len(rb)] = free_energy_read(
                     p, v[b, h, :n], beta[h], logp=lp)
+                pos += len(rb)
+    return out
+
+
+def fem_softmax_encoder(q, k, v, beta, rows=None, block: int = 512) -> np.ndarray:
+    """FEM read with the unmasked (encoder) softmax prior: every query sees
+    all T keys.  Shapes as fem_softmax (d_v may differ from d)."""
+    q, k, v, beta = _as64(q), _as64(k), _as64(v), _as64(beta)
+    B, H, T, _ = q.shape
+    dv = v.shape[3]
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = np.empty((B, H, len(rows), dv))
+    for b in range(B):
+        for h in range(H):
+            pos = 0
+            for rb in _row_blocks(rows, block):
+                p = softmax_prior_all(q[b, h], k[b, h], rb)
+                lp = (lambda qq=q[b, h], kk=k[b, h], rr=rb:
+                      softmax_logprior_all(qq, kk, rr))
+                out[b, h, pos:pos + len(rb)] = free_energy_read(p, v[b, h], beta[h], logp=lp)
                 pos += len(rb)
     return out
 
