@@ -78,6 +78,38 @@ int fem_softmax_fwd(const void* Q, const void* K, const void* V,
                     const float* beta, float* out,
                     int B, int H, int T, int d, int dtype, hipStream_t stream);
 
+/* Option bits of fem_softmax_fwd_ex. */
+typedef enum {
+  FEM_FLAG_ENCODER = 1,  /* no causal mask: every query sees all T keys       */
+  FEM_FLAG_OUT_BF16 = 2  /* out is bfloat16 (round to nearest even), not fp32 */
+} fem_flags;
+
+/*
+ * Variants of the softmax-prior read (same definition as fem_softmax_fwd):
+ *
+ *   - FEM_FLAG_ENCODER: the encoder read, p_t(i) = softmax over every i < T
+ *     (encoder-only use removes the mask; Sec. "Empirical Evaluation").
+ *   - d_v != d_qk: budget (i) of Sec. "Free Energy Mixer" gives the values
+ *     half the key width.  The score scale stays 1/sqrt(d_qk).
+ *   - FEM_FLAG_OUT_BF16: bf16 output.  Its rounding adds up to 2^-9 |o| to
+ *     the read's own error.
+ *
+ *   Q, K     : [B, H, T, d_qk] bfloat16
+ *   V        : [B, H, T, d_v] bfloat16
+ *   beta     : [H, d_v] float32, > 0
+ *   out      : [B, H, T, d_v], float32 or (FEM_FLAG_OUT_BF16) bfloat16
+ *   (d_qk, d_v): (32, 32), (64, 64), (128, 128), (64, 32) or (128, 64)
+ *   flags    : an OR of fem_flags; other bits return FEM_ERR_UNSUPPORTED
+ *   dtype    : FEM_DTYPE_BF16
+ *
+ * With flags = 0 and d_qk = d_v this is fem_softmax_fwd's bf16 path.
+ * Returns a fem_status.
+ */
+int fem_softmax_fwd_ex(const void* Q, const void* K, const void* V,
+                       const float* beta, void* out,
+                       int B, int H, int T, int d_qk, int d_v, int flags,
+                       int dtype, hipStream_t stream);
+
 /*
  * Two-level gated FEM read with the causal softmax prior (Sec. "Two-Level
  * Gated FEM", eqs. inner-gate-main and fem-two-gates-main; the inner gate is

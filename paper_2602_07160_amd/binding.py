@@ -18,7 +18,11 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfem.so")
 
 FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 
-EXPORTS = ("fem_softmax_fwd", "fem_softmax_gated_fwd", "fem_linear_fwd", "fem_status_str")
+EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_gated_fwd", "fem_linear_fwd",
+           "fem_status_str")
+
+FEM_FLAG_ENCODER = 1
+FEM_FLAG_OUT_BF16 = 2
 
 _lib = None
 
@@ -39,6 +43,8 @@ def load() -> ctypes.CDLL:
         vp, i, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p
         lib.fem_softmax_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_fwd.restype = i
+        lib.fem_softmax_fwd_ex.argtypes = [vp, vp, vp, f, vp, i, i, i, i, i, i, i, vp]
+        lib.fem_softmax_fwd_ex.restype = i
         lib.fem_softmax_gated_fwd.argtypes = [vp, vp, vp, f, f, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_gated_fwd.restype = i
         lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp]
@@ -97,6 +103,40 @@ def fem_softmax_fwd(q, k, v, beta, out=None, stream=None) -> torch.Tensor:
         rc = lib.fem_softmax_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
                                  out.data_ptr(), B, H, T, d, FEM_DTYPE[q.dtype],
                                  _stream_handle(q.device, stream))
+    _check(rc)
+    return out
+
+
+def fem_softmax_fwd_ex(q, k, v, beta, out=None, causal: bool = True, out_dtype=torch.float32,
+                       stream=None) -> torch.Tensor:
+    """Variants of the softmax-prior read: causal or encoder (all keys),
+    d_v = d_qk or d_qk / 2, fp32 or bf16 output.  q, k: [B, H, T, d_qk] bf16;
+    v: [B, H, T, d_v] bf16; beta: [H, d_v] fp32.  Returns [B, H, T, d_v]."""
+    lib = load()
+    for name, x in (("q", q), ("k", k), ("v", v)):
+        _dev_tensor(x, name, torch.bfloat16)
+        if x.dim() != 4:
+            raise ValueError(f"{name} must be [B, H, T, width]")
+    if k.shape != q.shape or v.shape[:3] != q.shape[:3]:
+        raise ValueError("q, k must be [B, H, T, d_qk] and v [B, H, T, d_v]")
+    B, H, T, dqk = q.shape
+    dv = v.shape[3]
+    _dev_tensor(beta, "beta", torch.float32)
+    if tuple(beta.shape) != (H, dv):
+        raise ValueError("beta must be [H, d_v]")
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be float32 or bfloat16")
+    if out is None:
+        out = torch.empty((B, H, T, dv), device=q.device, dtype=out_dtype)
+    _dev_tensor(out, "out", out_dtype)
+    if tuple(out.shape) != (B, H, T, dv):
+        raise ValueError("out must be [B, H, T, d_v]")
+    flags = (0 if causal else FEM_FLAG_ENCODER) | \
+        (FEM_FLAG_OUT_BF16 if out_dtype == torch.bfloat16 else 0)
+    with torch.cuda.device(q.device):
+        rc = lib.fem_softmax_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
+                                    out.data_ptr(), B, H, T, dqk, dv, flags, FEM_DTYPE[q.dtype],
+                                    _stream_handle(q.device, stream))
     _check(rc)
     return out
 

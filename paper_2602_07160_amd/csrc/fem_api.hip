@@ -45,6 +45,22 @@ extern "C" int fem_softmax_fwd(const void* Q, const void* K, const void* V, cons
   return FEM_ERR_UNSUPPORTED;
 }
 
+extern "C" int fem_softmax_fwd_ex(const void* Q, const void* K, const void* V, const float* beta,
+                                  void* out, int B, int H, int T, int d_qk, int d_v, int flags,
+                                  int dtype, hipStream_t stream) {
+  if (!Q || !K || !V || !beta || !out) return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, T, d_qk) || !sizes_ok(B, H, T, d_v)) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  if (flags & ~(FEM_FLAG_ENCODER | FEM_FLAG_OUT_BF16)) return FEM_ERR_UNSUPPORTED;
+  const bool pair_ok = (d_qk == d_v && (d_v == 32 || d_v == 64 || d_v == 128)) ||
+                       (d_qk == 2 * d_v && (d_v == 32 || d_v == 64));
+  if (!pair_ok) return FEM_ERR_UNSUPPORTED;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return FEM_ERR_ALIGN;
+  return from_hip(fem::launch_softmax_ex_bf16(Q, K, V, beta, out, B, H, T, d_qk, d_v,
+                                              !(flags & FEM_FLAG_ENCODER),
+                                              (flags & FEM_FLAG_OUT_BF16) != 0, stream));
+}
+
 extern "C" int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V,
                                      const float* beta_max, const float* lam, const float* gate,
                                      float* out, int B, int H, int T, int d, int dtype,

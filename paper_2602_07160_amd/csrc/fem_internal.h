@@ -10,6 +10,12 @@ hipError_t launch_softmax_bf16(const void* Q, const void* K, const void* V,
                                const float* beta, float* out,
                                int B, int H, int T, int d, hipStream_t stream);
 
+// The plain read's variants: (dk, dv) in {(32,32), (64,64), (128,128),
+// (64,32), (128,64)}, causal or encoder (all keys), fp32 or bf16 output.
+hipError_t launch_softmax_ex_bf16(const void* Q, const void* K, const void* V, const float* beta,
+                                  void* out, int B, int H, int T, int dk, int dv, bool causal,
+                                  bool obf16, hipStream_t stream);
+
 // Two-level gated read g * ((1 - lam) mu + lam F(beta_max)) with the softmax
 // prior, bf16, d in {32, 64, 128}; gate may be null (g = 1).
 hipError_t launch_softmax_gated_bf16(const void* Q, const void* K, const void* V,

@@ -90,41 +90,53 @@ constexpr int kSgDSRead = 0x100;
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
 
-template <int D, int NW>
+// Compile-time shape and variant of a launch: the width of Q and K (DK) and
+// of V and the output (DV), the waves per workgroup, what the launch computes
+// (MODE), causal or encoder (all keys) read, and fp32 or bf16 output.
+template <int DK_, int DV_, int NW_, int MODE_, bool CAUSAL_ = true, bool OBF16_ = false>
 struct Cfg {
+  static constexpr int DK = DK_, DV = DV_, NW = NW_, MODE = MODE_;
+  static constexpr bool CAUSAL = CAUSAL_, OBF16 = OBF16_;
   static constexpr int BQ = NW * 32;      // query rows per workgroup
   static constexpr int BK = 64;           // keys per tile
   static constexpr int NT = NW * 64;      // threads
-  static constexpr int NCB = D / 32;      // 32-channel output blocks
-  static constexpr int NKS = D / 16;      // 16-wide k-steps of Q K^T
-  static constexpr int KROW = D + 8;      // K / V tile row stride (bf16): one 16-byte pad slot
+  static constexpr int NCB = DV / 32;     // 32-channel output blocks
+  static constexpr int NKS = DK / 16;     // 16-wide k-steps of Q K^T
+  static constexpr int KROW = DK + 8;     // K tile row stride (bf16): one 16-byte pad slot
+  static constexpr int VROW = DV + 8;     // V tile row stride (bf16)
   static constexpr int EROW = BK + 8;     // E^T row stride (bf16), +16 B pad
-  static constexpr int CPW = D / NW;      // channels tilted per wave
+  static constexpr int CPW = DV / NW;     // channels tilted per wave
   static constexpr int G = 64 / CPW;      // lanes per channel in the tilt
   static constexpr int RPL = 16 / G;      // 4-key runs per tilt lane
   // K / V tiles are filled by direct global->LDS loads: each wave instruction
-  // writes 64 consecutive 16-byte slots (1 KiB); a padded row is SPR slots.
-  static constexpr int SPR = KROW / 8;               // slots per padded row
-  static constexpr int BLOCKS = BK * SPR / 64;       // 1 KiB blocks per tile
-  static constexpr int BPW = (BLOCKS + NW - 1) / NW; // blocks per wave
+  // writes 64 consecutive 16-byte slots (1 KiB); a padded row is (W+8)/8 slots.
+  static constexpr int BLOCKSK = BK * (KROW / 8) / 64;  // 1 KiB blocks per K tile
+  static constexpr int BLOCKSV = BK * (VROW / 8) / 64;  // ... per V tile
+  static constexpr int BPWK = (BLOCKSK + NW - 1) / NW;  // blocks per wave
+  static constexpr int BPWV = (BLOCKSV + NW - 1) / NW;
+  static constexpr bool SAME = DK == DV;  // K and V tiles share their load offsets
   // LDS layout (bytes)
   static constexpr int KB = BK * KROW * 2;
-  static constexpr int EB = D * EROW * 2;
+  static constexpr int VB = BK * VROW * 2;
+  static constexpr int EB = DV * EROW * 2;
   static constexpr int OFF_K = 0;                 // 2 buffers
   static constexpr int OFF_V = OFF_K + 2 * KB;    // 2 buffers
-  static constexpr int OFF_EH = OFF_V + 2 * KB;   // 2 buffers
+  static constexpr int OFF_EH = OFF_V + 2 * VB;   // 2 buffers
   static constexpr int OFF_EL = OFF_EH + 2 * EB;  // 2 buffers
   static constexpr int OFF_F = OFF_EL + 2 * EB;   // floats
-  static constexpr int NF = D /*bl*/ + D /*inv*/ + 2 * D /*c*/ + 2 * D /*g*/ + 64 /*sink*/;
+  static constexpr int NF = DV /*bl*/ + DV /*inv*/ + 2 * DV /*c*/ + 2 * DV /*g*/ + 64 /*sink*/;
   static constexpr int OFF_R = OFF_F + NF * 4;    // column-update flags [2][NW]
-  static constexpr int OFF_T = OFF_R + 2 * NW * 4;  // tile-load lane offsets [NW][64][TW]
-  static constexpr int TW = (BPW + 3) / 4 * 4;
+  // tile-load lane offsets [NW][64][TW]: K tile, then V tile unless SAME
+  static constexpr int OFF_T = OFF_R + 2 * NW * 4;
+  static constexpr int TWK = (BPWK + 3) / 4 * 4;
+  static constexpr int TW = TWK + (SAME ? 0 : (BPWV + 3) / 4 * 4);
   static constexpr size_t LDS = OFF_T + NW * 64 * TW * 4;
-  static_assert(CPW * NW == D && G * CPW == 64 && RPL * G == 16, "tilt mapping");
-  static_assert(BK * SPR % 64 == 0, "tile = whole 1 KiB blocks");
+  static_assert(CPW * NW == DV && G * CPW == 64 && RPL * G == 16, "tilt mapping");
+  static_assert(DK % 32 == 0 && DV % 32 == 0, "widths");
   static_assert(NW % 4 == 0, "flags are read as int4");
   static_assert(LDS <= 160 * 1024, "LDS budget");
-  static_assert(OFF_EL - OFF_EH + D * EROW * 2 < 65536, "hi and lo share a base register");
+  static_assert(OFF_EL - OFF_EH + EB < 65536, "hi and lo share a base register");
+  static_assert(!OBF16 || MODE == kFem, "bf16 output only for the plain read");
 };
 
 // Position of key r (0..63 within a tile) inside an E^T row.  Within each
@@ -155,48 +167,50 @@ __device__ __forceinline__ unsigned pin(unsigned x) {
 }
 
 // Exact fp32 read of one (t, j) by the whole wave: joint log-sum-exp of
-// (score + tilt) over i <= t, minus the log-sum-exp of the scores.
-template <int D>
+// (score + tilt) over the keys i < n, minus the log-sum-exp of the scores.
+template <class C>
 __device__ float exact_read(const bf16* __restrict__ Qh, const bf16* __restrict__ Kh,
-                            const bf16* __restrict__ Vh, int t, int j, float scale2,
+                            const bf16* __restrict__ Vh, int t, int n, int j, float scale2,
                             float bl) {
   const int lane = threadIdx.x & 63;
   Lse2 num, den;
-  const bf16x8* qrow = reinterpret_cast<const bf16x8*>(Qh + (size_t)t * D);
-  for (int i = lane; i <= t; i += 64) {
-    const bf16x8* krow = reinterpret_cast<const bf16x8*>(Kh + (size_t)i * D);
+  const bf16x8* qrow = reinterpret_cast<const bf16x8*>(Qh + (size_t)t * C::DK);
+  for (int i = lane; i < n; i += 64) {
+    const bf16x8* krow = reinterpret_cast<const bf16x8*>(Kh + (size_t)i * C::DK);
     float dot = 0.f;
 #pragma unroll 4
-    for (int c = 0; c < D / 8; ++c) {
+    for (int c = 0; c < C::DK / 8; ++c) {
       bf16x8 a = qrow[c], b = krow[c];
 #pragma unroll
       for (int e = 0; e < 8; ++e) dot += (float)a[e] * (float)b[e];
     }
     const float s = dot * scale2;
     den.add(s);
-    num.add(s + (float)Vh[(size_t)i * D + j] * bl);
+    num.add(s + (float)Vh[(size_t)i * C::DV + j] * bl);
   }
   return (num.wave_total() - den.wave_total()) / bl;
 }
 
-template <int D, int NW>
+template <class C>
 struct Smem {
-  using C = Cfg<D, NW>;
+  static constexpr int DV = C::DV;
   unsigned char* base;
   __device__ unsigned char* k(int b) const { return base + C::OFF_K + b * C::KB; }
-  __device__ unsigned char* v(int b) const { return base + C::OFF_V + b * C::KB; }
+  __device__ unsigned char* v(int b) const { return base + C::OFF_V + b * C::VB; }
   __device__ unsigned char* eh(int b) const { return base + C::OFF_EH + b * C::EB; }
   __device__ unsigned char* el(int b) const { return base + C::OFF_EL + b * C::EB; }
   __device__ float* bl() const { return reinterpret_cast<float*>(base + C::OFF_F); }
-  __device__ float* inv() const { return bl() + D; }
-  __device__ float* c(int b) const { return bl() + 2 * D + b * D; }
-  __device__ float* g(int b) const { return bl() + 4 * D + b * D; }
+  __device__ float* inv() const { return bl() + DV; }
+  __device__ float* c(int b) const { return bl() + 2 * DV + b * DV; }
+  __device__ float* g(int b) const { return bl() + 4 * DV + b * DV; }
   // Write-only slots for lanes whose store would otherwise need a branch.
-  __device__ float* sink() const { return bl() + 6 * D; }
-  __device__ int* upd(int b) const { return reinterpret_cast<int*>(base + C::OFF_R) + b * NW; }
+  __device__ float* sink() const { return bl() + 6 * DV; }
+  __device__ int* upd(int b) const { return reinterpret_cast<int*>(base + C::OFF_R) + b * C::NW; }
+  // this lane's offsets of a whole K tile; those of a V tile follow unless SAME
   __device__ unsigned* ltab(int w, int l) const {
     return reinterpret_cast<unsigned*>(base + C::OFF_T) + (w * 64 + l) * C::TW;
   }
+  __device__ unsigned* ltabv(int w, int l) const { return ltab(w, l) + (C::SAME ? 0 : C::TWK); }
 };
 
 // Bits of two floats' upper halves packed into one dword (bf16 truncation).
@@ -235,24 +249,24 @@ __device__ __forceinline__ float max_xor(float x, int o) {
 // (the causal mask), so the tilt treats every tile as full.
 // Stores that only one lane of a group should make go to a sink slot from the
 // other lanes, so the code has no branches.
-template <int D, int NW, int MODE>
+template <class C>
 struct Tilt {
-  using C = Cfg<D, NW>;
+  static constexpr int MODE = C::MODE;
   float v[C::RPL][4];
   float e[C::RPL][4];
   float bl, cold, cnew, sh;
   unsigned char* eh;
 
-  __device__ __forceinline__ void read(const Smem<D, NW>& sm, int tt, int wave, int lane) {
+  __device__ __forceinline__ void read(const Smem<C>& sm, int tt, int wave, int lane) {
     const int jj = lane % C::CPW, g = lane / C::CPW;
     const int j = wave * C::CPW + jj;
     const unsigned char* sv =
-        sm.base + pin(C::OFF_V + (tt & 1) * C::KB + j * 2 + 4 * g * C::KROW * 2);
+        sm.base + pin(C::OFF_V + (tt & 1) * C::VB + j * 2 + 4 * g * C::VROW * 2);
 #pragma unroll
     for (int u = 0; u < C::RPL; ++u) {
 #pragma unroll
       for (int b = 0; b < 4; ++b)
-        v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + (4 * C::G * u + b) * C::KROW * 2);
+        v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + (4 * C::G * u + b) * C::VROW * 2);
     }
     if (MODE == kMean) {
       eh = sm.base + pin(C::OFF_EH + (tt & 1) * C::EB + j * C::EROW * 2 + e_pos(4 * g) * 2);
@@ -278,7 +292,7 @@ struct Tilt {
     return x;
   }
 
-  __device__ __forceinline__ void shift(const Smem<D, NW>& sm, int tt, int wave, int lane,
+  __device__ __forceinline__ void shift(const Smem<C>& sm, int tt, int wave, int lane,
                                         float vmax) {
     const int jj = lane % C::CPW, g = lane / C::CPW;
     const int j = wave * C::CPW + jj;
@@ -388,32 +402,29 @@ struct Softmax {
 // use scalar-base addressing.  The lane offsets of a whole tile (no clamping)
 // are computed once into an LDS table (tile_offsets) and read back per tile,
 // rather than held in registers across the loop.
-template <int D, int NW>
+template <int W, int NW>
 __device__ __forceinline__ unsigned tile_offset(int u, int k0, int T, int wave, int lane) {
-  using C = Cfg<D, NW>;
+  constexpr int SPR = (W + 8) / 8;  // 16-byte slots per padded row
   const int slot = (wave + NW * u) * 64 + lane;
-  const int row = min(slot / C::SPR, T - 1 - k0), chunk = slot % C::SPR;
-  return (unsigned)(row * D + (chunk < D / 8 ? chunk * 8 : 0)) * 2u;
+  const int row = min(slot / SPR, T - 1 - k0), chunk = slot % SPR;
+  return (unsigned)(row * W + (chunk < W / 8 ? chunk * 8 : 0)) * 2u;
 }
 
-template <int D, int NW>
-__device__ __forceinline__ void tile_offsets(const Smem<D, NW>& sm, int wave, int lane,
-                                             unsigned (&off)[Cfg<D, NW>::BPW]) {
-  using C = Cfg<D, NW>;
-  const unsigned* t = sm.ltab(wave, lane);
+template <int BPW>
+__device__ __forceinline__ void tile_offsets(const unsigned* t, unsigned* off) {
 #pragma unroll
-  for (int u = 0; u < C::BPW; ++u) off[u] = t[u];
+  for (int u = 0; u < BPW; ++u) off[u] = t[u];
 }
 
-template <int D, int NW>
+template <int W, int NW, int BPW>
 __device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned char* dst, int k0,
                                           int wave, const unsigned* off) {
-  using C = Cfg<D, NW>;
-  const char* base = reinterpret_cast<const char*>(src + (size_t)k0 * D);
+  constexpr int BLOCKS = 64 * ((W + 8) / 8) / 64;
+  const char* base = reinterpret_cast<const char*>(src + (size_t)k0 * W);
 #pragma unroll
-  for (int u = 0; u < C::BPW; ++u) {
+  for (int u = 0; u < BPW; ++u) {
     const int blk = wave + NW * u;
-    if (C::BLOCKS % NW == 0 || blk < C::BLOCKS)
+    if (BLOCKS % NW == 0 || blk < BLOCKS)
       __builtin_amdgcn_global_load_lds(base + off[u], dst + blk * 1024, 16, 0, 0);
   }
 }
@@ -432,12 +443,12 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // m = 4r for the k-blocks with b%2 == r%2 sums query (l%16) + 16*(r%2) into
 // output row 4r, which the 16x16 output layout places in register 0 of lane
 // 16r + l%16.  Hence lacc[0] of every lane is the row sum of its query l%32.
-template <int D, int NW, int MODE, bool PVA, bool QKT>
-__device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW, MODE>& tl, int k, int wave,
-                                       int lane, int kofs, int eofs, const bf16x8 (&qf)[D / 16],
-                                       f32x16 (&s)[2], f32x16 (&acc)[D / 32], f32x4& lacc,
+template <class C, bool PVA, bool QKT>
+__device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, int wave, int lane,
+                                       int kofs, int eofs, const bf16x8 (&qf)[C::NKS],
+                                       f32x16 (&s)[2], f32x16 (&acc)[C::NCB], f32x4& lacc,
                                        const bf16x8 (&pp)[4], const bf16x8& lsel) {
-  using C = Cfg<D, NW>;
+  constexpr int MODE = C::MODE;
   constexpr int NL = PVA ? 4 : 0;             // row-sum MFMAs
   constexpr int NLO = MODE == kMean ? 0 : C::NCB;  // lo blocks
   constexpr int NE = PVA ? C::NCB + NLO : 0;  // PV k-step 0: hi blocks, then lo blocks
@@ -507,11 +518,11 @@ __device__ __forceinline__ void phase1(const Smem<D, NW>& sm, Tilt<D, NW, MODE>&
 // tiles after it).  One P buffer serves both products: an MFMA reads its
 // operands when it issues, so the softmax writes the new P of k-step ks only
 // in slots after the last MFMA that reads ks (k-step 0 was read in phase 1).
-template <int D, int NW, int MODE, bool PVB, bool SM, bool MASK>
-__device__ __forceinline__ void phase2(const Smem<D, NW>& sm, f32x16 (&acc)[D / 32],
+template <class C, bool PVB, bool SM, bool MASK>
+__device__ __forceinline__ void phase2(const Smem<C>& sm, f32x16 (&acc)[C::NCB],
                                        bf16x8 (&pp)[4], f32x16 (&sc)[2], float& m, float& apend,
                                        int j, int eofs, int k0, int tq, int hl, float scale2) {
-  using C = Cfg<D, NW>;
+  constexpr int MODE = C::MODE;
   constexpr int NPK = MODE == kMean ? C::NCB : 2 * C::NCB;  // fragments per k-step
   constexpr int NF = PVB ? 3 * NPK : 0;               // k-steps 1..3
   constexpr int RING = 4;
@@ -568,14 +579,14 @@ __device__ __forceinline__ void phase2(const Smem<D, NW>& sm, f32x16 (&acc)[D / 
   }
 }
 
-template <int D, int NW, int MODE>
-__global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
+template <class C>
+__global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ beta, const float* lam, const float* gate, float* out, int H,
     int T, int nqb, int nbh) {
-  using C = Cfg<D, NW>;
+  constexpr int MODE = C::MODE;
   extern __shared__ __align__(16) unsigned char smem[];
-  const Smem<D, NW> sm{smem};
+  const Smem<C> sm{smem};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -588,14 +599,16 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const int bh = bid % nbh;
   const int h = bh % H;
   const int q0 = qblk * C::BQ;
-  const size_t base = (size_t)bh * T * D;
-  const bf16* Qh = Q + base;
-  const bf16* Kh = K + base;
+  const size_t baseq = (size_t)bh * T * C::DK;  // Q, K
+  const size_t base = (size_t)bh * T * C::DV;   // V, out, lam, gate
+  const bf16* Qh = Q + baseq;
+  const bf16* Kh = K + baseq;
   const bf16* Vh = V + base;
   float* Oh = out + base;
+  bf16* Ob = reinterpret_cast<bf16*>(out) + base;
 
-  for (int j = tid; j < D; j += C::NT) {
-    const float bl = beta[h * D + j] * kLog2e;
+  for (int j = tid; j < C::DV; j += C::NT) {
+    const float bl = beta[h * C::DV + j] * kLog2e;
     sm.bl()[j] = bl;
     sm.inv()[j] = 1.f / bl;
   }
@@ -604,28 +617,41 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   const int tq = wq0 + n;          // this lane's query row
   const bool wave_live = wq0 < T;
   const int qlast = min(q0 + C::BQ, T) - 1;
-  const int ntiles = qlast / C::BK + 1;
-  // The tile holding the wave's diagonal.  The wave's first row is a multiple
-  // of 32, which divides the tile size, so earlier tiles lie wholly below the
-  // wave's rows and need no causal mask; this and later tiles are masked.
-  const int wlast = wave_live ? min((wq0 + 31) / C::BK, ntiles - 1) : -1;
+  // last key a lane's row may see: its own row (causal) or the last key
+  const int tm = C::CAUSAL ? tq : T - 1;
+  const int ntiles = (C::CAUSAL ? qlast : T - 1) / C::BK + 1;
+  // The first masked tile.  Causal: the tile holding the wave's diagonal (the
+  // wave's first row is a multiple of 32, which divides the tile size, so
+  // earlier tiles lie wholly below the wave's rows); encoder read: the last
+  // tile, whose keys at or past T are masked.
+  const int wlast = !wave_live ? -1
+                    : C::CAUSAL ? min((wq0 + 31) / C::BK, ntiles - 1)
+                                : ntiles - 1;
 
   {
-    unsigned off[C::BPW];
+    unsigned offk[C::BPWK], offv[C::BPWV];
 #pragma unroll
-    for (int u = 0; u < C::BPW; ++u) {
-      off[u] = tile_offset<D, NW>(u, 0, T, wave, lane);
-      sm.ltab(wave, lane)[u] = tile_offset<D, NW>(u, 0, 1 << 30, wave, lane);
+    for (int u = 0; u < C::BPWK; ++u) {
+      offk[u] = tile_offset<C::DK, C::NW>(u, 0, T, wave, lane);
+      sm.ltab(wave, lane)[u] = tile_offset<C::DK, C::NW>(u, 0, 1 << 30, wave, lane);
     }
-    load_tile<D, NW>(Kh, sm.k(0), 0, wave, off);
-    load_tile<D, NW>(Vh, sm.v(0), 0, wave, off);
+    if (!C::SAME) {
+#pragma unroll
+      for (int u = 0; u < C::BPWV; ++u) {
+        offv[u] = tile_offset<C::DV, C::NW>(u, 0, T, wave, lane);
+        sm.ltabv(wave, lane)[u] = tile_offset<C::DV, C::NW>(u, 0, 1 << 30, wave, lane);
+      }
+    }
+    load_tile<C::DK, C::NW, C::BPWK>(Kh, sm.k(0), 0, wave, offk);
+    load_tile<C::DV, C::NW, C::BPWV>(Vh, sm.v(0), 0, wave, C::SAME ? offk : offv);
   }
   bf16x8 qf[C::NKS];
 #pragma unroll
   for (int ks = 0; ks < C::NKS; ++ks) {
     bf16x8 z = {};
-    qf[ks] = (tq < T) ? *reinterpret_cast<const bf16x8*>(Qh + (size_t)tq * D + ks * 16 + hl * 8)
-                      : z;
+    qf[ks] = (tq < T)
+                 ? *reinterpret_cast<const bf16x8*>(Qh + (size_t)tq * C::DK + ks * 16 + hl * 8)
+                 : z;
   }
   wait_vmem();
   __syncthreads();
@@ -645,25 +671,31 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
 #pragma unroll
     for (int e = 0; e < 8; ++e) lsel[e] = one;
   }
-  const float scale2 = kLog2e / sqrtf((float)D);
+  const float scale2 = kLog2e / sqrtf((float)C::DK);
   const int kofs = n * C::KROW * 2 + hl * 16;  // lane part of K fragment addresses
   const int eofs = n * C::EROW * 2 + hl * 16;  // lane part of E fragment addresses
 
   // The lane offsets of the next tile's loads: the table, or clamped rows for
   // the last tile.
-  auto next_offsets = [&](int k, unsigned (&off)[C::BPW]) {
+  auto next_offsets = [&](int k, unsigned* offk, unsigned* offv) {
     const int kn = (k + 1) * C::BK;
     if (kn + C::BK <= T) {
-      tile_offsets<D, NW>(sm, wave, lane, off);
+      tile_offsets<C::BPWK>(sm.ltab(wave, lane), offk);
+      if (!C::SAME) tile_offsets<C::BPWV>(sm.ltabv(wave, lane), offv);
     } else {  // last tile: rows at or past T read row T-1
 #pragma unroll
-      for (int u = 0; u < C::BPW; ++u) off[u] = tile_offset<D, NW>(u, kn, T, wave, lane);
+      for (int u = 0; u < C::BPWK; ++u) offk[u] = tile_offset<C::DK, C::NW>(u, kn, T, wave, lane);
+      if (!C::SAME) {
+#pragma unroll
+        for (int u = 0; u < C::BPWV; ++u)
+          offv[u] = tile_offset<C::DV, C::NW>(u, kn, T, wave, lane);
+      }
     }
   };
-  auto load_next = [&](int k, const unsigned (&off)[C::BPW]) {
+  auto load_next = [&](int k, const unsigned* offk, const unsigned* offv) {
     const int kn = (k + 1) * C::BK;
-    load_tile<D, NW>(Kh, sm.k((k + 1) & 1), kn, wave, off);
-    load_tile<D, NW>(Vh, sm.v((k + 1) & 1), kn, wave, off);
+    load_tile<C::DK, C::NW, C::BPWK>(Kh, sm.k((k + 1) & 1), kn, wave, offk);
+    load_tile<C::DV, C::NW, C::BPWV>(Vh, sm.v((k + 1) & 1), kn, wave, C::SAME ? offk : offv);
   };
   // Deferred rescales owed before PV(j): the row factor of softmax(j) and the
   // column factors of tilt(j) (flag word from upd(j)).
@@ -689,14 +721,13 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     const i32x4* uf = reinterpret_cast<const i32x4*>(sm.upd(j & 1));
     i32x4 any4 = uf[0];
 #pragma unroll
-    for (int w = 1; w < NW / 4; ++w) any4 |= uf[w];
+    for (int w = 1; w < C::NW / 4; ++w) any4 |= uf[w];
     return any4;
   };
 #define FEM_PHASE1(PVA, QKT) \
-  phase1<D, NW, MODE, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, pp, lsel)
-#define FEM_PHASE2(PVB, SM, MK)                                                               \
-  phase2<D, NW, MODE, PVB, SM, MK>(sm, acc, pp, sacc, m, apend, k - 1, eofs, k * C::BK, tq, hl, \
-                                   scale2)
+  phase1<C, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, pp, lsel)
+#define FEM_PHASE2(PVB, SM, MK) \
+  phase2<C, PVB, SM, MK>(sm, acc, pp, sacc, m, apend, k - 1, eofs, k * C::BK, tm, hl, scale2)
 
   // Every wave runs the same steps on every tile: past its diagonal tile the
   // softmax masks every key, so P = 0 and PV adds nothing, while the
@@ -707,11 +738,11 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   {
     const int k = 0;
     if (k + 1 < ntiles) {
-      unsigned off[C::BPW];
-      next_offsets(k, off);
-      load_next(k, off);
+      unsigned offk[C::BPWK], offv[C::BPWV];
+      next_offsets(k, offk, offv);
+      load_next(k, offk, offv);
     }
-    Tilt<D, NW, MODE> tl;
+    Tilt<C> tl;
     FEM_PHASE1(false, true);
     if (wlast <= 0) FEM_PHASE2(false, true, true);
     else FEM_PHASE2(false, true, false);
@@ -722,12 +753,12 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     // LDS reads of the flag words and the load offsets go out together
     const i32x4 any4 = flags_of(k - 1);
     if (k + 1 < ntiles) {
-      unsigned off[C::BPW];
-      next_offsets(k, off);
-      load_next(k, off);
+      unsigned offk[C::BPWK], offv[C::BPWV];
+      next_offsets(k, offk, offv);
+      load_next(k, offk, offv);
     }
     if (k > 1) rescale(k - 1, any4);
-    Tilt<D, NW, MODE> tl;
+    Tilt<C> tl;
     FEM_PHASE1(true, true);
     if (k >= wlast) FEM_PHASE2(true, true, true);
     else FEM_PHASE2(true, true, false);
@@ -737,7 +768,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   {
     const int k = ntiles;
     if (k > 1) rescale(k - 1, flags_of(k - 1));
-    Tilt<D, NW, MODE> tl;
+    Tilt<C> tl;
     FEM_PHASE1(true, false);
     FEM_PHASE2(true, false, false);
   }
@@ -757,7 +788,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
         f32x4 o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = acc[cb][g * 4 + e] * rl;
-        *reinterpret_cast<f32x4*>(Oh + (size_t)tq * D + ch0) = o;
+        *reinterpret_cast<f32x4*>(Oh + (size_t)tq * C::DV + ch0) = o;
       }
     }
     return;
@@ -789,7 +820,7 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
         if (!(a >= kUnderflow) && tq < T) flags |= 1ull << (cb * 16 + g * 4 + e);
       }
       if (tq >= T) continue;
-      const size_t at = (size_t)tq * D + ch0;
+      const size_t at = (size_t)tq * C::DV + ch0;
       if (MODE == kGated) {
         // mu from the kMean launch; an underflowed F keeps mu in place for
         // the exact path below
@@ -802,7 +833,13 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
           o[e] = flagged ? mu[e] : gg[e] * fmaf(lm[e], o[e] - mu[e], mu[e]);
         }
       }
-      *reinterpret_cast<f32x4*>(Oh + at) = o;
+      if (C::OBF16) {
+        const bf16x2 o01 = to_bf16x2(o[0], o[1]), o23 = to_bf16x2(o[2], o[3]);
+        const u32x2 ob = {__builtin_bit_cast(unsigned, o01), __builtin_bit_cast(unsigned, o23)};
+        *reinterpret_cast<u32x2*>(Ob + at) = ob;
+      } else {
+        *reinterpret_cast<f32x4*>(Oh + at) = o;
+      }
     }
   }
 
@@ -818,13 +855,15 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
     const int t = __builtin_amdgcn_readlane(tq, src);
     const int cb = e >> 4, i = e & 15;
     const int ch = cb * 32 + (i >> 2) * 8 + (src >> 5) * 4 + (i & 3);
-    const float o = exact_read<D>(Qh, Kh, Vh, t, ch, scale2, sm.bl()[ch]);
+    const float o = exact_read<C>(Qh, Kh, Vh, t, C::CAUSAL ? t + 1 : T, ch, scale2, sm.bl()[ch]);
     if (lane == src) {
       flags &= ~(1ull << e);
-      const size_t at = (size_t)t * D + ch;
+      const size_t at = (size_t)t * C::DV + ch;
       if (MODE == kGated) {
         const float mu = Oh[at];
         Oh[at] = (Gh ? Gh[at] : 1.f) * fmaf(Lh[at], o - mu, mu);
+      } else if (C::OBF16) {
+        Ob[at] = (bf16)o;
       } else {
         Oh[at] = o;
       }
@@ -832,56 +871,81 @@ __global__ __launch_bounds__(NW * 64) void softmax_bf16_kernel(
   }
 }
 
-template <int D, int NW, int MODE>
+template <class C>
 hipError_t launch(const void* Q, const void* K, const void* V, const float* beta,
-                  const float* lam, const float* gate, float* out, int B, int H, int T,
+                  const float* lam, const float* gate, void* out, int B, int H, int T,
                   hipStream_t stream) {
-  using C = Cfg<D, NW>;
   static std::once_flag once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(once, [] {
-    attr_err =
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&softmax_bf16_kernel<D, NW, MODE>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
+    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&softmax_bf16_kernel<C>),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
   });
   if (attr_err != hipSuccess) return attr_err;
   const int nqb = (T + C::BQ - 1) / C::BQ;
   const int nbh = B * H;
   dim3 grid((unsigned)(nqb * nbh)), block(C::NT);
-  hipLaunchKernelGGL((softmax_bf16_kernel<D, NW, MODE>), grid, block, C::LDS, stream,
+  hipLaunchKernelGGL((softmax_bf16_kernel<C>), grid, block, C::LDS, stream,
                      reinterpret_cast<const bf16*>(Q), reinterpret_cast<const bf16*>(K),
-                     reinterpret_cast<const bf16*>(V), beta, lam, gate, out, H, T, nqb, nbh);
+                     reinterpret_cast<const bf16*>(V), beta, lam, gate,
+                     reinterpret_cast<float*>(out), H, T, nqb, nbh);
   return hipGetLastError();
 }
 
-template <int D, int NW>
+template <int D>
 hipError_t launch_gated(const void* Q, const void* K, const void* V, const float* beta_max,
                         const float* lam, const float* gate, float* out, int B, int H, int T,
                         hipStream_t stream) {
-  hipError_t e = launch<D, NW, kMean>(Q, K, V, beta_max, nullptr, nullptr, out, B, H, T, stream);
+  hipError_t e =
+      launch<Cfg<D, D, 8, kMean>>(Q, K, V, beta_max, nullptr, nullptr, out, B, H, T, stream);
   if (e != hipSuccess) return e;
-  return launch<D, NW, kGated>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
+  return launch<Cfg<D, D, 8, kGated>>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
+}
+
+// The variants of the plain read: widths (d_qk, d_v), causal or encoder
+// read, fp32 or bf16 output.
+template <int DK, int DV>
+hipError_t launch_ex(const void* Q, const void* K, const void* V, const float* beta, void* out,
+                     int B, int H, int T, bool causal, bool obf16, hipStream_t stream) {
+  if (causal && !obf16)
+    return launch<Cfg<DK, DV, 8, kFem, true, false>>(Q, K, V, beta, nullptr, nullptr, out, B, H,
+                                                     T, stream);
+  if (causal)
+    return launch<Cfg<DK, DV, 8, kFem, true, true>>(Q, K, V, beta, nullptr, nullptr, out, B, H,
+                                                    T, stream);
+  if (!obf16)
+    return launch<Cfg<DK, DV, 8, kFem, false, false>>(Q, K, V, beta, nullptr, nullptr, out, B, H,
+                                                      T, stream);
+  return launch<Cfg<DK, DV, 8, kFem, false, true>>(Q, K, V, beta, nullptr, nullptr, out, B, H, T,
+                                                   stream);
 }
 
 }  // namespace
 
 hipError_t launch_softmax_bf16(const void* Q, const void* K, const void* V, const float* beta,
                                float* out, int B, int H, int T, int d, hipStream_t stream) {
-  switch (d) {
-    case 32: return launch<32, 8, kFem>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream);
-    case 64: return launch<64, 8, kFem>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream);
-    case 128: return launch<128, 8, kFem>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream);
-    default: return hipErrorInvalidValue;
-  }
+  return launch_softmax_ex_bf16(Q, K, V, beta, out, B, H, T, d, d, true, false, stream);
+}
+
+hipError_t launch_softmax_ex_bf16(const void* Q, const void* K, const void* V, const float* beta,
+                                  void* out, int B, int H, int T, int dk, int dv, bool causal,
+                                  bool obf16, hipStream_t stream) {
+  const auto go = [&](auto f) { return f(Q, K, V, beta, out, B, H, T, causal, obf16, stream); };
+  if (dk == 32 && dv == 32) return go(launch_ex<32, 32>);
+  if (dk == 64 && dv == 64) return go(launch_ex<64, 64>);
+  if (dk == 128 && dv == 128) return go(launch_ex<128, 128>);
+  if (dk == 64 && dv == 32) return go(launch_ex<64, 32>);
+  if (dk == 128 && dv == 64) return go(launch_ex<128, 64>);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_softmax_gated_bf16(const void* Q, const void* K, const void* V,
                                      const float* beta_max, const float* lam, const float* gate,
                                      float* out, int B, int H, int T, int d, hipStream_t stream) {
   switch (d) {
-    case 32: return launch_gated<32, 8>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
-    case 64: return launch_gated<64, 8>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
-    case 128: return launch_gated<128, 8>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
+    case 32: return launch_gated<32>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
+    case 64: return launch_gated<64>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
+    case 128: return launch_gated<128>(Q, K, V, beta_max, lam, gate, out, B, H, T, stream);
     default: return hipErrorInvalidValue;
   }
 }

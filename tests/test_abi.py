@@ -96,3 +96,19 @@ def test_gated_validation(lib):
     assert gt(lib, lam=A + 4) == ALIGN
     assert gt(lib, gate=A + 8) == ALIGN
     assert gt(lib, gate=None, k=A + 2) == ALIGN
+
+
+def ex(lib, q=A, k=A, v=A, beta=A, out=A, B=1, H=1, T=8, dqk=64, dv=64, flags=0, dt=BF16):
+    return lib.fem_softmax_fwd_ex(q, k, v, beta, out, B, H, T, dqk, dv, flags, dt, None)
+
+
+def test_ex_validation(lib):
+    assert ex(lib, v=None) == NULLPTR
+    assert ex(lib, T=-3) == SHAPE
+    assert ex(lib, dv=0) == SHAPE
+    assert ex(lib, flags=4) == UNSUPPORTED
+    assert ex(lib, dt=F32) == UNSUPPORTED
+    for dqk, dv in ((64, 128), (128, 32), (96, 48), (256, 128), (16, 16)):
+        assert ex(lib, dqk=dqk, dv=dv) == UNSUPPORTED, (dqk, dv)
+    assert ex(lib, out=A + 2, flags=3) == ALIGN
+    assert ex(lib, dqk=128, dv=64, k=A + 8) == ALIGN
