@@ -16,6 +16,7 @@ from .fem_oracle import (  # noqa: F401
     fem_softmax_ltl,
     fem_softmax,
     fem_softmax_encoder,
+    fem_softmax_decode,
     softmax_prior_all,
     fem_linear,
     fem_linear_recurrent,

@@ -248,6 +248,29 @@ def fem_softmax_encoder(q, k, v, beta, rows=None, block: int = 512) -> np.ndarra
     return out
 
 
+def fem_softmax_decode(q, kc, vc, lens, beta) -> np.ndarray:
+    """One decoding step against a KV cache: the read of a single new query
+    per (b, h) over the first lens[b] cached keys, which include the new
+    token's own key and value (the autoregressive O(T) KV-cache setting of the
+    softmax prior, Appendix "Parameterizations of the Prior Selection").
+
+    q: [B, H, d]; kc: [B, H, L, d]; vc: [B, H, L, d_v]; lens: [B] ints in
+    [1, L]; beta: [H, d_v].  Returns float64 [B, H, d_v].
+    """
+    q, kc, vc, beta = _as64(q), _as64(kc), _as64(vc), _as64(beta)
+    B, H, _, _ = kc.shape
+    out = np.empty((B, H, vc.shape[3]))
+    for b in range(B):
+        n = int(lens[b])
+        for h in range(H):
+            qq = q[b, h][None, :]
+            kk = kc[b, h, :n]
+            p = softmax_prior_all(qq, kk, np.array([0]))
+            lp = (lambda qq=qq, kk=kk: softmax_logprior_all(qq, kk, np.array([0])))
+            out[b, h] = free_energy_read(p, vc[b, h, :n], beta[h], logp=lp)[0]
+    return out
+
+
 def fem_softmax_ltl(q, k, v, beta_max, lam, gate=None, rows=None,
                     block: int = 512) -> np.ndarray:
     """Two-level gated FEM read with the causal softmax prior.

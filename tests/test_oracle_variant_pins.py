@@ -8,6 +8,8 @@ Evaluation") is pinned by facts that do not retype it:
   * joint permutations of the (k_i, v_i) pairs leave every row unchanged;
   * under a uniform prior every row is the log-mean-exp of the whole column;
   * beta -> 0 gives unmasked softmax attention (torch SDPA, float64).
+The decode step against a KV cache is pinned to the causal read's row t
+(query t over the first t + 1 keys) and to the 50-digit evaluation.
 d_v != d_qk (budget (i) of Sec. "Free Energy Mixer", d_v = d_qk / 2): the
 score scale stays 1/sqrt(d_qk) and each value channel is read independently,
 so the read of a value subset equals the read of the full width restricted to
@@ -153,3 +155,42 @@ def test_encoder_pins_catch_planted_mistakes(name, patch):
     assert _enc_pins_pass(oracle.fem_softmax_encoder) == []
     with np.errstate(divide="ignore"):
         assert _enc_pins_pass(_mutant(patch)) != [], name
+
+
+# ---------------------------------------------------------------------------
+# Decode step against a KV cache
+# ---------------------------------------------------------------------------
+def test_decode_is_causal_row():
+    """The decode read of q_t over the first t+1 cached keys is row t of the
+    causal read (whose own pins fix it)."""
+    rng = np.random.default_rng(58)
+    B, H, L, d, dv = 2, 3, 50, 8, 4
+    q = rng.standard_normal((B, H, L, d))
+    k = rng.standard_normal((B, H, L, d))
+    v = 2 * rng.standard_normal((B, H, L, dv))
+    beta = np.exp(rng.uniform(np.log(0.1), np.log(8.0), (H, dv)))
+    full = oracle.fem_softmax(q, k, v, beta)
+    for t in (0, 1, 31, 49):
+        lens = np.array([t + 1, t + 1])
+        got = oracle.fem_softmax_decode(q[:, :, t], k, v, lens, beta)
+        np.testing.assert_allclose(got, full[:, :, t], rtol=0, atol=1e-12)
+    lens = np.array([7, 50])
+    got = oracle.fem_softmax_decode(q[:, :, 20], k, v, lens, beta)
+    want0 = oracle.fem_softmax_encoder(q[0:1, :, 20:21], k[0:1, :, :7], v[0:1, :, :7], beta)[0, :, 0]
+    np.testing.assert_allclose(got[0], want0, rtol=0, atol=1e-12)
+
+
+def test_decode_brute_force():
+    rng = np.random.default_rng(59)
+    L, d, dv = 11, 4, 3
+    q = rng.standard_normal((1, 1, d))
+    k = rng.standard_normal((1, 1, L, d))
+    v = 2 * rng.standard_normal((1, 1, L, dv))
+    beta = np.array([[0.3, 2.0, 9.0]])
+    n = 8
+    # brute causal read with the query in the last row: its last row is the step
+    qq = np.concatenate([np.zeros((n - 1, d)), q[0, 0][None]], axis=0)
+    want = brute.brute_fem_softmax(qq.tolist(), k[0, 0, :n].tolist(), v[0, 0, :n].tolist(),
+                                   beta[0].tolist())[-1]
+    got = oracle.fem_softmax_decode(q, k, v, np.array([n]), beta)[0, 0]
+    np.testing.assert_allclose(got, np.array(want, dtype=np.float64), rtol=0, atol=1e-12)
