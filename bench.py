@@ -12,7 +12,9 @@ multiply-adds over the causal triangle, diagonal included; exponentials not
 counted).  The linear-prior read (fem_linear_fwd, B=4, H=16, T=8192,
 d_k=d_v=64, chunk 64) is timed too and reported under "linear", and the
 two-level gated read (fem_softmax_gated_fwd) on the headline shape under
-"gated" (FLOP = 3*B*H*T*(T+1)*d: Q K^T, P E and P V).
+"gated" (FLOP = 3*B*H*T*(T+1)*d: Q K^T, P E and P V), and one decoding step
+(fem_softmax_decode) against a full B=8, H=16, L=4096, d=128 KV cache under
+"decode" (bytes = the caches read once + q + out).
 """
 
 from __future__ import annotations
@@ -105,6 +107,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-linear", action="store_true")
     ap.add_argument("--no-gated", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a known-size "
                          "kernel for calibrating hardware byte counters)")
@@ -180,6 +183,20 @@ def main():
             "kernels": ["softmax_bf16_kernel<128,8,kMean>", "softmax_bf16_kernel<128,8,kGated>"],
         }
         del lamd, gd
+    if not args.no_decode:
+        q1 = qd[:, :, -1].contiguous()
+        outd = torch.empty((B, H, d), device=dev, dtype=torch.float32)
+        fnd = lambda: binding.fem_softmax_decode(q1, kd, vd, bd, out=outd)
+        msd = time_calls(fnd, args.steps, args.warmup)
+        io = 2 * B * H * T * d * 2 + q1.numel() * 2 + outd.numel() * 4
+        result["decode"] = {
+            "workload": f"fem_softmax_decode_bf16_B{B}_H{H}_L{T}_d{d}", "ms": round(msd, 4),
+            "algorithmic_bytes": io,
+            "achieved_GBs": round(io / (msd * 1e-3) / 1e9, 1),
+            "peak_GBs": PEAK_HBM_GBS,
+            "frac": round(io / (msd * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        }
+        del q1, outd
     del qd, kd, vd, out
     torch.cuda.empty_cache()
 

@@ -111,6 +111,39 @@ int fem_softmax_fwd_ex(const void* Q, const void* K, const void* V,
                        int dtype, hipStream_t stream);
 
 /*
+ * One decoding step of the softmax-prior read against a KV cache: for every
+ * (b, h) the new query q[b,h] reads the first lens[b] cached keys and values,
+ * which include the new token's own k and v (the autoregressive KV-cache
+ * setting, Appendix "Parameterizations of the Prior Selection"):
+ *
+ *   out[b,h,j] = (1/beta[h,j]) log sum_{i < lens[b]} p(i) exp(beta[h,j] v[b,h,i,j]),
+ *   p(i) = softmax_{i < lens[b]}( q[b,h] . k[b,h,i] / sqrt(d_qk) )
+ *
+ * i.e. row lens[b]-1 of fem_softmax_fwd when q is that row's query.
+ *
+ *   q      : [B, H, d_qk] bfloat16
+ *   Kc     : [B, H, L, d_qk] bfloat16 key cache (rows >= lens[b] are not read)
+ *   Vc     : [B, H, L, d_v] bfloat16 value cache
+ *   lens   : [B] int32 DEVICE array, each in [1, L]; NULL means L for every b.
+ *            A length outside [1, L] is not an error on the host (it would
+ *            need a device read): that sequence's outputs are NaN.
+ *   beta   : [H, d_v] float32, > 0
+ *   out    : [B, H, d_v] float32
+ *   (d_qk, d_v): as fem_softmax_fwd_ex
+ *   dtype  : FEM_DTYPE_BF16
+ *
+ * fp32 arithmetic with a per-channel joint log-sum-exp (no shared shift).
+ * The keys are split over workgroups whose partial results live in a
+ * stream-ordered workspace of 8 * (d_v + 1) bytes per split and (b, h) (at
+ * most 4 * compute units / (B * H) splits, each a multiple of 64 keys), taken
+ * from the library's pool as in fem_linear_fwd.  Returns a fem_status.
+ */
+int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
+                       const int* lens, const float* beta, float* out,
+                       int B, int H, int L, int d_qk, int d_v, int dtype,
+                       hipStream_t stream);
+
+/*
  * Two-level gated FEM read with the causal softmax prior (Sec. "Two-Level
  * Gated FEM", eqs. inner-gate-main and fem-two-gates-main; the inner gate is
  * the linearized temperature learning of eqs. ltl and ltl-final):

@@ -18,8 +18,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfem.so")
 
 FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 
-EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_gated_fwd", "fem_linear_fwd",
-           "fem_status_str")
+EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_gated_fwd",
+           "fem_softmax_decode", "fem_linear_fwd", "fem_status_str")
 
 FEM_FLAG_ENCODER = 1
 FEM_FLAG_OUT_BF16 = 2
@@ -45,6 +45,8 @@ def load() -> ctypes.CDLL:
         lib.fem_softmax_fwd.restype = i
         lib.fem_softmax_fwd_ex.argtypes = [vp, vp, vp, f, vp, i, i, i, i, i, i, i, vp]
         lib.fem_softmax_fwd_ex.restype = i
+        lib.fem_softmax_decode.argtypes = [vp, vp, vp, vp, f, f, i, i, i, i, i, i, vp]
+        lib.fem_softmax_decode.restype = i
         lib.fem_softmax_gated_fwd.argtypes = [vp, vp, vp, f, f, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_gated_fwd.restype = i
         lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp]
@@ -136,6 +138,42 @@ def fem_softmax_fwd_ex(q, k, v, beta, out=None, causal: bool = True, out_dtype=t
     with torch.cuda.device(q.device):
         rc = lib.fem_softmax_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
                                     out.data_ptr(), B, H, T, dqk, dv, flags, FEM_DTYPE[q.dtype],
+                                    _stream_handle(q.device, stream))
+    _check(rc)
+    return out
+
+
+def fem_softmax_decode(q, k_cache, v_cache, beta, lens=None, out=None, stream=None) -> torch.Tensor:
+    """One decoding step: q [B, H, d_qk] reads the first lens[b] rows of the
+    caches k_cache [B, H, L, d_qk], v_cache [B, H, L, d_v] (bf16).  lens: [B]
+    int32 GPU tensor or None (all L).  Returns [B, H, d_v] fp32."""
+    lib = load()
+    _dev_tensor(q, "q", torch.bfloat16)
+    _dev_tensor(k_cache, "k_cache", torch.bfloat16)
+    _dev_tensor(v_cache, "v_cache", torch.bfloat16)
+    if q.dim() != 3 or k_cache.dim() != 4 or v_cache.dim() != 4:
+        raise ValueError("q must be [B, H, d_qk], caches [B, H, L, width]")
+    B, H, dqk = q.shape
+    L = k_cache.shape[2]
+    if tuple(k_cache.shape) != (B, H, L, dqk) or v_cache.shape[:3] != k_cache.shape[:3]:
+        raise ValueError("k_cache must be [B, H, L, d_qk] and v_cache [B, H, L, d_v]")
+    dv = v_cache.shape[3]
+    _dev_tensor(beta, "beta", torch.float32)
+    if tuple(beta.shape) != (H, dv):
+        raise ValueError("beta must be [H, d_v]")
+    if lens is not None:
+        _dev_tensor(lens, "lens", torch.int32)
+        if tuple(lens.shape) != (B,):
+            raise ValueError("lens must be [B]")
+    if out is None:
+        out = torch.empty((B, H, dv), device=q.device, dtype=torch.float32)
+    _dev_tensor(out, "out", torch.float32)
+    if tuple(out.shape) != (B, H, dv):
+        raise ValueError("out must be [B, H, d_v]")
+    with torch.cuda.device(q.device):
+        rc = lib.fem_softmax_decode(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                    None if lens is None else lens.data_ptr(), beta.data_ptr(),
+                                    out.data_ptr(), B, H, L, dqk, dv, FEM_DTYPE[q.dtype],
                                     _stream_handle(q.device, stream))
     _check(rc)
     return out

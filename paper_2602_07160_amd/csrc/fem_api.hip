@@ -61,6 +61,21 @@ extern "C" int fem_softmax_fwd_ex(const void* Q, const void* K, const void* V, c
                                               (flags & FEM_FLAG_OUT_BF16) != 0, stream));
 }
 
+extern "C" int fem_softmax_decode(const void* q, const void* Kc, const void* Vc, const int* lens,
+                                  const float* beta, float* out, int B, int H, int L, int d_qk,
+                                  int d_v, int dtype, hipStream_t stream) {
+  if (!q || !Kc || !Vc || !beta || !out) return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, L, d_qk) || !sizes_ok(B, H, L, d_v)) return FEM_ERR_SHAPE;
+  if ((unsigned long long)B * H > 65535ull) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  const bool pair_ok = (d_qk == d_v && (d_v == 32 || d_v == 64 || d_v == 128)) ||
+                       (d_qk == 2 * d_v && (d_v == 32 || d_v == 64));
+  if (!pair_ok) return FEM_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(Kc) || !aligned16(Vc)) return FEM_ERR_ALIGN;
+  return from_hip(
+      fem::launch_decode_bf16(q, Kc, Vc, lens, beta, out, B, H, L, d_qk, d_v, stream));
+}
+
 extern "C" int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V,
                                      const float* beta_max, const float* lam, const float* gate,
                                      float* out, int B, int H, int T, int d, int dtype,

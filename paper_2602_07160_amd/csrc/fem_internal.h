@@ -22,6 +22,12 @@ hipError_t launch_softmax_gated_bf16(const void* Q, const void* K, const void* V
                                      const float* beta_max, const float* lam, const float* gate,
                                      float* out, int B, int H, int T, int d, hipStream_t stream);
 
+// One decoding step against a KV cache (single query per (b, h)), bf16,
+// (dk, dv) as launch_softmax_ex_bf16.  lens may be null (every row has L keys).
+hipError_t launch_decode_bf16(const void* q, const void* Kc, const void* Vc, const int* lens,
+                              const float* beta, float* out, int B, int H, int L, int dk, int dv,
+                              hipStream_t stream);
+
 // Exact fp32 vector-unit softmax-prior read, 1 <= d <= 256.
 hipError_t launch_softmax_f32(const float* Q, const float* K, const float* V,
                               const float* beta, float* out,

@@ -112,3 +112,17 @@ def test_ex_validation(lib):
         assert ex(lib, dqk=dqk, dv=dv) == UNSUPPORTED, (dqk, dv)
     assert ex(lib, out=A + 2, flags=3) == ALIGN
     assert ex(lib, dqk=128, dv=64, k=A + 8) == ALIGN
+
+
+def dec(lib, q=A, k=A, v=A, lens=A, beta=A, out=A, B=1, H=1, L=8, dqk=64, dv=64, dt=BF16):
+    return lib.fem_softmax_decode(q, k, v, lens, beta, out, B, H, L, dqk, dv, dt, None)
+
+
+def test_decode_validation(lib):
+    assert dec(lib, q=None) == NULLPTR
+    assert dec(lib, out=None) == NULLPTR
+    assert dec(lib, L=0) == SHAPE
+    assert dec(lib, B=70000) == SHAPE
+    assert dec(lib, dqk=32, dv=64) == UNSUPPORTED
+    assert dec(lib, dt=F32) == UNSUPPORTED
+    assert dec(lib, k=A + 4) == ALIGN
