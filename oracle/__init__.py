@@ -20,5 +20,9 @@ from .fem_oracle import (  # noqa: F401
     softmax_prior_all,
     fem_linear,
     fem_linear_recurrent,
+    fem_gla,
+    fem_gla_recurrent,
+    rope,
+    gla_features,
     posterior,
 )

@@ -87,3 +87,43 @@ def brute_fem_softmax_encoder(q, k, v, beta, dps=50):
 
 def brute_fem_linear(q, k, v, beta, dps=50):
     return brute_read(brute_linear_prior(q, k, dps), v, beta, dps)
+
+
+def brute_gla_prior(q, k, g, eps, base, gmin, dps=50):
+    """GLA prior rows term by term: features ReLU(RoPE(x)) + eps, decay
+    exp(sum_{tau=i+1}^{t} clip(g_tau)) per key channel (Appendix "Gated Linear
+    Attention (GLA) Prior", eq. gla-score-appendix)."""
+    with mpmath.workdps(dps):
+        T = len(q)
+        d = len(q[0])
+
+        def feat(x, t):
+            out = [mpmath.mpf(0)] * d
+            for m in range(d // 2):
+                ang = t * mpmath.power(mpmath.mpf(base), -mpmath.mpf(2 * m) / d)
+                c, s = mpmath.cos(ang), mpmath.sin(ang)
+                a, b = mpmath.mpf(x[2 * m]), mpmath.mpf(x[2 * m + 1])
+                out[2 * m] = a * c - b * s
+                out[2 * m + 1] = a * s + b * c
+            return [max(u, 0) + mpmath.mpf(eps) for u in out]
+
+        gg = [[min(max(mpmath.mpf(g[t][c]), mpmath.mpf(gmin)), 0) for c in range(d)]
+              for t in range(T)]
+        rows = []
+        for t in range(T):
+            fq = feat(q[t], t)
+            s = []
+            for i in range(t + 1):
+                fk = feat(k[i], i)
+                tot = mpmath.mpf(0)
+                for c in range(d):
+                    dec = mpmath.exp(sum(gg[tau][c] for tau in range(i + 1, t + 1)))
+                    tot += fq[c] * fk[c] * dec
+                s.append(tot)
+            z = sum(s)
+            rows.append([x / z for x in s])
+        return rows
+
+
+def brute_fem_gla(q, k, v, g, beta, eps, base, gmin, dps=50):
+    return brute_read(brute_gla_prior(q, k, g, eps, base, gmin, dps), v, beta, dps)

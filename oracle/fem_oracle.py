@@ -14,6 +14,8 @@ Prior Selection", softmax prior):
             p_t(i) = <phi(q_t), phi(k_i)> / sum_{r<=t} <phi(q_t), phi(k_r)>
                      with phi = elu + 1                                (linear)
             p_t(i) = softmax over every i < T                  (encoder: no mask)
+            p_t(i) propto <q~_t, exp(G_t - G_i) k~_i>, q~ = ReLU(RoPE(q)) + eps,
+                     G_t = sum_{tau<=t} g_tau                         (GLA)
   read      F_{t,j} = (1 / beta_j) * log sum_{i<=t} p_t(i) * exp(beta_j v_{i,j})
                                   (free-energy read, eq. fem-free-energy-main)
   gated     o_{t,j} = g_{t,j} * ((1 - lam_{t,j}) * mu_{t,j} + lam_{t,j} * F_{t,j}(beta_max))
@@ -298,6 +300,109 @@ def fem_softmax_ltl(q, k, v, beta_max, lam, gate=None, rows=None,
                 out[b, h, pos:pos + len(rb)] = ltl_read(
                     p, v[b, h, :n], beta_max[h], lam[b, h, rb], g, logp=lp)
                 pos += len(rb)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Gated linear attention (GLA) prior (Appendix "Gated Linear Attention (GLA)
+# Prior": RoPE, then ReLU + eps features; decay envelope; eqs.
+# gla-score-appendix and gla-assoc).
+# ---------------------------------------------------------------------------
+GLA_EPS = 1e-6          # the small positive constant of the feature map
+GLA_ROPE_BASE = 10000.0  # RoPE frequency base
+GLA_G_MIN = -2.0        # log-decays are clipped to [GLA_G_MIN, 0]
+
+
+def rope(x: np.ndarray, pos: np.ndarray, base: float = GLA_ROPE_BASE) -> np.ndarray:
+    """Rotary position embedding of rows x[r] at positions pos[r]: the pair of
+    dimensions (2m, 2m+1) is rotated by the angle pos * base^(-2m/d)."""
+    d = x.shape[-1]
+    theta = base ** (-2.0 * np.arange(d // 2) / d)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * theta[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    out = np.empty_like(x, dtype=np.float64)
+    out[:, 0::2] = x[:, 0::2] * c - x[:, 1::2] * s
+    out[:, 1::2] = x[:, 0::2] * s + x[:, 1::2] * c
+    return out
+
+
+def gla_features(x: np.ndarray, pos: np.ndarray) -> np.ndarray:
+    """ReLU(RoPE(x)) + eps, the nonnegative GLA features."""
+    return np.maximum(rope(x, pos), 0.0) + GLA_EPS
+
+
+def gla_log_decay(g: np.ndarray) -> np.ndarray:
+    """The learned log-decays g <= 0, clipped to [GLA_G_MIN, 0] (the envelope
+    is clipped in practice)."""
+    return np.clip(g, GLA_G_MIN, 0.0)
+
+
+def gla_prior_rows(q: np.ndarray, k: np.ndarray, g: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """Causal GLA prior p_t(i) = s_t(i) / Z_t (eq. gla-score-appendix) with a
+    per-key-channel decay: s_t(i) = sum_c q~_{t,c} k~_{i,c} exp(sum_{tau=i+1}^{t}
+    g_{tau,c}) for i <= t, i.e. <D_t q~_t, D_i^{-1} k~_i> with the envelope D
+    acting element-wise.  q, k, g: [T, d_k]; returns [len(rows), max(rows)+1].
+    """
+    n = int(rows.max()) + 1
+    fq = gla_features(q[rows], rows)
+    fk = gla_features(k[:n], np.arange(n))
+    G = np.cumsum(gla_log_decay(g[:n]), axis=0)  # G_t = sum_{tau <= t} g_tau
+    s = np.zeros((len(rows), n))
+    step = max(1, (1 << 21) // (n * k.shape[1]))
+    for a in range(0, len(rows), step):
+        rr = rows[a:a + step]
+        e = G[rr][:, None, :] - G[None, :, :]                     # [r, i, c]
+        e = np.where(np.arange(n)[None, :, None] <= rr[:, None, None], e, -np.inf)
+        s[a:a + step] = np.einsum("ric,ic,rc->ri", np.exp(e), fk, fq[a:a + step])
+    return s / s.sum(axis=1, keepdims=True)
+
+
+def fem_gla(q, k, v, g, beta, rows=None, block: int = 256) -> np.ndarray:
+    """FEM read with the causal GLA prior: q, k, g: [B, H, T, d_k] (g the
+    log-decays); v: [B, H, T, d_v]; beta: [H, d_v].  Float64 [B, H, R, d_v]."""
+    q, k, v, g, beta = _as64(q), _as64(k), _as64(v), _as64(g), _as64(beta)
+    B, H, T, _ = q.shape
+    dv = v.shape[3]
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    out = np.empty((B, H, len(rows), dv))
+    for b in range(B):
+        for h in range(H):
+            pos = 0
+            for rb in _row_blocks(rows, block):
+                n = int(rb.max()) + 1
+                p = gla_prior_rows(q[b, h], k[b, h], g[b, h], rb)
+                out[b, h, pos:pos + len(rb)] = free_energy_read(p, v[b, h, :n], beta[h])
+                pos += len(rb)
+    return out
+
+
+def fem_gla_recurrent(q, k, v, g, beta) -> np.ndarray:
+    """The GLA-prior read as a float64 recurrence over t (the streaming
+    recurrences of the GLA appendix, with the constant value channel):
+      S_t = diag(e^{g_t}) S_{t-1} + k~_t exp(beta v_t - c)^T,
+      z_t = diag(e^{g_t}) z_{t-1} + k~_t,
+      F_t = (log(q~_t^T S_t) - log(q~_t^T z_t) + c) / beta,
+    one global per-channel shift c_j.  An independent cross-check of
+    ``fem_gla`` on small T."""
+    q, k, v, g, beta = _as64(q), _as64(k), _as64(v), _as64(g), _as64(beta)
+    B, H, T, dk = q.shape
+    dv = v.shape[3]
+    out = np.empty((B, H, T, dv))
+    pos = np.arange(T)
+    for b in range(B):
+        for h in range(H):
+            x = v[b, h] * beta[h][None, :]
+            c = x.max(axis=0)
+            e = np.exp(x - c[None, :])
+            fq = gla_features(q[b, h], pos)
+            fk = gla_features(k[b, h], pos)
+            a = np.exp(gla_log_decay(g[b, h]))
+            S = np.zeros((dk, dv))
+            z = np.zeros(dk)
+            for t in range(T):
+                S = a[t][:, None] * S + np.outer(fk[t], e[t])
+                z = a[t] * z + fk[t]
+                out[b, h, t] = (np.log(fq[t] @ S) - np.log(fq[t] @ z) + c) / beta[h]
     return out
 
 
