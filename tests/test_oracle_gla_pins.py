@@ -156,7 +156,7 @@ _rope = fo.rope
 
 
 def _prior_decay_from_i(q, k, g, rows):
-    # exp(sum_{tau=i}^{t} g): one step too many
+    # exp(sum_{tau=i+2}^{t+1} g): the decay window shifted by one step
     n = int(rows.max()) + 1
     g2 = np.concatenate([g[1:n], np.zeros((1, g.shape[1]))])
     return _prior(q, k, np.concatenate([g2, g[n:]]), rows)
@@ -183,7 +183,7 @@ def _features_no_relu(x, pos):
 
 
 @pytest.mark.parametrize("name,patch", [
-    ("decay one step too long", {"gla_prior_rows": _prior_decay_from_i}),
+    ("decay window shifted by one step", {"gla_prior_rows": _prior_decay_from_i}),
     ("decay rate halved", {"gla_prior_rows": _prior_decay_halved}),
     ("RoPE pairs (m, m + d/2)", {"rope": _rope_rotate_half}),
     ("ReLU left out", {"gla_features": _features_no_relu}),
