@@ -14,7 +14,9 @@ d_k=d_v=64, chunk 64) is timed too and reported under "linear", and the
 two-level gated read (fem_softmax_gated_fwd) on the headline shape under
 "gated" (FLOP = 3*B*H*T*(T+1)*d: Q K^T, P E and P V), and one decoding step
 (fem_softmax_decode) against a full B=8, H=16, L=4096, d=128 KV cache under
-"decode" (bytes = the caches read once + q + out).
+"decode" (bytes = the caches read once + q + out), and the GLA-prior read
+(fem_gla_fwd) on the linear workload's shape with seeded log-decays under
+"gla" (bytes = q, k, v, the fp32 decays and out, once each).
 """
 
 from __future__ import annotations
@@ -108,6 +110,7 @@ def main():
     ap.add_argument("--no-linear", action="store_true")
     ap.add_argument("--no-gated", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-gla", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a known-size "
                          "kernel for calibrating hardware byte counters)")
@@ -219,6 +222,20 @@ def main():
             }
         except binding.FemError as e:
             result["linear"] = {"error": str(e)}
+        if not args.no_gla:
+            gld = inputs.draw_gla_decay(inputs.BASE_SEED + 105, wl.B, wl.H, wl.T, wl.d).to(dev)
+            fng = lambda: binding.fem_gla_fwd(qld, kld, vld, gld, bld, out=outl, chunk=wl.chunk)
+            msg = time_calls(fng, args.steps, args.warmup)
+            iog = 3 * ql.numel() * 2 + gld.numel() * 4 + outl.numel() * 4
+            result["gla"] = {
+                "workload": wl.name.replace("linear", "gla"), "chunk": wl.chunk,
+                "ms": round(msg, 4), "tokens_per_s": round(wl.B * wl.T / (msg * 1e-3), 1),
+                "algorithmic_bytes": iog,
+                "achieved_GBs": round(iog / (msg * 1e-3) / 1e9, 1),
+                "peak_GBs": PEAK_HBM_GBS,
+                "frac": round(iog / (msg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            }
+            del gld
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(q, k, v, beta, args.cpu_budget)

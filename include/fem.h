@@ -15,6 +15,8 @@
  *   fem_linear_fwd:   p_t(i) = <phi(q_t), phi(k_i)> / sum_{r <= t} <phi(q_t), phi(k_r)>,
  *                     phi = elu + 1  (Appendix "Selection distributions,
  *                      support, and normalization", linear attention)
+ *   fem_gla_fwd:      the decay-gated linear (GLA) prior of the appendix
+ *                     "Gated Linear Attention (GLA) Prior"
  *
  * and the two-level gated read of the paper's models, which mixes F at a
  * per-channel beta_max with the prior's expectation (fem_softmax_gated_fwd).
@@ -200,6 +202,35 @@ int fem_linear_fwd(const void* Q, const void* K, const void* V,
                    const float* beta, float* out,
                    int B, int H, int T, int d_k, int d_v, int chunk,
                    int dtype, hipStream_t stream);
+
+/*
+ * Causal GLA-prior FEM read as an O(T) chunked scan (Appendix "Gated Linear
+ * Attention (GLA) Prior", eqs. gla-score-appendix and gla-assoc):
+ *
+ *   p_t(i) = sum_c q~[t,c] k~[i,c] exp(sum_{tau=i+1}^{t} g[tau,c]) / Z_t,  i <= t,
+ *   q~ = ReLU(RoPE(q)) + 1e-6, k~ likewise,
+ *
+ * with the read of fem_linear_fwd on top.  RoPE rotates the pair of
+ * dimensions (2m, 2m+1) of position t by t * 10000^(-2m/d_k); the decay is
+ * per key channel c (a scalar or per-head decay is the same value repeated).
+ *
+ *   Q, K    : [B, H, T, d_k] bfloat16
+ *   V       : [B, H, T, d_v] bfloat16
+ *   G       : [B, H, T, d_k] float32 log-decays; clipped to [-2, 0] (a decay
+ *             factor of at least e^-2 per step), so g <= 0 as the paper
+ *             requires and every factor of the 64-token chunk form stays
+ *             inside float range
+ *   beta    : [H, d_v] float32, > 0
+ *   out     : [B, H, T, d_v] float32
+ *   d_k, d_v: 64 (both);  chunk: 64;  dtype: FEM_DTYPE_BF16
+ *
+ * Workspace as fem_linear_fwd (plus 256 B per segment and (b, h)).  Returns a
+ * fem_status.
+ */
+int fem_gla_fwd(const void* Q, const void* K, const void* V, const float* G,
+                const float* beta, float* out,
+                int B, int H, int T, int d_k, int d_v, int chunk,
+                int dtype, hipStream_t stream);
 
 /* Static, NUL-terminated name of a status code (never NULL). */
 const char* fem_status_str(int status);

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfem.so")
 FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 
 EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_gated_fwd",
-           "fem_softmax_decode", "fem_linear_fwd", "fem_status_str")
+           "fem_softmax_decode", "fem_linear_fwd", "fem_gla_fwd", "fem_status_str")
 
 FEM_FLAG_ENCODER = 1
 FEM_FLAG_OUT_BF16 = 2
@@ -51,6 +51,8 @@ def load() -> ctypes.CDLL:
         lib.fem_softmax_gated_fwd.restype = i
         lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp]
         lib.fem_linear_fwd.restype = i
+        lib.fem_gla_fwd.argtypes = [vp, vp, vp, f, f, f, i, i, i, i, i, i, i, vp]
+        lib.fem_gla_fwd.restype = i
         lib.fem_status_str.argtypes = [i]
         lib.fem_status_str.restype = ctypes.c_char_p
         _lib = lib
@@ -239,5 +241,35 @@ def fem_linear_fwd(q, k, v, beta, out=None, chunk: int = 64, stream=None) -> tor
         rc = lib.fem_linear_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
                                 out.data_ptr(), B, H, T, dk, dv, int(chunk),
                                 FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+    _check(rc)
+    return out
+
+
+def fem_gla_fwd(q, k, v, g, beta, out=None, chunk: int = 64, stream=None) -> torch.Tensor:
+    """Causal GLA-prior FEM read.  q, k: [B, H, T, d_k] bf16; v: [B, H, T, d_v]
+    bf16; g: [B, H, T, d_k] fp32 log-decays; beta: [H, d_v] fp32.  Returns
+    [B, H, T, d_v] fp32."""
+    lib = load()
+    _dev_tensor(q, "q", torch.bfloat16)
+    _dev_tensor(k, "k", torch.bfloat16)
+    _dev_tensor(v, "v", torch.bfloat16)
+    _dev_tensor(g, "g", torch.float32)
+    if q.dim() != 4 or k.shape != q.shape or g.shape != q.shape or v.dim() != 4 or \
+            v.shape[:3] != q.shape[:3]:
+        raise ValueError("q, k, g must be [B, H, T, d_k] and v [B, H, T, d_v]")
+    B, H, T, dk = q.shape
+    dv = v.shape[3]
+    _dev_tensor(beta, "beta", torch.float32)
+    if tuple(beta.shape) != (H, dv):
+        raise ValueError("beta must be [H, d_v]")
+    if out is None:
+        out = torch.empty((B, H, T, dv), device=q.device, dtype=torch.float32)
+    _dev_tensor(out, "out", torch.float32)
+    if tuple(out.shape) != (B, H, T, dv):
+        raise ValueError("out must be [B, H, T, d_v]")
+    with torch.cuda.device(q.device):
+        rc = lib.fem_gla_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), g.data_ptr(),
+                             beta.data_ptr(), out.data_ptr(), B, H, T, dk, dv, int(chunk),
+                             FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
     _check(rc)
     return out

@@ -105,6 +105,22 @@ extern "C" int fem_linear_fwd(const void* Q, const void* K, const void* V, const
   return from_hip(e);
 }
 
+extern "C" int fem_gla_fwd(const void* Q, const void* K, const void* V, const float* G,
+                           const float* beta, float* out, int B, int H, int T, int d_k, int d_v,
+                           int chunk, int dtype, hipStream_t stream) {
+  if (!Q || !K || !V || !G || !beta || !out) return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, T, d_k) || !sizes_ok(B, H, T, d_v)) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  if (d_k != 64 || d_v != 64) return FEM_ERR_UNSUPPORTED;
+  if (chunk != 64) return FEM_ERR_UNSUPPORTED;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(G) || !aligned16(out))
+    return FEM_ERR_ALIGN;
+  const hipError_t e =
+      fem::launch_gla_bf16(Q, K, V, G, beta, out, B, H, T, d_k, d_v, chunk, stream);
+  if (e == hipErrorNotSupported) return FEM_ERR_UNSUPPORTED;
+  return from_hip(e);
+}
+
 extern "C" const char* fem_status_str(int status) {
   switch (status) {
     case FEM_OK: return "FEM_OK";

@@ -39,6 +39,12 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V,
                               int B, int H, int T, int dk, int dv, int chunk,
                               hipStream_t stream);
 
+// Chunked-scan GLA-prior read (RoPE, ReLU + eps features, per-channel
+// log-decays G [B, H, T, d_k] clipped to [-2, 0]), bf16, d_k = d_v = 64.
+hipError_t launch_gla_bf16(const void* Q, const void* K, const void* V, const float* G,
+                           const float* beta, float* out, int B, int H, int T, int dk, int dv,
+                           int chunk, hipStream_t stream);
+
 // Stream-ordered scratch from a library-owned pool (see fem_workspace.hip).
 hipError_t workspace_alloc(void** p, size_t bytes, hipStream_t stream);
 hipError_t workspace_free(void* p, hipStream_t stream);

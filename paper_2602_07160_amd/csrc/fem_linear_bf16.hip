@@ -28,6 +28,17 @@
 //                      K^T masked) E, inter-chunk phi Q S, and the state update
 //                      phi K^T E.  The next chunk's Q, K, V are fetched into
 //                      registers while the current one is processed.
+// GLA prior (Appendix "Gated Linear Attention (GLA) Prior"): the same scan
+// with features q~ = ReLU(RoPE(q)) + eps, k~ likewise, and a decay envelope
+// per key channel c: p_t(i) propto sum_c q~_tc k~_ic exp(G_tc - G_ic), G the
+// running sum of the log-decays g (clipped to [-2, 0]).  Inside a chunk, with
+// B the chunk-local running sum and R = B at its middle row:
+//   intra:  A_ti = sum_c (q~_tc e^{B_tc - R_c}) (k~_ic e^{R_c - B_ic})
+//   inter:  num_t += sum_c (q~_tc e^{B_tc - R_c}) (e^{R_c} S_c)
+//   update: S_c <- e^{B_last,c} S_c + sum_i k~_ic e^{B_last,c - B_ic} [E_i | 1]
+// Every factor stays within e^{+-64} because a chunk has 64 rows and g >= -2.
+// The segment prefix carries each segment's total log-decay.
+//
 // All products run on v_mfma_f32_32x32x16_bf16 in transposed form (outputs
 // are [channel][token]); E and S enter as bf16 hi + lo pairs, the masked
 // intra-chunk scores A enter as bf16 and the normaliser is summed from the
@@ -50,6 +61,39 @@ constexpr int NTH = 256;         // 4 waves
 constexpr int ROW = 64 + 8;      // padded bf16 row (64 values + 16 B)
 constexpr int SROW = DK + 8;     // padded S^T row (bf16)
 constexpr int STATE = DV * DK + DK + DV;  // floats per saved segment state
+constexpr int kElu = 0, kGla = 1;         // the prior
+// GLA adds the segment's total log-decay per key channel
+template <int PRIOR>
+constexpr int state_floats() { return PRIOR == kGla ? STATE + DK : STATE; }
+
+constexpr float kGlaEps = 1e-6f;   // the feature map's positive constant
+constexpr float kGlaGMin = -2.f;   // log-decays are clipped to [kGlaGMin, 0]
+
+// RoPE frequencies in revolutions per position, f_m = 10000^(-2m/DK) / (2 pi),
+// as float hi + lo pairs of the double value (m = 0 .. DK/2 - 1), so that the
+// angle of position t reduces modulo one revolution almost exactly.
+constexpr double cexp_neg(double x) {  // e^x for -10 <= x <= 0
+  double y = x / 1024.0, term = 1.0, sum = 1.0;
+  for (int n = 1; n < 24; ++n) {
+    term *= y / n;
+    sum += term;
+  }
+  for (int i = 0; i < 10; ++i) sum *= sum;
+  return sum;
+}
+struct RopeTab {
+  float hi[DK / 2], lo[DK / 2];
+};
+constexpr RopeTab make_rope_tab() {
+  RopeTab t{};
+  for (int m = 0; m < DK / 2; ++m) {
+    const double f = cexp_neg(-2.0 * m / DK * 9.210340371976184) / 6.283185307179586;
+    t.hi[m] = (float)f;
+    t.lo[m] = (float)(f - (double)t.hi[m]);
+  }
+  return t;
+}
+__constant__ RopeTab kRope = make_rope_tab();
 
 constexpr float kBias = 64.f;
 constexpr float kColLag = 16.f;
@@ -69,6 +113,27 @@ struct LinSmem {
   float inv[DV];
   float z[DK];          // sum of phi(k) over earlier chunks
   float zc[4 * DK];     // partial sums of phi(k) over this chunk (four row quarters)
+};
+
+// GLA: chunk-local running log-decay B[token][d_k] (fp32), its quarter
+// totals, and e^{R} z for the inter-chunk normaliser.
+struct GlaSmem {
+  float b[CH * DK];
+  float bq[4 * DK];
+  float zr[DK];
+};
+template <int PRIOR>
+struct ScanSmem : LinSmem {
+  __device__ float* gb() { return nullptr; }
+  __device__ float* gbq() { return nullptr; }
+  __device__ float* gzr() { return nullptr; }
+};
+template <>
+struct ScanSmem<kGla> : LinSmem {
+  GlaSmem gla;
+  __device__ float* gb() { return gla.b; }
+  __device__ float* gbq() { return gla.bq; }
+  __device__ float* gzr() { return gla.zr; }
 };
 static_assert(ROW == SROW, "S^T hi shares the V^T rows");
 
@@ -102,6 +167,63 @@ __device__ __forceinline__ float phi(float x) {
   return x > 0.f ? x + 1.f : e;
 }
 
+// RoPE of the pair (x0, x1) = dims (2m, 2m+1) at position t, then ReLU + eps.
+__device__ __forceinline__ void gla_pair(float& x0, float& x1, int m, int t) {
+  const float tf = (float)t;
+  const float p = tf * kRope.hi[m];
+  const float e = fmaf(tf, kRope.hi[m], -p);  // exact rounding error of p
+  float r = (p - floorf(p)) + (e + tf * kRope.lo[m]);
+  r -= floorf(r);
+  const float c = __builtin_amdgcn_cosf(r), s = __builtin_amdgcn_sinf(r);  // revolutions
+  const float y0 = x0 * c - x1 * s, y1 = x0 * s + x1 * c;
+  x0 = fmaxf(y0, 0.f) + kGlaEps;
+  x1 = fmaxf(y1, 0.f) + kGlaEps;
+}
+
+__device__ __forceinline__ float clip_g(float g) { return fminf(fmaxf(g, kGlaGMin), 0.f); }
+
+// Exact fp32 read of one (t, j) of the GLA prior by the whole wave: lane c
+// holds key channel c (d_k = 64), the keys are walked from t down to 0 with
+// each lane's decay exp(sum_{tau=i+1}^{t} g_tau,c) kept as a running product.
+__device__ float exact_read_gla(const bf16* __restrict__ Qh, const bf16* __restrict__ Kh,
+                                const bf16* __restrict__ Vh, const float* __restrict__ Gh,
+                                int t, int j, float bl) {
+  static_assert(DK == 64, "one lane per key channel");
+  constexpr int U = 8;  // keys whose loads are in flight together
+  const int c = threadIdx.x & 63;
+  float q0 = (float)Qh[(size_t)t * DK + (c & ~1)], q1 = (float)Qh[(size_t)t * DK + (c | 1)];
+  gla_pair(q0, q1, c >> 1, t);
+  const float qc = (c & 1) ? q1 : q0;
+  Lse2 num, den;
+  float dec = 1.f;
+  for (int i0 = t; i0 >= 0; i0 -= U) {
+    float k0[U], k1[U], gg[U], vv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = max(i0 - u, 0);
+      k0[u] = (float)Kh[(size_t)i * DK + (c & ~1)];
+      k1[u] = (float)Kh[(size_t)i * DK + (c | 1)];
+      gg[u] = Gh[(size_t)i * DK + c];
+      vv[u] = (float)Vh[(size_t)i * DV + j];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 - u;
+      if (i < 0) break;
+      gla_pair(k0[u], k1[u], c >> 1, i);
+      const float a = wave_sum(qc * ((c & 1) ? k1[u] : k0[u]) * dec);
+      if (a > 0.f) {
+        const float w = log2_hw(a);
+        den.add(w);
+        num.add(w + vv[u] * bl);
+      }
+      dec *= exp2_hw(clip_g(gg[u]) * kLog2e);
+    }
+  }
+  // every lane holds the same (num, den)
+  return (num.m + log2_hw(num.s) - (den.m + log2_hw(den.s))) / bl;
+}
+
 // Exact fp32 read of one (t, j) of the linear prior by the whole wave.
 __device__ float exact_read_linear(const bf16* __restrict__ Qh, const bf16* __restrict__ Kh,
                                    const bf16* __restrict__ Vh, int t, int j, float bl) {
@@ -124,6 +246,7 @@ __device__ float exact_read_linear(const bf16* __restrict__ Qh, const bf16* __re
 constexpr int SLOTS = CH * 8 / NTH;
 struct ChunkRegs {
   bf16x8 q[SLOTS], k[SLOTS], v[SLOTS];
+  f32x4 g[SLOTS][2];  // GLA log-decays of the slot's 8 channels
 };
 
 // Buffer resource over `bytes` bytes from `base` (raw, untyped): a load at
@@ -138,9 +261,13 @@ __device__ __forceinline__ bf16x8 load16(__amdgpu_buffer_rsrc_t r, unsigned off)
 }
 
 // Rows past T come back as zeros (the resource ends at row T).
-template <bool OUT>
+__device__ __forceinline__ f32x4 load16f(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
+template <int PRIOR, bool OUT>
 __device__ __forceinline__ void fetch_chunk(ChunkRegs& cr, const bf16* Qh, const bf16* Kh,
-                                            const bf16* Vh, int t0, int T) {
+                                            const bf16* Vh, const float* Gh, int t0, int T) {
   const int tid = threadIdx.x;
   const unsigned rows = (unsigned)min(CH, T - t0);
   const __amdgpu_buffer_rsrc_t rk = rsrc(Kh + (size_t)t0 * DK, rows * DK * 2u);
@@ -152,6 +279,15 @@ __device__ __forceinline__ void fetch_chunk(ChunkRegs& cr, const bf16* Qh, const
     cr.k[i] = load16(rk, (unsigned)(r * DK + c8) * 2u);
     cr.v[i] = load16(rv, (unsigned)(r * DV + c8) * 2u);
     if (OUT) cr.q[i] = load16(rq, (unsigned)(r * DK + c8) * 2u);
+  }
+  if (PRIOR == kGla) {
+    const __amdgpu_buffer_rsrc_t rg = rsrc(Gh + (size_t)t0 * DK, rows * DK * 4u);
+#pragma unroll
+    for (int i = 0; i < SLOTS; ++i) {
+      const int e = tid + NTH * i, r = e >> 3, c8 = (e & 7) * 8;
+      cr.g[i][0] = load16f(rg, (unsigned)(r * DK + c8) * 4u);
+      cr.g[i][1] = load16f(rg, (unsigned)(r * DK + c8 + 4) * 4u);
+    }
   }
 }
 
@@ -166,34 +302,100 @@ __device__ __forceinline__ void fetch_chunk(ChunkRegs& cr, const bf16* Qh, const
 // the keys at MFMA positions ks*16 + hl*8 .. +8 of each k-step ks, read from
 // V^T staged in the same key order.  The two waves of a channel block form
 // the same E; each lane keeps the running shift cj of its channel.
-template <bool OUT>
-__device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, float& cj, float blj,
-                                           ChunkRegs& cr, const bf16* Qh, const bf16* Kh,
-                                           const bf16* Vh, float* Oh, int t0, int tnext, int T) {
+template <int PRIOR, bool OUT>
+__device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, float& cj, float blj,
+                                           float& ldc, ChunkRegs& cr, const bf16* Qh,
+                                           const bf16* Kh, const bf16* Vh, const float* Gh,
+                                           float* Oh, int t0, int tnext, int T) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, hl = lane >> 5;
   const int dvb = wave >> 1, sub = wave & 1;
   const int ch = dvb * 32 + n;
 
-  // ---- stage phi(Q), phi(K), phi(K)^T and V^T; phi in fp32, rounded to bf16
+  if (PRIOR == kGla) {
+    // ---- chunk-local running log-decay B down each key channel: clipped g
+    // into LDS, prefix of each quarter of 16 rows, then the lower quarters'
+    // totals added (rows past T hold g = 0 from the fetch)
+#pragma unroll
+    for (int i = 0; i < SLOTS; ++i) {
+      const int e = tid + NTH * i, r = e >> 3, c8 = (e & 7) * 8;
+      f32x4 g0, g1;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        g0[u] = clip_g(cr.g[i][0][u]);
+        g1[u] = clip_g(cr.g[i][1][u]);
+      }
+      *reinterpret_cast<f32x4*>(sm.gb() + r * DK + c8) = g0;
+      *reinterpret_cast<f32x4*>(sm.gb() + r * DK + c8 + 4) = g1;
+    }
+    lds_barrier();
+    {
+      const int c = tid & 63, q4 = tid >> 6;
+      float run = 0.f;
+#pragma unroll
+      for (int r = 0; r < CH / 4; ++r) {
+        run += sm.gb()[(q4 * (CH / 4) + r) * DK + c];
+        sm.gb()[(q4 * (CH / 4) + r) * DK + c] = run;
+      }
+      sm.gbq()[q4 * DK + c] = run;
+    }
+    lds_barrier();
+    {
+      const int c = tid & 63, q4 = tid >> 6;
+      float off = 0.f;
+      for (int w = 0; w < q4; ++w) off += sm.gbq()[w * DK + c];
+      if (q4 > 0) {
+#pragma unroll
+        for (int r = 0; r < CH / 4; ++r) sm.gb()[(q4 * (CH / 4) + r) * DK + c] += off;
+      }
+    }
+    lds_barrier();
+  }
+
+  // ---- stage phi(Q), phi(K), phi(K)^T and V^T; phi in fp32, rounded to bf16.
+  // GLA: phi(Q) = q~ e^{B - R}, phi(K) = k~ e^{R - B}, phi(K)^T = k~ e^{B_last - B}.
 #pragma unroll
   for (int i = 0; i < SLOTS; ++i) {
     const int e = tid + NTH * i, r = e >> 3, c8 = (e & 7) * 8;
     // rows past T: phi of the zeros fetched there, times 0 (no branch)
     const float okf = t0 + r < T ? 1.f : 0.f;
     bf16x8 pk, pq;
+    if (PRIOR == kGla) {
+      float kx[8], qx[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      pk[u] = (bf16)(phi((float)cr.k[i][u]) * okf);
-      if (OUT) pq[u] = (bf16)(phi((float)cr.q[i][u]) * okf);
-      sm.fkt[tpos(c8 + u, e_pos(r))] = pk[u];
-      sm.vt_sh[tpos(c8 + u, e_pos(r))] = cr.v[i][u];
+      for (int u = 0; u < 8; ++u) {
+        kx[u] = (float)cr.k[i][u];
+        qx[u] = OUT ? (float)cr.q[i][u] : 0.f;
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        gla_pair(kx[2 * m], kx[2 * m + 1], c8 / 2 + m, t0 + r);
+        if (OUT) gla_pair(qx[2 * m], qx[2 * m + 1], c8 / 2 + m, t0 + r);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float b = sm.gb()[r * DK + c8 + u];
+        const float R = sm.gb()[(CH / 2 - 1) * DK + c8 + u];
+        const float bl = sm.gb()[(CH - 1) * DK + c8 + u];
+        pk[u] = (bf16)(kx[u] * exp2_hw((R - b) * kLog2e) * okf);
+        if (OUT) pq[u] = (bf16)(qx[u] * exp2_hw((b - R) * kLog2e) * okf);
+        sm.fkt[tpos(c8 + u, e_pos(r))] = (bf16)(kx[u] * exp2_hw((bl - b) * kLog2e) * okf);
+        sm.vt_sh[tpos(c8 + u, e_pos(r))] = cr.v[i][u];
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        pk[u] = (bf16)(phi((float)cr.k[i][u]) * okf);
+        if (OUT) pq[u] = (bf16)(phi((float)cr.q[i][u]) * okf);
+        sm.fkt[tpos(c8 + u, e_pos(r))] = pk[u];
+        sm.vt_sh[tpos(c8 + u, e_pos(r))] = cr.v[i][u];
+      }
     }
     *reinterpret_cast<bf16x8*>(sm.fk + r * ROW + c8) = pk;
     if (OUT) *reinterpret_cast<bf16x8*>(sm.fq + r * ROW + c8) = pq;
   }
   // the next chunk's loads run while this one is processed
-  if (tnext < T) fetch_chunk<OUT>(cr, Qh, Kh, Vh, tnext, T);
+  if (tnext < T) fetch_chunk<PRIOR, OUT>(cr, Qh, Kh, Vh, Gh, tnext, T);
   lds_barrier();
 
   // ---- tilt of the wave's channel block, in registers
@@ -247,8 +449,13 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, float& cj, f
     const int dkc = tid & 63, q4 = tid >> 6;
     float s = 0.f;
 #pragma unroll
-    for (int r = 0; r < CH / 4; ++r) s += (float)sm.fk[(q4 * (CH / 4) + r) * ROW + dkc];
+    for (int r = 0; r < CH / 4; ++r)
+      s += PRIOR == kGla ? (float)sm.fkt[tpos(dkc, q4 * (CH / 4) + r)]
+                         : (float)sm.fk[(q4 * (CH / 4) + r) * ROW + dkc];
     sm.zc[q4 * DK + dkc] = s;
+    // GLA: the inter-chunk normaliser reads e^{R} z
+    if (PRIOR == kGla && q4 == 0)
+      sm.gzr()[dkc] = sm.z[dkc] * exp2_hw(sm.gb()[(CH / 2 - 1) * DK + dkc] * kLog2e);
   }
 
   // ---- rescale the state rows (d_v) when a shift of the block rose
@@ -258,13 +465,16 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, float& cj, f
   }
   if (OUT) {
     lds_barrier();  // every wave has read V^T before S^T hi replaces it
+    const float eR =
+        PRIOR == kGla ? exp2_hw(sm.gb()[(CH / 2 - 1) * DK + sub * 32 + n] * kLog2e) : 1.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
       const int col = sub * 32 + n;
-      const bf16 hi = (bf16)st[i];
+      const float sv = st[i] * eR;
+      const bf16 hi = (bf16)sv;
       sm.vt_sh[row * SROW + col] = hi;
-      sm.sl[row * SROW + col] = (bf16)(st[i] - (float)hi);
+      sm.sl[row * SROW + col] = (bf16)(sv - (float)hi);
     }
     if (sub == 0 && hl == 0) sm.c[ch] = cj;
     lds_barrier();
@@ -322,8 +532,9 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, float& cj, f
       const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + (qb * 32 + n) * ROW + ks * 16 + hl * 8);
       num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
       num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, num, 0, 0, 0);
-      const f32x4 z0 = *reinterpret_cast<const f32x4*>(sm.z + ks * 16 + hl * 8);
-      const f32x4 z1 = *reinterpret_cast<const f32x4*>(sm.z + ks * 16 + hl * 8 + 4);
+      const float* zz = PRIOR == kGla ? sm.gzr() : sm.z;
+      const f32x4 z0 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8);
+      const f32x4 z1 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8 + 4);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         dz[u] = fmaf((float)b[u], z0[u], dz[u]);
@@ -360,7 +571,8 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, float& cj, f
       const int e = __builtin_ctz(fl);
       const int t = __builtin_amdgcn_readlane(tq, src);
       const int ch2 = dvb * 32 + (e >> 2) * 8 + (src >> 5) * 4 + (e & 3);
-      const float o = exact_read_linear(Qh, Kh, Vh, t, ch2, sm.bl[ch2]);
+      const float o = PRIOR == kGla ? exact_read_gla(Qh, Kh, Vh, Gh, t, ch2, sm.bl[ch2])
+                                    : exact_read_linear(Qh, Kh, Vh, t, ch2, sm.bl[ch2]);
       if (lane == src) {
         flags &= ~(1u << e);
         Oh[(size_t)t * DV + ch2] = o;
@@ -368,8 +580,14 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, float& cj, f
     }
   }
 
-  // ---- state update S^T(dvb, dkb = sub) += E^T phi(K)   (keys of this chunk)
+  // ---- state update S^T(dvb, dkb = sub) += E^T phi(K)   (keys of this chunk);
+  // GLA: the state first decays by e^{B_last} along its key channel (column)
   {
+    if (PRIOR == kGla) {
+      const float dcy = exp2_hw(sm.gb()[(CH - 1) * DK + sub * 32 + n] * kLog2e);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) st[i] *= dcy;
+    }
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const bf16x8 b =
@@ -380,49 +598,69 @@ __device__ __forceinline__ void scan_chunk(LinSmem& sm, f32x16& st, float& cj, f
   }
   // every read of this chunk's LDS tiles and of z is done before the next
   // chunk stages and before z moves on
+  // (B_last is read before the barrier: the next chunk overwrites B after it)
+  const float blast = (PRIOR == kGla && tid < DK) ? sm.gb()[(CH - 1) * DK + tid] : 0.f;
   lds_barrier();
-  if (tid < DK) sm.z[tid] += (sm.zc[tid] + sm.zc[DK + tid]) + (sm.zc[2 * DK + tid] + sm.zc[3 * DK + tid]);
+  if (tid < DK) {
+    const float add = (sm.zc[tid] + sm.zc[DK + tid]) + (sm.zc[2 * DK + tid] + sm.zc[3 * DK + tid]);
+    if (PRIOR == kGla) {
+      sm.z[tid] = sm.z[tid] * exp2_hw(blast * kLog2e) + add;
+      ldc += blast;  // the segment's total log-decay of channel tid
+    } else {
+      sm.z[tid] += add;
+    }
+  }
 }
 
 // Exclusive prefix of the segment states of one (b, h) (blockIdx.y): slot s
 // of `pre` receives the state entering segment s, combined from the own states
 // of segments 0 .. s-1 in `own`, each relative to its own shift.  One thread
 // per state entry: S[j][*] carries row shift c_j, z needs none, c is the max.
+// GLA: the state entering segment s+1 is the one entering s, decayed by the
+// total log-decay of segment s along its key channel, plus the own state of s.
+template <int PRIOR>
 __global__ __launch_bounds__(NTH) void prefix_kernel(const float* __restrict__ own,
                                                      float* __restrict__ pre, int nseg) {
+  constexpr int SF = state_floats<PRIOR>();
   const int e = blockIdx.x * NTH + threadIdx.x;
-  if (e >= STATE) return;
-  const size_t base = (size_t)blockIdx.y * nseg * STATE;
+  if (e >= STATE) return;  // (the GLA log-decays need no prefix)
+  const size_t base = (size_t)blockIdx.y * nseg * SF;
   const float* ob = own + base;
   float* pb = pre + base;
   const int j = e < DV * DK ? e / DK : (e >= DV * DK + DK ? e - DV * DK - DK : -1);
+  // key channel of an S or z entry (decay), -1 for a shift entry
+  const int kc = e < DV * DK ? e % DK : (e < DV * DK + DK ? e - DV * DK : -1);
   float acc = 0.f, C = -INFINITY;
   for (int sg = 0; sg + 1 < nseg; ++sg) {
-    const float val = ob[(size_t)sg * STATE + e];
+    const float val = ob[(size_t)sg * SF + e];
+    const float dcy =
+        (PRIOR == kGla && kc >= 0) ? exp2_hw(ob[(size_t)sg * SF + STATE + kc] * kLog2e) : 1.f;
     if (e < DV * DK) {
-      const float cs = ob[(size_t)sg * STATE + DV * DK + DK + j];
+      const float cs = ob[(size_t)sg * SF + DV * DK + DK + j];
       const float Cn = fmaxf(C, cs);
-      acc = acc * exp2_hw(C - Cn) + val * exp2_hw(cs - Cn);
+      acc = acc * dcy * exp2_hw(C - Cn) + val * exp2_hw(cs - Cn);
       C = Cn;
     } else if (e < DV * DK + DK) {
-      acc += val;
+      acc = acc * dcy + val;
     } else {
       acc = fmaxf(C, val);
       C = acc;
     }
-    pb[(size_t)(sg + 1) * STATE + e] = acc;
+    pb[(size_t)(sg + 1) * SF + e] = acc;
   }
 }
 
-template <bool OUT>
+template <int PRIOR, bool OUT>
 __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
                                                      const bf16* __restrict__ K,
                                                      const bf16* __restrict__ V,
+                                                     const float* __restrict__ G,
                                                      const float* __restrict__ beta,
                                                      float* __restrict__ out,
                                                      float* __restrict__ ws, int H, int T,
                                                      int nseg, int segc) {
-  __shared__ __align__(16) LinSmem sm;
+  constexpr int SF = state_floats<PRIOR>();
+  __shared__ __align__(16) ScanSmem<PRIOR> sm;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hl = lane >> 5;
   const int seg = blockIdx.x % nseg;
@@ -431,8 +669,9 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   const bf16* Qh = Q + (size_t)bh * T * DK;
   const bf16* Kh = K + (size_t)bh * T * DK;
   const bf16* Vh = V + (size_t)bh * T * DV;
+  const float* Gh = PRIOR == kGla ? G + (size_t)bh * T * DK : nullptr;
   float* Oh = out + (size_t)bh * T * DV;
-  float* wsh = ws + (size_t)bh * nseg * STATE;  // own states; entering states follow gridDim.x slots on
+  float* wsh = ws + (size_t)bh * nseg * SF;  // own states; entering states follow gridDim.x slots on
   const int dvb = wave >> 1, sub = wave & 1;
   const int ch = dvb * 32 + (lane & 31);  // this lane's tilt channel
 
@@ -445,16 +684,17 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   f32x16 st = f32x16{};
   const float blj = beta[h * DV + ch] * kLog2e;
   float cj = -INFINITY;  // running shift of channel ch
+  float ldc = 0.f;       // GLA: this segment's total log-decay of key channel tid (tid < DK)
   __syncthreads();
 
   const int tbeg = seg * segc * CH;
   const int tend = min(tbeg + segc * CH, T);
   ChunkRegs cr;
-  fetch_chunk<OUT>(cr, Qh, Kh, Vh, tbeg, T);
+  fetch_chunk<PRIOR, OUT>(cr, Qh, Kh, Vh, Gh, tbeg, T);
 
   if (OUT && seg > 0) {
     // entering state, left by the prefix kernel in the second half of ws
-    const float* S = wsh + (size_t)gridDim.x * STATE + (size_t)seg * STATE;
+    const float* S = wsh + (size_t)gridDim.x * SF + (size_t)seg * SF;
     if (tid < DK) sm.z[tid] = S[DV * DK + tid];
     cj = S[DV * DK + DK + ch];
 #pragma unroll
@@ -467,10 +707,11 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   }
 
   for (int t0 = tbeg; t0 < tend; t0 += CH)
-    scan_chunk<OUT>(sm, st, cj, blj, cr, Qh, Kh, Vh, Oh, t0, t0 + CH < tend ? t0 + CH : T, T);
+    scan_chunk<PRIOR, OUT>(sm, st, cj, blj, ldc, cr, Qh, Kh, Vh, Gh, Oh, t0,
+                           t0 + CH < tend ? t0 + CH : T, T);
 
   if (!OUT) {
-    float* S = wsh + (size_t)seg * STATE;
+    float* S = wsh + (size_t)seg * SF;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
@@ -480,15 +721,15 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
     __syncthreads();  // the last z update
     if (tid < DK) S[DV * DK + tid] = sm.z[tid];
     if (sub == 0 && hl == 0) S[DV * DK + DK + ch] = cj;
+    if (PRIOR == kGla && tid < DK) S[STATE + tid] = ldc;
   }
 }
 
-}  // namespace
-
-hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const float* beta,
-                              float* out, int B, int H, int T, int dk, int dv, int chunk,
-                              hipStream_t stream) {
-  if (dk != DK || dv != DV || chunk != CH) return hipErrorNotSupported;
+template <int PRIOR>
+hipError_t launch_scan(const void* Q, const void* K, const void* V, const float* G,
+                       const float* beta, float* out, int B, int H, int T,
+                       hipStream_t stream) {
+  constexpr int SF = state_floats<PRIOR>();
   const int nbh = B * H;
   // Segments: the scan is sequential inside one, so the fewest chunks per
   // segment that still let every workgroup be resident at once.
@@ -499,28 +740,46 @@ hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const
   const int nseg = (nchunk + segc - 1) / segc;
   float* ws = nullptr;
   // own segment states, then the entering (prefix) states
-  const size_t bytes = 2 * (size_t)nbh * nseg * STATE * sizeof(float);
+  const size_t bytes = 2 * (size_t)nbh * nseg * SF * sizeof(float);
   hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
   if (e != hipSuccess) return e;
+  const bf16* q = reinterpret_cast<const bf16*>(Q);
+  const bf16* k = reinterpret_cast<const bf16*>(K);
+  const bf16* v = reinterpret_cast<const bf16*>(V);
   if (nseg > 1) {
-    hipLaunchKernelGGL(linear_kernel<false>, dim3((unsigned)(nbh * nseg)), dim3(NTH), 0, stream,
-                       reinterpret_cast<const bf16*>(Q), reinterpret_cast<const bf16*>(K),
-                       reinterpret_cast<const bf16*>(V), beta, out, ws, H, T, nseg, segc);
+    hipLaunchKernelGGL((linear_kernel<PRIOR, false>), dim3((unsigned)(nbh * nseg)), dim3(NTH), 0,
+                       stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
     e = hipGetLastError();
     if (e == hipSuccess) {
-      hipLaunchKernelGGL(prefix_kernel, dim3((unsigned)((STATE + NTH - 1) / NTH), (unsigned)nbh),
-                         dim3(NTH), 0, stream, ws, ws + (size_t)nbh * nseg * STATE, nseg);
+      hipLaunchKernelGGL(prefix_kernel<PRIOR>,
+                         dim3((unsigned)((STATE + NTH - 1) / NTH), (unsigned)nbh), dim3(NTH), 0,
+                         stream, ws, ws + (size_t)nbh * nseg * SF, nseg);
       e = hipGetLastError();
     }
   }
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(linear_kernel<true>, dim3((unsigned)(nbh * nseg)), dim3(NTH), 0, stream,
-                       reinterpret_cast<const bf16*>(Q), reinterpret_cast<const bf16*>(K),
-                       reinterpret_cast<const bf16*>(V), beta, out, ws, H, T, nseg, segc);
+    hipLaunchKernelGGL((linear_kernel<PRIOR, true>), dim3((unsigned)(nbh * nseg)), dim3(NTH), 0,
+                       stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
     e = hipGetLastError();
   }
   const hipError_t f = workspace_free(ws, stream);
   return e != hipSuccess ? e : f;
+}
+
+}  // namespace
+
+hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const float* beta,
+                              float* out, int B, int H, int T, int dk, int dv, int chunk,
+                              hipStream_t stream) {
+  if (dk != DK || dv != DV || chunk != CH) return hipErrorNotSupported;
+  return launch_scan<kElu>(Q, K, V, nullptr, beta, out, B, H, T, stream);
+}
+
+hipError_t launch_gla_bf16(const void* Q, const void* K, const void* V, const float* G,
+                           const float* beta, float* out, int B, int H, int T, int dk, int dv,
+                           int chunk, hipStream_t stream) {
+  if (dk != DK || dv != DV || chunk != CH) return hipErrorNotSupported;
+  return launch_scan<kGla>(Q, K, V, G, beta, out, B, H, T, stream);
 }
 
 }  // namespace fem

@@ -24,6 +24,10 @@ near 1 and in between; g = softplus(y), y ~ N(0, 1), divided by its root mean
 square over the channels of the step (the paper's RMS-normalised positive
 outer gate, with unit scale).
 
+GLA log-decays (``draw_gla_decay``), per (b, h, t, c): g = log(sigmoid(z)) / 16,
+z ~ N(0, 1) -- the gate parameterisation of gated linear attention with its
+usual normaliser of 16, i.e. decay factors around 0.96 per step.
+
 The paper's own speed measurements use randomly generated data, and its
 language-model runs use T=4096 with head dimension 128; these shapes stand in
 for those workloads.  beta has shape [H, d] (one inverse temperature per head
@@ -137,3 +141,12 @@ def draw_gates(seed: int, B: int, H: int, T: int, d: int):
     g = g / np.sqrt(np.mean(g * g, axis=-1, keepdims=True))
     return torch.from_numpy(np.ascontiguousarray(lam)), \
         torch.from_numpy(np.ascontiguousarray(g.astype(np.float32)))
+
+
+def draw_gla_decay(seed: int, B: int, H: int, T: int, dk: int, scale: float = 1.0 / 16.0):
+    """Draw GLA log-decays g = scale * log(sigmoid(z)), z ~ N(0, 1), as a CPU
+    float32 tensor [B, H, T, dk] (recipe above)."""
+    rng = np.random.default_rng(seed)
+    z = rng.standard_normal((B, H, T, dk))
+    g = -np.logaddexp(0.0, -z) * scale
+    return torch.from_numpy(np.ascontiguousarray(g.astype(np.float32)))

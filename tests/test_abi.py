@@ -126,3 +126,16 @@ def test_decode_validation(lib):
     assert dec(lib, dqk=32, dv=64) == UNSUPPORTED
     assert dec(lib, dt=F32) == UNSUPPORTED
     assert dec(lib, k=A + 4) == ALIGN
+
+
+def gla(lib, q=A, k=A, v=A, g=A, beta=A, out=A, B=1, H=1, T=8, dk=64, dv=64, chunk=64, dt=BF16):
+    return lib.fem_gla_fwd(q, k, v, g, beta, out, B, H, T, dk, dv, chunk, dt, None)
+
+
+def test_gla_validation(lib):
+    assert gla(lib, g=None) == NULLPTR
+    assert gla(lib, T=0) == SHAPE
+    assert gla(lib, dk=128) == UNSUPPORTED
+    assert gla(lib, chunk=32) == UNSUPPORTED
+    assert gla(lib, dt=F32) == UNSUPPORTED
+    assert gla(lib, g=A + 4) == ALIGN

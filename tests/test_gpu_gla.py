@@ -1,0 +1,111 @@
+"""GPU parity of fem_gla_fwd (GLA-prior FEM read, HIP through the C ABI)
+against the float64 oracle's fem_gla.
+
+Tolerance: 2e-2 max abs (the bf16-input budget).  Every case prints its name,
+shape and seed before touching the GPU.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_07160_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def run(fem, q, k, v, g, b):
+    dev = torch.device("cuda:0")
+    out = fem.fem_gla_fwd(q.to(dev), k.to(dev), v.to(dev), g.to(dev), b.to(dev))
+    torch.cuda.synchronize()
+    return out.cpu().double().numpy()
+
+
+def ref(q, k, v, g, b, rows=None):
+    return oracle.fem_gla(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                          g.double().numpy(), b.double().numpy(), rows=rows)
+
+
+def check(got, want, what):
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got - want).max()
+    say(f"{what}: max abs err {err:.3e} (tol {TOL})")
+    assert err <= TOL, f"{what}: {err} > {TOL}"
+
+
+@pytest.mark.parametrize("T", [1, 63, 64, 65, 200, 700, 2000])
+def test_gla_shapes(fem, T):
+    say(f"gla B2 H3 T{T} d64, seeds {10000 + T}/{11000 + T}")
+    q, k, v, b = inputs.draw(10000 + T, 2, 3, T, 64, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
+    g = inputs.draw_gla_decay(11000 + T, 2, 3, T, 64)
+    check(run(fem, q, k, v, g, b), ref(q, k, v, g, b), f"gla T{T}")
+
+
+@pytest.mark.parametrize("regime", ["none", "strong", "clipped"])
+def test_gla_decay_regimes(fem, regime):
+    say(f"gla decay regime {regime}: B1 H2 T900 d64, seed 12000")
+    q, k, v, b = inputs.draw(12000, 1, 2, 900, 64, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
+    if regime == "none":
+        g = torch.zeros(1, 2, 900, 64)
+    elif regime == "strong":
+        g = inputs.draw_gla_decay(12001, 1, 2, 900, 64, scale=1.0)
+    else:  # values outside [-2, 0] are clipped by the kernel and the oracle alike
+        g = 3.0 * torch.randn(1, 2, 900, 64, generator=torch.Generator().manual_seed(12002))
+    check(run(fem, q, k, v, g, b), ref(q, k, v, g, b), f"gla {regime}")
+
+
+def test_gla_full_size_sampled(fem):
+    say("gla B4 H16 T8192 d64 (workload 5 shapes), seeds 47/12100, sampled rows")
+    q, k, v, b = inputs.make_inputs(5)
+    g = inputs.draw_gla_decay(12100, 4, 16, 8192, 64)
+    got = run(fem, q, k, v, g, b)
+    rows = np.array([0, 1, 63, 64, 1023, 1024, 4095, 5000, 8190, 8191])
+    for bb, hh in [(0, 0), (3, 15)]:
+        sl = lambda x: x[bb:bb + 1, hh:hh + 1]
+        want = ref(sl(q), sl(k), sl(v), sl(g), b[hh:hh + 1], rows=rows)[0, 0]
+        check(got[bb, hh, rows], want, f"gla T8192 b{bb} h{hh}")
+
+
+def test_gla_underflow_repair(fem):
+    """Values -5 with one +5 at key 32 and beta = 16: the chunk's column shift
+    leaves rows 0..31 with an underflowed numerator, repaired exactly."""
+    say("gla forced underflow: B1 H1 T200 d64, v=-5 then +5 at key 32, beta=16")
+    q, k, _, _ = inputs.draw(12200, 1, 1, 200, 64, dtype="bf16")
+    v = torch.full((1, 1, 200, 64), -5.0)
+    v[:, :, 32] = 5.0
+    v[:, :, 40:] = torch.randn(1, 1, 160, 64, generator=torch.Generator().manual_seed(1))
+    v = v.to(torch.bfloat16)
+    b = torch.full((1, 64), 16.0)
+    g = inputs.draw_gla_decay(12201, 1, 1, 200, 64)
+    got = run(fem, q, k, v, g, b)
+    check(got, ref(q, k, v, g, b), "gla underflow repair")
+    np.testing.assert_allclose(got[0, 0, :32], -5.0, atol=TOL)
+
+
+def test_gla_deterministic(fem):
+    say("gla determinism: B2 H2 T1500 d64, seed 12300")
+    q, k, v, b = inputs.draw(12300, 2, 2, 1500, 64, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
+    g = inputs.draw_gla_decay(12301, 2, 2, 1500, 64)
+    assert np.array_equal(run(fem, q, k, v, g, b), run(fem, q, k, v, g, b))
+
+
+def test_gla_rejects_bad_arguments(fem):
+    say("gla argument errors")
+    dev = torch.device("cuda:0")
+    q = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16, device=dev)
+    b = torch.ones(1, 64, device=dev)
+    with pytest.raises(ValueError):
+        fem.fem_gla_fwd(q, q, q, torch.zeros(1, 1, 8, 32, device=dev), b)
+    with pytest.raises(fem.FemError) as e:
+        fem.fem_gla_fwd(q, q, q, torch.zeros(1, 1, 8, 64, device=dev), b, chunk=32)
+    assert e.value.status == 3
