@@ -15,6 +15,7 @@ from .fem_oracle import (  # noqa: F401
     ltl_read,
     fem_softmax_ltl,
     fem_softmax,
+    fem_softmax_grads,
     fem_softmax_encoder,
     fem_softmax_decode,
     softmax_prior_all,

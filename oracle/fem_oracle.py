@@ -230,6 +230,51 @@ def fem_softmax(q, k, v, beta, rows=None, block: int = 512) -> np.ndarray:
     return out
 
 
+def fem_softmax_grads(q, k, v, beta, gout, block: int = 128):
+    """Gradients of L = sum_{b,h,t,j} gout[b,h,t,j] F[b,h,t,j] for the causal
+    softmax-prior read, from the paper's closed forms:
+      dF_tj/dv_ij = q_tj(i)                 (posterior; Proposition "Local
+                                              geometry", eq. app-grad-hess)
+      dF_tj/db_ti = (q_tj(i) - p_t(i))/beta_j  (normalized logits b; prior
+                                              sensitivity, Proposition (iv))
+      dF_tj/dbeta_j = KL(q_tj || p_t)/beta_j^2   (eq. app-beta-deriv)
+    with q_tj(i) = p_t(i) e^{beta_j v_ij} / sum_r p_t(r) e^{beta_j v_rj} and
+    b_ti = q_t.k_i / sqrt d, so dQ = dB K / sqrt d and dK = dB^T Q / sqrt d.
+    Returns float64 (dq, dk, dv, dbeta) shaped like q, k, v and beta [H, d_v]
+    (dbeta summed over batch and time).
+    """
+    q, k, v, beta, gout = _as64(q), _as64(k), _as64(v), _as64(beta), _as64(gout)
+    B, H, T, d = q.shape
+    dv_ = v.shape[3]
+    dq, dk, dvv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    dbeta = np.zeros((H, dv_))
+    for b in range(B):
+        for h in range(H):
+            bt = beta[h]
+            x = v[b, h] * bt[None, :]                       # beta v   [T, D]
+            for r0 in range(0, T, block):
+                rows = np.arange(r0, min(T, r0 + block))
+                n = int(rows[-1]) + 1
+                p = softmax_prior_rows(q[b, h], k[b, h], rows)   # [R, n]
+                with np.errstate(divide="ignore"):
+                    lp = np.log(p)
+                # posterior q_tj(i) in log space, per channel: [R, n, D]
+                w = lp[:, :, None] + x[None, :n, :]
+                m = w.max(axis=1, keepdims=True)
+                post = np.exp(w - m)
+                post /= post.sum(axis=1, keepdims=True)
+                g = gout[b, h, rows]                          # [R, D]
+                dvv[b, h, :n] += np.einsum("rj,rij->ij", g, post)
+                dB = np.einsum("rj,rij->ri", g / bt[None, :], post) - \
+                    p * (g / bt[None, :]).sum(axis=1, keepdims=True)
+                dq[b, h, rows] += dB @ k[b, h, :n] / math.sqrt(d)
+                dk[b, h, :n] += dB.T @ q[b, h, rows] / math.sqrt(d)
+                with np.errstate(divide="ignore", invalid="ignore"):
+                    kl = np.where(post > 0, post * (np.log(post) - lp[:, :, None]), 0.0).sum(axis=1)
+                dbeta[h] += (g * kl).sum(axis=0) / bt ** 2
+    return dq, dk, dvv, dbeta
+
+
 def fem_softmax_encoder(q, k, v, beta, rows=None, block: int = 512) -> np.ndarray:
     """FEM read with the unmasked (encoder) softmax prior: every query sees
     all T keys.  Shapes as fem_softmax (d_v may differ from d)."""
