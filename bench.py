@@ -16,7 +16,11 @@ two-level gated read (fem_softmax_gated_fwd) on the headline shape under
 (fem_softmax_decode) against a full B=8, H=16, L=4096, d=128 KV cache under
 "decode" (bytes = the caches read once + q + out), and the GLA-prior read
 (fem_gla_fwd) on the linear workload's shape with seeded log-decays under
-"gla" (bytes = q, k, v, the fp32 decays and out, once each).
+"gla" (bytes = q, k, v, the fp32 decays and out, once each), and the
+backward pass (fem_softmax_bwd) on the headline shape under "backward": its
+posterior terms (t, i <= t, j) are each evaluated twice (dK/dV and dQ
+kernels) with one exponential, so its roofline is the vector units'
+transcendental rate.
 """
 
 from __future__ import annotations
@@ -33,6 +37,9 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak (published)
+# v_exp_f32 at a quarter of the fp32 vector rate: 256 CUs x 4 SIMDs x 16 lanes
+# x 2.4 GHz / 4
+PEAK_EXP_PER_S = 256 * 4 * 16 * 2.4e9 / 4
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -111,6 +118,8 @@ def main():
     ap.add_argument("--no-gated", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-gla", action="store_true")
+    ap.add_argument("--no-backward", action="store_true")
+    ap.add_argument("--backward-steps", type=int, default=3)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a known-size "
                          "kernel for calibrating hardware byte counters)")
@@ -186,6 +195,23 @@ def main():
             "kernels": ["softmax_bf16_kernel<128,8,kMean>", "softmax_bf16_kernel<128,8,kGated>"],
         }
         del lamd, gd
+    if not args.no_backward:
+        outt, lse = binding.fem_softmax_fwd_train(qd, kd, vd, bd)
+        gout = torch.randn(outt.shape, device=dev, dtype=torch.float32,
+                           generator=torch.Generator(device=dev).manual_seed(7))
+        fnb = lambda: binding.fem_softmax_bwd(qd, kd, vd, bd, outt, lse, gout)
+        msb = time_calls(fnb, args.backward_steps, 1)
+        terms = B * H * T * (T + 1) / 2 * d
+        exp_rate = 2 * terms / (msb * 1e-3)
+        result["backward"] = {
+            "workload": w.name + "_bwd", "ms": round(msb, 3), "steps": args.backward_steps,
+            "posterior_terms": terms,
+            "exp_per_s": exp_rate,
+            "peak_exp_per_s": PEAK_EXP_PER_S,
+            "frac": round(exp_rate / PEAK_EXP_PER_S, 4),
+            "kernels": ["bwd_kv_kernel<128>", "bwd_q_kernel<128>", "dbeta_final_kernel<128>"],
+        }
+        del outt, lse, gout
     if not args.no_decode:
         q1 = qd[:, :, -1].contiguous()
         outd = torch.empty((B, H, d), device=dev, dtype=torch.float32)

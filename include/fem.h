@@ -146,6 +146,41 @@ int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
                        hipStream_t stream);
 
 /*
+ * Training pair of the causal softmax-prior read (bf16 inputs, d = 32, 64 or
+ * 128).
+ *
+ * fem_softmax_fwd_train: fem_softmax_fwd that also writes
+ *   lse[b,h,t] = ln sum_{i <= t} exp(q_t . k_i / sqrt d)      [B, H, T] float32,
+ * the prior's log-normaliser, which the backward pass reads.
+ *
+ * fem_softmax_bwd: gradients of L = sum dout * out from the paper's closed
+ * forms (posterior as the value gradient, Proposition "Local geometry" /
+ * eq. app-grad-hess; (q - p)/beta as the normalized-logit gradient, prior
+ * sensitivity (iv); KL(q || p)/beta^2 as the temperature derivative, eq.
+ * app-beta-deriv):
+ *   Q, K, V, beta  : the forward's inputs
+ *   out, lse       : the forward's outputs (fem_softmax_fwd_train)
+ *   dout           : [B, H, T, d] float32, dL/dout
+ *   dQ, dK, dV     : [B, H, T, d] float32, overwritten
+ *   dbeta          : [H, d] float32, overwritten (summed over batch and time)
+ * The posterior is evaluated element by element in the exponent domain, so
+ * the pass is exact in form for every beta > 0 (no shared shift, no
+ * underflow case), at O(T^2 d) exponentials; dbeta is formed from the
+ * normalised posterior sums, so the forward's rounding of out cancels from
+ * it.  A workspace of 4 * B * H * ceil(T / 64) * d bytes comes from the
+ * library's pool as in fem_linear_fwd.  All pointers 16-byte aligned;
+ * outputs must not alias inputs.  Returns a fem_status.
+ */
+int fem_softmax_fwd_train(const void* Q, const void* K, const void* V,
+                          const float* beta, float* out, float* lse,
+                          int B, int H, int T, int d, int dtype, hipStream_t stream);
+
+int fem_softmax_bwd(const void* Q, const void* K, const void* V,
+                    const float* beta, const float* out, const float* lse,
+                    const float* dout, float* dQ, float* dK, float* dV, float* dbeta,
+                    int B, int H, int T, int d, int dtype, hipStream_t stream);
+
+/*
  * Two-level gated FEM read with the causal softmax prior (Sec. "Two-Level
  * Gated FEM", eqs. inner-gate-main and fem-two-gates-main; the inner gate is
  * the linearized temperature learning of eqs. ltl and ltl-final):

@@ -18,8 +18,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfem.so")
 
 FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 
-EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_gated_fwd",
-           "fem_softmax_decode", "fem_linear_fwd", "fem_gla_fwd", "fem_status_str")
+EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_fwd_train", "fem_softmax_bwd",
+           "fem_softmax_gated_fwd", "fem_softmax_decode", "fem_linear_fwd", "fem_gla_fwd",
+           "fem_status_str")
 
 FEM_FLAG_ENCODER = 1
 FEM_FLAG_OUT_BF16 = 2
@@ -53,6 +54,10 @@ def load() -> ctypes.CDLL:
         lib.fem_linear_fwd.restype = i
         lib.fem_gla_fwd.argtypes = [vp, vp, vp, f, f, f, i, i, i, i, i, i, i, vp]
         lib.fem_gla_fwd.restype = i
+        lib.fem_softmax_fwd_train.argtypes = [vp, vp, vp, f, f, f, i, i, i, i, i, vp]
+        lib.fem_softmax_fwd_train.restype = i
+        lib.fem_softmax_bwd.argtypes = [vp, vp, vp, f, f, f, f, f, f, f, f, i, i, i, i, i, vp]
+        lib.fem_softmax_bwd.restype = i
         lib.fem_status_str.argtypes = [i]
         lib.fem_status_str.restype = ctypes.c_char_p
         _lib = lib
@@ -273,3 +278,59 @@ def fem_gla_fwd(q, k, v, g, beta, out=None, chunk: int = 64, stream=None) -> tor
                              FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
     _check(rc)
     return out
+
+
+def fem_softmax_fwd_train(q, k, v, beta, out=None, lse=None, stream=None):
+    """fem_softmax_fwd (bf16) that also returns the prior's log-normaliser
+    lse [B, H, T] fp32.  Returns (out, lse)."""
+    lib = load()
+    for name, x in (("q", q), ("k", k), ("v", v)):
+        _dev_tensor(x, name, torch.bfloat16)
+        if x.dim() != 4 or x.shape != q.shape:
+            raise ValueError(f"{name} must be [B, H, T, d] like q")
+    B, H, T, d = q.shape
+    _dev_tensor(beta, "beta", torch.float32)
+    if tuple(beta.shape) != (H, d):
+        raise ValueError("beta must be [H, d]")
+    out = torch.empty((B, H, T, d), device=q.device, dtype=torch.float32) if out is None else out
+    lse = torch.empty((B, H, T), device=q.device, dtype=torch.float32) if lse is None else lse
+    _dev_tensor(out, "out", torch.float32)
+    _dev_tensor(lse, "lse", torch.float32)
+    if tuple(out.shape) != (B, H, T, d) or tuple(lse.shape) != (B, H, T):
+        raise ValueError("out must be [B, H, T, d] and lse [B, H, T]")
+    with torch.cuda.device(q.device):
+        rc = lib.fem_softmax_fwd_train(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
+                                       out.data_ptr(), lse.data_ptr(), B, H, T, d,
+                                       FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+    _check(rc)
+    return out, lse
+
+
+def fem_softmax_bwd(q, k, v, beta, out, lse, dout, stream=None):
+    """Gradients of sum(dout * out) w.r.t. q, k, v (fp32, shaped like them) and
+    beta ([H, d], summed over batch and time).  Returns (dq, dk, dv, dbeta)."""
+    lib = load()
+    for name, x in (("q", q), ("k", k), ("v", v)):
+        _dev_tensor(x, name, torch.bfloat16)
+        if x.dim() != 4 or x.shape != q.shape:
+            raise ValueError(f"{name} must be [B, H, T, d] like q")
+    B, H, T, d = q.shape
+    _dev_tensor(beta, "beta", torch.float32)
+    for name, x, shp in (("out", out, (B, H, T, d)), ("lse", lse, (B, H, T)),
+                         ("dout", dout, (B, H, T, d))):
+        _dev_tensor(x, name, torch.float32)
+        if tuple(x.shape) != shp:
+            raise ValueError(f"{name} must be {list(shp)}")
+    if tuple(beta.shape) != (H, d):
+        raise ValueError("beta must be [H, d]")
+    dq = torch.empty((B, H, T, d), device=q.device, dtype=torch.float32)
+    dk = torch.empty_like(dq)
+    dv = torch.empty_like(dq)
+    db = torch.empty((H, d), device=q.device, dtype=torch.float32)
+    with torch.cuda.device(q.device):
+        rc = lib.fem_softmax_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
+                                 out.data_ptr(), lse.data_ptr(), dout.data_ptr(), dq.data_ptr(),
+                                 dk.data_ptr(), dv.data_ptr(), db.data_ptr(), B, H, T, d,
+                                 FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+    _check(rc)
+    return dq, dk, dv, db

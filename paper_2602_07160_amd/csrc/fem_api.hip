@@ -76,6 +76,34 @@ extern "C" int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
       fem::launch_decode_bf16(q, Kc, Vc, lens, beta, out, B, H, L, d_qk, d_v, stream));
 }
 
+extern "C" int fem_softmax_fwd_train(const void* Q, const void* K, const void* V,
+                                     const float* beta, float* out, float* lse, int B, int H,
+                                     int T, int d, int dtype, hipStream_t stream) {
+  if (!Q || !K || !V || !beta || !out || !lse) return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, T, d)) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  if (d != 32 && d != 64 && d != 128) return FEM_ERR_UNSUPPORTED;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return FEM_ERR_ALIGN;
+  return from_hip(fem::launch_softmax_train_bf16(Q, K, V, beta, out, lse, B, H, T, d, stream));
+}
+
+extern "C" int fem_softmax_bwd(const void* Q, const void* K, const void* V, const float* beta,
+                               const float* out, const float* lse, const float* dout, float* dQ,
+                               float* dK, float* dV, float* dbeta, int B, int H, int T, int d,
+                               int dtype, hipStream_t stream) {
+  if (!Q || !K || !V || !beta || !out || !lse || !dout || !dQ || !dK || !dV || !dbeta)
+    return FEM_ERR_NULLPTR;
+  if (!sizes_ok(B, H, T, d)) return FEM_ERR_SHAPE;
+  if ((unsigned long long)H > 65535ull) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  if (d != 32 && d != 64 && d != 128) return FEM_ERR_UNSUPPORTED;
+  const void* ptrs[] = {Q, K, V, out, dout, dQ, dK, dV};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return FEM_ERR_ALIGN;
+  return from_hip(fem::launch_softmax_bwd_bf16(Q, K, V, beta, out, lse, dout, dQ, dK, dV, dbeta,
+                                               B, H, T, d, stream));
+}
+
 extern "C" int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V,
                                      const float* beta_max, const float* lam, const float* gate,
                                      float* out, int B, int H, int T, int d, int dtype,

@@ -16,6 +16,18 @@ hipError_t launch_softmax_ex_bf16(const void* Q, const void* K, const void* V, c
                                   void* out, int B, int H, int T, int dk, int dv, bool causal,
                                   bool obf16, hipStream_t stream);
 
+// The plain causal read (bf16, d in {32, 64, 128}) that also writes the
+// prior's log-normaliser lse [B, H, T] (natural log) for the backward pass.
+hipError_t launch_softmax_train_bf16(const void* Q, const void* K, const void* V,
+                                     const float* beta, float* out, float* lse, int B, int H,
+                                     int T, int d, hipStream_t stream);
+
+// Backward of the causal softmax-prior read (bf16 inputs, d in {32, 64, 128}).
+hipError_t launch_softmax_bwd_bf16(const void* Q, const void* K, const void* V,
+                                   const float* beta, const float* out, const float* lse,
+                                   const float* dout, float* dQ, float* dK, float* dV,
+                                   float* dbeta, int B, int H, int T, int d, hipStream_t stream);
+
 // Two-level gated read g * ((1 - lam) mu + lam F(beta_max)) with the softmax
 // prior, bf16, d in {32, 64, 128}; gate may be null (g = 1).
 hipError_t launch_softmax_gated_bf16(const void* Q, const void* K, const void* V,

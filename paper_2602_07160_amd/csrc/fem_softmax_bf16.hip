@@ -582,8 +582,8 @@ __device__ __forceinline__ void phase2(const Smem<C>& sm, f32x16 (&acc)[C::NCB],
 template <class C>
 __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ beta, const float* lam, const float* gate, float* out, int H,
-    int T, int nqb, int nbh) {
+    const float* __restrict__ beta, const float* lam, const float* gate, float* out,
+    float* __restrict__ lse, int H, int T, int nqb, int nbh) {
   constexpr int MODE = C::MODE;
   extern __shared__ __align__(16) unsigned char smem[];
   const Smem<C> sm{smem};
@@ -798,6 +798,8 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
   // logarithms are split into exponent and mantissa so the bias and the
   // integer parts cancel exactly (tiny beta amplifies any error here).
   const float lt = lacc[0];
+  // the prior's log-normaliser ln sum_i exp(q.k_i / sqrt d), for a backward pass
+  if (MODE == kFem && lse && hl == 0 && tq < T) lse[(size_t)bh * T + tq] = (m + log2_hw(lt)) * kLn2;
   int el;
   const float fl = log2_hw(frexpf(lt, &el));
   const float* cw = sm.c((ntiles - 1) & 1);  // the accumulator's final column frame
@@ -874,7 +876,7 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
 template <class C>
 hipError_t launch(const void* Q, const void* K, const void* V, const float* beta,
                   const float* lam, const float* gate, void* out, int B, int H, int T,
-                  hipStream_t stream) {
+                  hipStream_t stream, float* lse = nullptr) {
   static std::once_flag once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(once, [] {
@@ -888,7 +890,7 @@ hipError_t launch(const void* Q, const void* K, const void* V, const float* beta
   hipLaunchKernelGGL((softmax_bf16_kernel<C>), grid, block, C::LDS, stream,
                      reinterpret_cast<const bf16*>(Q), reinterpret_cast<const bf16*>(K),
                      reinterpret_cast<const bf16*>(V), beta, lam, gate,
-                     reinterpret_cast<float*>(out), H, T, nqb, nbh);
+                     reinterpret_cast<float*>(out), lse, H, T, nqb, nbh);
   return hipGetLastError();
 }
 
@@ -937,6 +939,21 @@ hipError_t launch_softmax_ex_bf16(const void* Q, const void* K, const void* V, c
   if (dk == 64 && dv == 32) return go(launch_ex<64, 32>);
   if (dk == 128 && dv == 64) return go(launch_ex<128, 64>);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_softmax_train_bf16(const void* Q, const void* K, const void* V,
+                                     const float* beta, float* out, float* lse, int B, int H,
+                                     int T, int d, hipStream_t stream) {
+  switch (d) {
+    case 32:
+      return launch<Cfg<32, 32, 8, kFem>>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream, lse);
+    case 64:
+      return launch<Cfg<64, 64, 8, kFem>>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream, lse);
+    case 128:
+      return launch<Cfg<128, 128, 8, kFem>>(Q, K, V, beta, nullptr, nullptr, out, B, H, T, stream,
+                                            lse);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_softmax_gated_bf16(const void* Q, const void* K, const void* V,

@@ -139,3 +139,20 @@ def test_gla_validation(lib):
     assert gla(lib, chunk=32) == UNSUPPORTED
     assert gla(lib, dt=F32) == UNSUPPORTED
     assert gla(lib, g=A + 4) == ALIGN
+
+
+def test_train_and_backward_validation(lib):
+    tr = lambda **kw: lib.fem_softmax_fwd_train(*[kw.get(n, A) for n in ("q", "k", "v", "b", "o", "l")],
+                                                kw.get("B", 1), 1, 8, kw.get("d", 64), kw.get("dt", BF16), None)
+    assert tr(l=None) == NULLPTR
+    assert tr(d=96) == UNSUPPORTED
+    assert tr(dt=F32) == UNSUPPORTED
+    assert tr(o=A + 4) == ALIGN
+    names = ("q", "k", "v", "b", "o", "l", "g", "dq", "dk", "dv", "db")
+    bw = lambda **kw: lib.fem_softmax_bwd(*[kw.get(n, A) for n in names], kw.get("B", 1), 1, 8,
+                                          kw.get("d", 64), kw.get("dt", BF16), None)
+    assert bw(db=None) == NULLPTR
+    assert bw(g=None) == NULLPTR
+    assert bw(B=0) == SHAPE
+    assert bw(d=16) == UNSUPPORTED
+    assert bw(dk=A + 8) == ALIGN

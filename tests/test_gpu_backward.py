@@ -1,0 +1,118 @@
+"""GPU parity of the training pair fem_softmax_fwd_train / fem_softmax_bwd
+(HIP, through the C ABI) against the float64 oracle's gradients.
+
+Tolerances (written per check): lse within 1e-2 absolute (the forward sums
+bf16-rounded probabilities, a relative 2^-9 per term); each gradient within
+2e-2 of its own scale plus a floor, max |g - g_ref| <= 2e-2 * max |g_ref| +
+1e-4 (the posterior uses the forward's F, whose bf16 rounding moves beta F by
+at most 2^-8, and dS enters the dQ / dK products in bf16; the floor covers
+fp32 rounding of sum_j (G/beta) q - p sum_j G/beta, which cancels exactly
+where the gradient is zero, e.g. a single key).  Every case prints its name, shape
+and seed before touching the GPU.
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_07160_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+ATOL = 1e-4
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def run(fem, q, k, v, b, g):
+    dev = torch.device("cuda:0")
+    qd, kd, vd, bd, gd = (x.to(dev) for x in (q, k, v, b, g))
+    out, lse = fem.fem_softmax_fwd_train(qd, kd, vd, bd)
+    grads = fem.fem_softmax_bwd(qd, kd, vd, bd, out, lse, gd)
+    torch.cuda.synchronize()
+    return out.cpu().double().numpy(), lse.cpu().double().numpy(), \
+        [x.cpu().double().numpy() for x in grads]
+
+
+def lse_ref(q, k):
+    qq, kk = q.double(), k.double()
+    T, d = q.shape[2], q.shape[3]
+    s = qq @ kk.transpose(-1, -2) / math.sqrt(d)
+    s = s.masked_fill(torch.triu(torch.ones(T, T, dtype=torch.bool), 1), float("-inf"))
+    return torch.logsumexp(s, dim=-1).numpy()
+
+
+def check_grads(got, want, what):
+    for name, a, b in zip(("dq", "dk", "dv", "dbeta"), got, want):
+        assert np.isfinite(a).all(), f"{what} {name}: non-finite"
+        scale = np.abs(b).max()
+        err = np.abs(a - b).max()
+        say(f"{what} {name}: max err {err:.3e}, scale {scale:.3e} (tol {TOL} * scale + {ATOL})")
+        assert err <= TOL * scale + ATOL, f"{what} {name}: {err} > {TOL} * {scale} + {ATOL}"
+
+
+def draw(seed, B, H, T, d, **kw):
+    q, k, v, b = inputs.draw(seed, B, H, T, d, dtype="bf16", **kw)
+    g = torch.from_numpy(np.random.default_rng(seed + 1).standard_normal((B, H, T, d)).astype(np.float32))
+    return q, k, v, b, g
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("T", [1, 33, 64, 65, 200])
+def test_backward_shapes(fem, d, T):
+    seed = 13000 + T + d
+    say(f"backward B2 H2 T{T} d{d}, seed {seed}")
+    q, k, v, b, g = draw(seed, 2, 2, T, d)
+    out, lse, grads = run(fem, q, k, v, b, g)
+    err = np.abs(lse - lse_ref(q, k)).max()
+    say(f"lse: max err {err:.3e} (tol 1e-2)")
+    assert err <= 1e-2
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, f"T{T} d{d}")
+
+
+def test_backward_forward_output_unchanged(fem):
+    say("fem_softmax_fwd_train out == fem_softmax_fwd out: B1 H2 T300 d128, seed 13100")
+    q, k, v, b, g = draw(13100, 1, 2, 300, 128)
+    dev = torch.device("cuda:0")
+    a = fem.fem_softmax_fwd(q.to(dev), k.to(dev), v.to(dev), b.to(dev))
+    out, _, _ = run(fem, q, k, v, b, g)
+    assert np.array_equal(a.cpu().double().numpy(), out)
+
+
+@pytest.mark.parametrize("beta", [0.01, 1.0, 16.0])
+def test_backward_beta_extremes(fem, beta):
+    say(f"backward constant beta {beta}: B1 H2 T256 d64, seed 13200")
+    q, k, v, _, g = draw(13200, 1, 2, 256, 64)
+    b = torch.full((2, 64), beta)
+    _, _, grads = run(fem, q, k, v, b, g)
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, f"beta={beta}")
+
+
+def test_backward_longer_sequence(fem):
+    say("backward B1 H2 T1024 d128 (workload-3 recipe), seed 13300")
+    q, k, v, b, g = draw(13300, 1, 2, 1024, 128)
+    _, _, grads = run(fem, q, k, v, b, g)
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, "T1024 d128")
+
+
+def test_backward_deterministic(fem):
+    say("backward determinism: B2 H2 T500 d64, seed 13400")
+    q, k, v, b, g = draw(13400, 2, 2, 500, 64)
+    a = run(fem, q, k, v, b, g)[2]
+    c = run(fem, q, k, v, b, g)[2]
+    for x, y in zip(a, c):
+        assert np.array_equal(x, y)
