@@ -48,15 +48,14 @@ def kernel_source_sha(name: str) -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic(kernel_file: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current source of the kernel; else None."""
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of ``kernel`` from the committed rocprofv3 counter
+    summary, if it was taken on the current source of the kernel; else None."""
     try:
-        doc = json.load(open(TRAFFIC_FILE))
-        ent = doc[kernel_file]
+        ent = json.load(open(TRAFFIC_FILE))[kernel]
     except Exception:
         return None
-    if ent.get("source_sha") != kernel_source_sha(kernel_file):
+    if ent.get("source_sha") != kernel_source_sha(ent["source"]):
         return None
     return ent["fetch_bytes"] + ent["write_bytes"]
 
@@ -175,7 +174,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic("fem_softmax_bf16.hip"),
+            "traffic": measured_traffic("softmax_bf16_kernel<128,8,kFem>"),
             "kernel": "softmax_bf16_kernel<128,8,kFem>",
         },
     }
