@@ -208,7 +208,7 @@ def main():
             "exp_per_s": exp_rate,
             "peak_exp_per_s": PEAK_EXP_PER_S,
             "frac": round(exp_rate / PEAK_EXP_PER_S, 4),
-            "kernels": ["bwd_kv_kernel<128>", "bwd_q_kernel<128>", "dbeta_final_kernel<128>"],
+            "kernels": ["bwd_q_fast_kernel<128>", "bwd_kv_fast_kernel<128>", "bwd_lse_kernel<128>", "bwd_prep_kernel<128>"],
         }
         del outt, lse, gout
     if not args.no_decode:

@@ -33,6 +33,7 @@ def say(*a):
 
 
 def run(fem, q, k, v, b, g):
+    """Forward (training) and backward through the C ABI; returns numpy."""
     dev = torch.device("cuda:0")
     qd, kd, vd, bd, gd = (x.to(dev) for x in (q, k, v, b, g))
     out, lse = fem.fem_softmax_fwd_train(qd, kd, vd, bd)
@@ -116,3 +117,20 @@ def test_backward_deterministic(fem):
     c = run(fem, q, k, v, b, g)[2]
     for x, y in zip(a, c):
         assert np.array_equal(x, y)
+
+
+def test_backward_exact_fallback(fem):
+    """Values spread over [-5, 5] with beta = 16 put a row's F far below its
+    key tile's largest beta v, so blocks fall back to the element-wise pass."""
+    say("backward fallback case: B1 H2 T300 d64, v in {-5, +5, N(0,1)}, beta 16, seed 13500")
+    q, k, _, _, g = draw(13500, 1, 2, 300, 64)
+    rng = np.random.default_rng(13501)
+    v = rng.standard_normal((1, 2, 300, 64))
+    v[:, :, ::7] = 5.0
+    v[:, :, 3::11] = -5.0
+    v = torch.from_numpy(v.astype(np.float32)).to(torch.bfloat16)
+    b = torch.full((2, 64), 16.0)
+    _, _, grads = run(fem, q, k, v, b, g)
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, "fallback")
