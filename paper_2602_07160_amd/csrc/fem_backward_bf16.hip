@@ -421,32 +421,50 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
 // 2^{bl_j v_ij - c_j}, U_tj = 2^{c_j - bl_j F^_tj} (bl = beta log2 e), so
 //   dS_ti = p_ti sum_j W_tj (R_tij - 1),   R = E U,   W = G / beta,
 //   dV_ij = E_ij sum_t p_ti G_tj U_tj
-// are products over j and over t.  Two forms per channel:
-//   split (bl_j times the range of v_.j over the sequence <= 4): c_j = bl_j max
-//     v_.j of the (b, h), R - 1 = A U + (U - 1) with A = E - 1 (expm1): the
-//     product sum_j (W U) A and the row constant sum_j W (U - 1) carry no
-//     cancellation when beta is small (|A|, |U - 1| are small, U in
-//     [2^-4, 2^4]);
-//   plain (otherwise): c_j = the key tile's max of bl v, R - 1 = E U - 1, row
-//     constant -sum_j W.
+// are products over j and over t.  c_j = bl_j max v_.j over the (b, h)'s
+// whole sequence, so E depends on the key alone and U on the query alone:
+// both are formed once, in the layouts the matrix cores read, and the passes
+// over tile pairs only stream them.  Two forms per channel:
+//   split (bl_j times the range of v_.j <= 4): R - 1 = A U + (U - 1) with
+//     A = E - 1 (expm1): the product sum_j (W U) A and the row constant
+//     sum_j W (U - 1) carry no cancellation when beta is small (|A|, |U - 1|
+//     are small, U in [1, 2^4]);
+//   plain (otherwise): R - 1 = E U - 1, row constant -sum_j W.
 // Both factors enter as bf16 hi + lo parts (three MFMAs, ~2^-16 relative).
+// Since out lies between the smallest and the largest v it averages,
+// E >= 2^-L and U <= 2^L with L = bl (max v - min v); with L <= 110 every
+// factor, product and sum stays inside fp32's normal range (the dV sums
+// sum_t p G U are at most T max|G| 2^L).  A channel with a wider range, or a
+// row whose W U would leave that range, sets a device flag; the element-wise
+// kernels then redo the whole pass, and otherwise return at once.
 // p comes from an fp32 log-normaliser recomputed here (the forward's lse sums
 // bf16-rounded probabilities), so the rows of p sum to one to fp32 accuracy.
-// A block whose U would exceed 2^100 (a row's F far below the key tile's
-// largest beta v) sets a device flag; the exact kernels then redo the whole
-// pass, and otherwise return at once.  Below that bound every product stays
-// inside fp32's range (W U <= 2^100 |G| / beta), and an E that flushes to
-// zero (< 2^-126) drops a posterior ratio R = E U < 2^-26.
 //
 // Normalisation: R^ built from the forward's F^ gives sum_i p R^ = Z/P =
 // e^{beta (F - F^)} != 1 (the forward rounds p to bf16).  The q kernel, which
-// sees every key of its rows, forms ln(Z/P) per (t, j) exactly -- from the
-// split form (D = (U - 1) P + U sum_i p A) for split channels, from a running
-// per-channel log-sum of the tiles' sum_i p E for plain ones -- and writes
-// it; the kv kernel then uses the normalised posterior R^ / (Z/P).  So
+// sees every key of its rows, forms ln(Z/P) per (t, j) from SA = sum_i p Y
+// (Y = A or E): split, Z/P - 1 = (U - 1) + U SA / P; plain, Z/P = U SA / P.
+// The kv pass then uses the normalised posterior, U' = U / (Z/P).  So
 // dbeta = sum_t G (E_q[v] - F) / beta = (sum_i v dV - sum_t G F) / beta with
 // F = F^ + ln(Z/P)/beta is formed from normalised quantities; its terms are
 // small next to their parts (~ beta Var/2 at small beta, ~ KL/beta at large).
+//
+// Kernels, in stream order:
+//   lse:   fp32 lse per query; per 64-row tile, each channel's max and min v;
+//   prepk: c_j and the channel form; Y row-major (hi and lo);
+//   q:     per 64-query tile over its key tiles: S^T, p, dP^T = Y (W U)^T,
+//          dS, dQ^T += K^T dS^T and SA^T += Y^T P^T; ln(Z/P) and the G F^
+//          terms of dbeta;
+//   prepq: W U' row-major (hi and lo) and the row constants;
+//   kv:    per 64-key tile over its query tiles: S, p, dP = (W U') Y^T, dS,
+//          dV^T += (W U')^T P (dV = beta E times it) and dK^T += Q^T dS; the
+//          v dV terms of dbeta;
+//   dbeta: per (h, j), the partial sums in double precision.
+// The streamed side of a pass (K, Y in the q pass; Q, W U' in the kv pass)
+// goes global -> LDS by direct loads into a double buffer, one tile pair
+// ahead, so the loads cost no registers and no waiting; the transposed
+// operands (K^T, Y^T; Q^T, (W U')^T) are read from the same row-major tiles
+// by transposing LDS reads (ds_read_b64_tr_b16).
 
 __host__ __device__ constexpr int epos32(int r) {
   return (r & 16) + (((r >> 2) & 1) << 3) + (((r >> 3) & 1) << 2) + (r & 3);
@@ -464,14 +482,106 @@ __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+constexpr float kRange = 110.f;  // largest bl (max v - min v) of a channel
+constexpr float kSplit = 4.f;    // largest bl (max v - min v) of a split channel
+constexpr float kGuardU = 120.f; // largest log2 U of a row
+constexpr float kGuardW = 0x1p124f;
+
+// Consecutive workgroups go to the eight XCDs in turn; this order hands each
+// XCD a contiguous range of tiles (one (b, h) at a time), so the key or query
+// tiles its workgroups stream stay in its own L2.
+__device__ __forceinline__ int xcd_order(int b, int nblk) {
+  if (nblk & 7) return b;
+  return (b & 7) * (nblk >> 3) + (b >> 3);
+}
+
+
+// ---- swizzled tiles ----------------------------------------------------------
+//
+// A streamed [64][D] bf16 tile sits in LDS unpadded, 16-byte chunk c of row r
+// at chunk position c ^ swz(r).  swz makes both read patterns bank-conflict
+// free: a row-major MFMA fragment (16 lanes, 16 consecutive rows, one chunk
+// each) and a transposing read (4 consecutive rows, 32 consecutive columns).
+template <int D>
+__host__ __device__ constexpr int swz(int r) {
+  return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3))
+       : D == 64  ? ((((r >> 1) & 1) << 2) | ((r >> 2) & 3))
+                  : ((r >> 2) & 3);
+}
+
+template <int D>
+__device__ __forceinline__ int swz_off(int row, int chunk) {  // byte offset
+  return row * D * 2 + ((chunk ^ swz<D>(row)) << 4);
+}
+
+// Direct global -> LDS copy of rows [0, 64) of a row-major [., D] bf16 source
+// into a swizzled tile; rows past lim re-read row lim (their keys or queries
+// are masked).  Wave w fills the 1 KiB blocks w, w + 4, ...: lane l of block
+// b fills slot 64 b + l, i.e. row (64 b + l) / (D / 8), chunk position
+// (64 b + l) % (D / 8), from the chunk that position holds.
+template <int D>
+__device__ __forceinline__ void load_swz(const bf16* __restrict__ src, bf16* dst, int lim) {
+  constexpr int CPR = D / 8;
+  static_assert(CPR % 4 == 0, "whole blocks per wave");
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const char* s8 = reinterpret_cast<const char*>(src);
+#pragma unroll
+  for (int u = 0; u < CPR / 4; ++u) {
+    const int blk = wave + 4 * u;
+    const int s = blk * 64 + lane, row = s / CPR, pos = s % CPR;
+    const unsigned off = (unsigned)(min(row, lim) * D * 2 + ((pos ^ swz<D>(row)) << 4));
+    __builtin_amdgcn_global_load_lds(s8 + off, dst + blk * 512, 16, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Row-major MFMA fragment of a swizzled tile: 8 bf16 of row `row`, chunk `chunk`.
+template <int D>
+__device__ __forceinline__ bf16x8 frag_rows(const bf16* t, int row, int chunk) {
+  return *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(t) + swz_off<D>(row, chunk));
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Transposed MFMA A fragment of a swizzled tile: A[m][k] = tile[row(p0 + k)][col0 + m]
+// for m < 32, k < 16, with the contraction positions p0 + k in permuted
+// order (row(p) = ppos(p)).  Two transposing reads: in each 16-lane group,
+// lanes 4r..4r+3 read 4 columns each of row r, and lane c gets column c of
+// the 4 rows.  Group g = lane / 16 takes columns col0 + 16 (g & 1) .. and
+// positions p0 + 8 (g >> 1) ..: the A layout of v_mfma_f32_32x32x16_bf16.
+template <int D>
+__device__ __forceinline__ bf16x8 frag_tr(const bf16* t, int col0, int p0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const int r = i >> 2, q = i & 3;
+  const int col = col0 + 16 * (g & 1) + 4 * q;
+  const int p = p0 + 8 * (g >> 1);
+  const char* b = reinterpret_cast<const char*>(t);
+  const int r0 = ppos(p) + r, r1 = ppos(p + 4) + r;
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)(b + swz_off<D>(r0, col >> 3) + (col & 7) * 2));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)(b + swz_off<D>(r1, col >> 3) + (col & 7) * 2));
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 x = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, x);
+}
+
 // The prior's log-normaliser in fp32 from unrounded probabilities:
 // lse_t = ln sum_{i<=t} exp(q_t.k_i / sqrt d).  One workgroup per (b, h,
 // 64-query tile); wave (kh, qh) takes the S^T block of keys kh*32.. and
-// queries qh*32..; lane (query n, half hl) keeps a running (max, sum).
+// queries qh*32..; lane (query n, half hl) keeps a running (max, sum).  The
+// workgroup also writes the max and min of each channel of V over its 64
+// rows, and the first one clears the fallback flag.
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_lse_kernel(const bf16* __restrict__ Q,
                                                            const bf16* __restrict__ K,
-                                                           float* __restrict__ lse, int T,
+                                                           const bf16* __restrict__ V,
+                                                           float* __restrict__ lse,
+                                                           float* __restrict__ vmx,
+                                                           float* __restrict__ vmn,
+                                                           int* __restrict__ flag, int T,
                                                            int ntile) {
   using C = Bw<D>;
   __shared__ __align__(16) bf16 qt[kTile * C::ROW];
@@ -483,6 +593,31 @@ __global__ __launch_bounds__(kThreads) void bwd_lse_kernel(const bf16* __restric
   const size_t base = (size_t)bh * T * D;
   const int kh = wave >> 1, qh = wave & 1;
   const int t = qh * 32 + n;
+  if (blockIdx.x == 0 && tid == 0) flag[0] = 0;
+  {
+    constexpr int RG = kThreads / D;
+    const int j = tid % D, rg = tid / D;
+    float a = -INFINITY, b = INFINITY;
+    for (int r = rg; r < kTile; r += RG)
+      if (q0 + r < T) {
+        const float v = (float)V[base + (size_t)(q0 + r) * D + j];
+        a = fmaxf(a, v);
+        b = fminf(b, v);
+      }
+    float* sx = &rm[0][0];
+    float* sn = &rs[0][0];
+    sx[tid] = a;
+    sn[tid] = b;
+    __syncthreads();
+    if (rg == 0) {
+      for (int g = 1; g < RG; ++g) {
+        a = fmaxf(a, sx[g * D + j]);
+        b = fminf(b, sn[g * D + j]);
+      }
+      vmx[((size_t)bh * ntile + qb) * D + j] = a;
+      vmn[((size_t)bh * ntile + qb) * D + j] = b;
+    }
+  }
   stage_tile<D>(Q + base, q0, T, qt, nullptr);
   const float scale2 = kLog2e / sqrtf((float)D);
   float m = -INFINITY, sum = 0.f;
@@ -509,6 +644,7 @@ __global__ __launch_bounds__(kThreads) void bwd_lse_kernel(const bf16* __restric
       m = mn;
     }
   }
+  __syncthreads();
   rm[wave][lane] = m;
   rs[wave][lane] = sum;
   __syncthreads();
@@ -528,254 +664,71 @@ __global__ __launch_bounds__(kThreads) void bwd_lse_kernel(const bf16* __restric
   }
 }
 
-// Per (b, h, j): whether channel j takes the split form, and its sequence-wide
-// shift c_j = bl_j max v.  Also clears the fallback flag.
+// Channel constants of a (b, h) from the per-tile max / min of V: c_j, the
+// form, and bl_j, into LDS; with publish, also to global memory, and a
+// channel whose range is beyond the matrix-core form raises the flag.
 template <int D>
-__global__ __launch_bounds__(kThreads) void bwd_prep_kernel(const bf16* __restrict__ V,
-                                                            const float* __restrict__ beta,
-                                                            float* __restrict__ cg,
-                                                            float* __restrict__ splitf,
-                                                            int* __restrict__ flag, int H,
-                                                            int T) {
-  constexpr int RG = kThreads / D;
-  __shared__ float mx[kThreads], mn[kThreads];
-  const int bh = blockIdx.x, h = bh % H, tid = threadIdx.x, j = tid % D, rg = tid / D;
-  if (bh == 0 && tid == 0) flag[0] = 0;
-  const bf16* Vh = V + (size_t)bh * T * D;
-  float a = -INFINITY, b = INFINITY;
-  for (int t = rg; t < T; t += RG) {
-    const float v = (float)Vh[(size_t)t * D + j];
-    a = fmaxf(a, v);
-    b = fminf(b, v);
-  }
-  mx[tid] = a;
-  mn[tid] = b;
-  __syncthreads();
-  if (rg == 0) {
-    for (int g = 1; g < RG; ++g) {
-      a = fmaxf(a, mx[g * D + j]);
-      b = fminf(b, mn[g * D + j]);
+__device__ __forceinline__ void channel_consts(const float* __restrict__ beta,
+                                               const float* __restrict__ vmx,
+                                               const float* __restrict__ vmn, int bh, int h,
+                                               int ntile, float* c, float* split, float* bl,
+                                               bool publish, float* __restrict__ cg,
+                                               float* __restrict__ splitf, int* __restrict__ flag) {
+  for (int j = threadIdx.x; j < D; j += kThreads) {
+    float a = -INFINITY, b = INFINITY;
+    for (int k = 0; k < ntile; ++k) {
+      a = fmaxf(a, vmx[((size_t)bh * ntile + k) * D + j]);
+      b = fminf(b, vmn[((size_t)bh * ntile + k) * D + j]);
     }
-    const float bl = beta[h * D + j] * kLog2e;
-    cg[bh * D + j] = bl * a;
-    splitf[bh * D + j] = bl * (a - b) <= 4.f ? 1.f : 0.f;
+    const float l = beta[h * D + j] * kLog2e, range = l * (a - b);
+    const float sp = range <= kSplit ? 1.f : 0.f;
+    c[j] = l * a;
+    split[j] = sp;
+    bl[j] = l;
+    if (publish) {
+      cg[bh * D + j] = l * a;
+      splitf[bh * D + j] = sp;
+      if (!(range <= kRange)) flag[0] = 1;
+    }
   }
 }
 
-constexpr float kGuard = 100.f;  // largest log2 U of the plain form
-
-// kv kernel, matrix-core form.  Wave (qh = w >> 1, kh = w & 1) owns the
-// 32 x 32 block (queries qh*32.., keys kh*32..) of each tile pair.
+// Y of each key: A = E - 1 (split) or E (plain), E = 2^{bl v - c}, row-major
+// hi and lo parts, zero past T.  One thread per 8 channels of a row.
 template <int D>
-struct KvFast {
-  using C = Bw<D>;
-  bf16 kt[kTile * C::ROW];                  // K [key][d]
-  bf16 qt[kTile * C::ROW];                  // Q [query][d]
-  bf16 qTp[D * C::TROW];                    // Q^T [d][query, permuted]
-  bf16 yh[kTile * C::ROW], yl[kTile * C::ROW];    // Y [key][j]
-  bf16 wuh[kTile * C::ROW], wul[kTile * C::ROW];  // W U [query][j]
-  bf16 guh[D * C::TROW], gul[D * C::TROW];        // (G U)^T [j][query, permuted]
-  float cst[kTile], lse2[kTile], c[D], split[D], bl[D];
-};
-
-template <int D>
-__global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ lse,
-    const float* __restrict__ G, const float* __restrict__ cg, const float* __restrict__ splitf,
-    const float* __restrict__ lnz, float* __restrict__ dK, float* __restrict__ dV,
-    float* __restrict__ vdv,
-    int* __restrict__ flag, int H, int T, int ntile) {
-  using C = Bw<D>;
-  constexpr int NB = C::NCB;  // 32-row blocks of d (and of j)
-  __shared__ __align__(16) KvFast<D> sm;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
+__global__ __launch_bounds__(kThreads) void bwd_prepk_kernel(
+    const bf16* __restrict__ V, const float* __restrict__ beta, const float* __restrict__ vmx,
+    const float* __restrict__ vmn, float* __restrict__ cg, float* __restrict__ splitf,
+    bf16* __restrict__ yh, bf16* __restrict__ yl, int* __restrict__ flag, int H, int T,
+    int ntile) {
+  __shared__ float c[D], split[D], bl[D];
   const int kb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
   const int k0 = kb * kTile;
+  channel_consts<D>(beta, vmx, vmn, bh, h, ntile, c, split, bl, kb == 0, cg, splitf, flag);
+  __syncthreads();
   const size_t base = (size_t)bh * T * D;
-  const int qh = wave >> 1, kh = wave & 1;
-
-  // ---- the key tile: shifts c_j and Y = A (split) or E (plain)
-  float* scratch = reinterpret_cast<float*>(sm.guh);  // [64][D] fp32 bl v (fits in guh + gul)
-  for (int j = tid; j < D; j += kThreads) {
-    sm.bl[j] = beta[h * D + j] * kLog2e;
-    sm.split[j] = splitf[bh * D + j];
-  }
-  stage_tile<D>(K + base, k0, T, sm.kt, nullptr);
-  __syncthreads();
-  for (int e = tid; e < kTile * D; e += kThreads) {
-    const int i = e / D, j = e % D;
-    scratch[e] = k0 + i < T ? sm.bl[j] * (float)V[base + (size_t)(k0 + i) * D + j] : -INFINITY;
-  }
-  __syncthreads();
-  for (int j = tid; j < D; j += kThreads) {
-    float mxv = -INFINITY;
-    for (int i = 0; i < kTile; ++i) mxv = fmaxf(mxv, scratch[i * D + j]);
-    sm.c[j] = sm.split[j] != 0.f ? cg[bh * D + j] : mxv;
-  }
-  __syncthreads();
-  for (int e = tid; e < kTile * D; e += kThreads) {
-    const int i = e / D, j = e % D;
-    const float x = scratch[e] - sm.c[j];
-    float y = 0.f;
-    if (k0 + i < T) y = sm.split[j] != 0.f ? expm1f(x * kLn2) : exp2_hw(x);
-    split_bf16(y, sm.yh[i * C::ROW + j], sm.yl[i * C::ROW + j]);
-  }
-
-  f32x16 dvt[NB], dkt[NB];  // (j or d block) x keys kh*32.., partial over this wave's queries
+  const size_t rows = ((size_t)bh * ntile + kb) * kTile;  // first row in the padded [., D] arrays
+  constexpr int CPR = D / 8;
+  for (int e = threadIdx.x; e < kTile * CPR; e += kThreads) {
+    const int i = e / CPR, c8 = (e % CPR) * 8;
+    const bool live = k0 + i < T;
+    bf16x8 vx = {}, hi, lo;
+    if (live) vx = *reinterpret_cast<const bf16x8*>(V + base + (size_t)(k0 + i) * D + c8);
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    dvt[b] = f32x16{};
-    dkt[b] = f32x16{};
-  }
-  const float scale2 = kLog2e / sqrtf((float)D);
-  const int qlast = (T - 1) / kTile;
-  bool bad = false;
-  for (int qb = kb; qb <= qlast; ++qb) {
-    const int q0 = qb * kTile;
-    __syncthreads();
-    // Q tile, row-major and transposed in permuted query order
-    {
-      constexpr int CPR = D / 8;
-      for (int e = tid; e < kTile * CPR; e += kThreads) {
-        const int r = e / CPR, c8 = (e % CPR) * 8;
-        bf16x8 x = {};
-        if (q0 + r < T) x = *reinterpret_cast<const bf16x8*>(Q + base + (size_t)(q0 + r) * D + c8);
-        *reinterpret_cast<bf16x8*>(sm.qt + r * C::ROW + c8) = x;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) sm.qTp[(c8 + u) * C::TROW + ppos(r)] = x[u];
+    for (int u = 0; u < 8; ++u) {
+      const int j = c8 + u;
+      float y = 0.f;
+      if (live) {
+        const float x = fmaf(bl[j], (float)vx[u], -c[j]);
+        y = split[j] != 0.f ? expm1f(x * kLn2) : exp2_hw(x);
       }
-    }
-    // W U', (G U')^T and the row constants, U' = U / (Z/P) normalising the
-    // posterior; thread (row tid >> 2, quarter tid & 3)
-    {
-      const int t = tid >> 2, j0 = (tid & 3) * (D / 4);
-      const bool live = q0 + t < T;
-      float cs = 0.f;
-      for (int u = 0; u < D / 4; ++u) {
-        const int j = j0 + u;
-        float w = 0.f, g = 0.f, x = 0.f, lz = 0.f;
-        if (live) {
-          const size_t at = base + (size_t)(q0 + t) * D + j;
-          g = G[at];
-          x = sm.c[j] - sm.bl[j] * F[at];
-          lz = lnz[at] * kLog2e;
-          w = g / beta[h * D + j];
-          if (x > kGuard) bad = true;
-        }
-        const float xu = fminf(x, kGuard) - lz;  // log2 U'
-        const float U = exp2_hw(xu);
-        cs += sm.split[j] != 0.f ? w * expm1f(xu * kLn2) : -w;
-        split_bf16(w * U, sm.wuh[t * C::ROW + j], sm.wul[t * C::ROW + j]);
-        split_bf16(g * U, sm.guh[j * C::TROW + ppos(t)], sm.gul[j * C::TROW + ppos(t)]);
-      }
-      cs += __shfl_xor(cs, 1);
-      cs += __shfl_xor(cs, 2);
-      if ((tid & 3) == 0) sm.cst[t] = cs;
-      if (tid < kTile) sm.lse2[tid] = q0 + tid < T ? lse[(size_t)bh * T + q0 + tid] * kLog2e : 0.f;
-    }
-    __syncthreads();
-
-    // S (queries x keys), p in fp32
-    const f32x16 s = score_block<D>(sm.qt, sm.kt, qh, kh);
-    const int i = kh * 32 + n;
-    float p[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = k0 + i <= q0 + t && q0 + t < T && k0 + i < T;
-      p[r] = ok ? exp2_hw(fmaf(s[r], scale2, -sm.lse2[t])) : 0.f;
-    }
-    // dP = (W U) Y^T over j
-    f32x16 dp = {};
-#pragma unroll
-    for (int ks = 0; ks < C::NKS; ++ks) {
-      const int ao = (qh * 32 + n) * C::ROW + ks * 16 + hl * 8, bo = (kh * 32 + n) * C::ROW + ks * 16 + hl * 8;
-      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.wuh + ao);
-      const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.wul + ao);
-      const bf16x8 bh8 = *reinterpret_cast<const bf16x8*>(sm.yh + bo);
-      const bf16x8 bl8 = *reinterpret_cast<const bf16x8*>(sm.yl + bo);
-      dp = mfma(ah, bh8, dp);
-      dp = mfma(al, bh8, dp);
-      dp = mfma(ah, bl8, dp);
-    }
-    // dS = p (dP + const); p and dS as B operands (k = this wave's queries, accumulator order)
-    bf16x8 ph[2], pl[2], dsb[2];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const float ds = p[r] * (dp[r] + sm.cst[t]);
       bf16 a, b;
-      split_bf16(p[r], a, b);
-      ph[r >> 3][r & 7] = a;
-      pl[r >> 3][r & 7] = b;
-      dsb[r >> 3][r & 7] = (bf16)ds;
+      split_bf16(y, a, b);
+      hi[u] = a;
+      lo[u] = b;
     }
-    // dV^T(j block, keys) += (G U)^T P ;  dK^T(d block, keys) += Q^T dS
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const int ao = (b * 32 + n) * C::TROW + qh * 32 + k2 * 16 + hl * 8;
-        const bf16x8 gh = *reinterpret_cast<const bf16x8*>(sm.guh + ao);
-        const bf16x8 gl = *reinterpret_cast<const bf16x8*>(sm.gul + ao);
-        dvt[b] = mfma(gh, ph[k2], dvt[b]);
-        dvt[b] = mfma(gl, ph[k2], dvt[b]);
-        dvt[b] = mfma(gh, pl[k2], dvt[b]);
-        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(sm.qTp + ao);
-        dkt[b] = mfma(qa, dsb[k2], dkt[b]);
-      }
-    }
-  }
-  if (bad) flag[0] = 1;
-
-  // ---- combine the two query halves (waves qh = 0, 1 of the same kh)
-  __syncthreads();
-  // [2 kh][2 sets][NB][16][64] fp32 (64 KiB at d = 128) over kt, qt, qTp, yh;
-  // the v dV products go to wuh onwards
-  float* red = reinterpret_cast<float*>(sm.kt);
-  static_assert(4 * C::NCB * 16 * 64 * 4 <= offsetof(KvFast<D>, wuh), "reduction area");
-  static_assert(offsetof(KvFast<D>, wuh) + kTile * D * 4 <= offsetof(KvFast<D>, cst), "v dV area");
-  auto slot = [&](int set, int b, int r) { return (((kh * 2 + set) * NB + b) * 16 + r) * 64 + lane; };
-  if (qh == 1) {
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        red[slot(0, b, r)] = dvt[b][r];
-        red[slot(1, b, r)] = dkt[b][r];
-      }
-  }
-  __syncthreads();
-  float* vdvs = reinterpret_cast<float*>(sm.wuh);  // [64 keys][D] v dV products
-  if (qh == 0) {
-    const float rs = 1.f / sqrtf((float)D);
-    const int key = k0 + kh * 32 + n;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);  // j or d
-        const float sv = dvt[b][r] + red[slot(0, b, r)];
-        const float sk = dkt[b][r] + red[slot(1, b, r)];
-        float dvv = 0.f;
-        if (key < T) {
-          const float vv = (float)V[base + (size_t)key * D + row];
-          const float E = exp2_hw(fmaf(sm.bl[row], vv, -sm.c[row]));
-          dvv = E * sv;
-          dV[base + (size_t)key * D + row] = dvv;
-          dK[base + (size_t)key * D + row] = sk * rs;
-          dvv *= vv;
-        }
-        vdvs[(kh * 32 + n) * D + row] = dvv;
-      }
-    }
-  }
-  __syncthreads();
-  for (int j = tid; j < D; j += kThreads) {
-    float acc = 0.f;
-    for (int i = 0; i < kTile; ++i) acc += vdvs[i * D + j];
-    vdv[((size_t)bh * ntile + kb) * D + j] = acc;
+    *reinterpret_cast<bf16x8*>(yh + (rows + i) * D + c8) = hi;
+    *reinterpret_cast<bf16x8*>(yl + (rows + i) * D + c8) = lo;
   }
 }
 
@@ -784,54 +737,68 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
 template <int D>
 struct QFast {
   using C = Bw<D>;
+  bf16 key[2][3][kTile * D];                      // [buffer][K, Y hi, Y lo], swizzled [key][d or j]
   bf16 qt[kTile * C::ROW];                        // Q [query][d]
-  bf16 kt[kTile * C::ROW];                        // K [key][d]
-  bf16 kTp[D * C::TROW];                          // K^T [d][key, permuted]
-  bf16 yh[kTile * C::ROW], yl[kTile * C::ROW];    // Y [key][j]
   bf16 wuh[kTile * C::ROW], wul[kTile * C::ROW];  // W U [query][j]
-  bf16 yTh[D * C::TROW], yTl[D * C::TROW];        // Y^T [j][key, permuted]
   float cst[kTile], lse2[kTile], c[D], split[D], bl[D], pt[2][kTile];
-  float cref[D], resc[D];  // running reference shift of the plain channels' sums, rescale
 };
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ lse,
-    const float* __restrict__ G, const float* __restrict__ cg, const float* __restrict__ splitf,
-    float* __restrict__ dQ, float* __restrict__ gf, float* __restrict__ lnz,
-    int* __restrict__ flag, int H, int T, int ntile) {
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const float* __restrict__ beta,
+    const float* __restrict__ F, const float* __restrict__ lse, const float* __restrict__ G,
+    const float* __restrict__ cg, const float* __restrict__ splitf, const bf16* __restrict__ yh,
+    const bf16* __restrict__ yl, float* __restrict__ dQ, float* __restrict__ gf,
+    float* __restrict__ lnz, int* __restrict__ flag, int H, int T, int ntile) {
   using C = Bw<D>;
   constexpr int NB = C::NCB;
   __shared__ __align__(16) QFast<D> sm;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
-  const int qb = ntile - 1 - blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
+  const int lb = xcd_order(blockIdx.x, gridDim.x);
+  const int qb = ntile - 1 - lb % ntile, bh = lb / ntile, h = bh % H;
   const int q0 = qb * kTile;
   const size_t base = (size_t)bh * T * D;
+  const size_t rows0 = (size_t)bh * ntile * kTile;
   const int kh = wave >> 1, qh = wave & 1;
+  auto fetch = [&](int kb) {
+    const int k0 = kb * kTile;
+    bf16* dst = &sm.key[kb & 1][0][0];
+    load_swz<D>(K + base + (size_t)k0 * D, dst, T - 1 - k0);
+    load_swz<D>(yh + (rows0 + k0) * D, dst + kTile * D, kTile - 1);
+    load_swz<D>(yl + (rows0 + k0) * D, dst + 2 * kTile * D, kTile - 1);
+  };
+  fetch(0);
 
   for (int j = tid; j < D; j += kThreads) {
     sm.bl[j] = beta[h * D + j] * kLog2e;
     sm.split[j] = splitf[bh * D + j];
-    sm.cref[j] = sm.split[j] != 0.f ? cg[bh * D + j] : -INFINITY;
+    sm.c[j] = cg[bh * D + j];
   }
   if (tid < kTile) sm.lse2[tid] = q0 + tid < T ? lse[(size_t)bh * T + q0 + tid] * kLog2e : 0.f;
   stage_tile<D>(Q + base, q0, T, sm.qt, nullptr);
   __syncthreads();
-  // row constants: sum_j (split ? W (U - 1) : -W), with U from the sequence-wide shift
+  // W U and the row constants sum_j (split ? W (U - 1) : -W); thread (row
+  // tid >> 2, channel quarter tid & 3)
+  bool bad = false;
   {
     const int t = tid >> 2, j0 = (tid & 3) * (D / 4);
+    const bool live = q0 + t < T;
     float cs = 0.f;
-    if (q0 + t < T) {
-      for (int u = 0; u < D / 4; ++u) {
-        const int j = j0 + u;
-        const float w = G[base + (size_t)(q0 + t) * D + j] / beta[h * D + j];
-        if (sm.split[j] != 0.f) {
-          const float x = cg[bh * D + j] - sm.bl[j] * F[base + (size_t)(q0 + t) * D + j];
-          cs += w * expm1f(x * kLn2);
-        } else {
-          cs -= w;
-        }
+    for (int u = 0; u < D / 4; u += 4) {
+      f32x4 g4 = {}, f4 = {};
+      if (live) {
+        g4 = *reinterpret_cast<const f32x4*>(G + base + (size_t)(q0 + t) * D + j0 + u);
+        f4 = *reinterpret_cast<const f32x4*>(F + base + (size_t)(q0 + t) * D + j0 + u);
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int j = j0 + u + v;
+        const float w = g4[v] / beta[h * D + j];
+        const float x = live ? sm.c[j] - sm.bl[j] * f4[v] : 0.f;
+        const float wu = w * exp2_hw(fminf(x, kGuardU));
+        if (!(x <= kGuardU && fabsf(wu) < kGuardW)) bad = true;
+        cs += sm.split[j] != 0.f ? w * expm1f(x * kLn2) : -w;
+        split_bf16(wu, sm.wuh[t * C::ROW + j], sm.wul[t * C::ROW + j]);
       }
     }
     cs += __shfl_xor(cs, 1);
@@ -847,101 +814,41 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
   }
   float psum = 0.f;
   const float scale2 = kLog2e / sqrtf((float)D);
-  bool bad = false;
-  float* scratch = reinterpret_cast<float*>(sm.yTh);  // [64][D] fp32 bl v (fits in yTh + yTl)
+  const int t = qh * 32 + n;
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * kTile;
-    __syncthreads();
-    {
-      constexpr int CPR = D / 8;
-      for (int e = tid; e < kTile * CPR; e += kThreads) {
-        const int r = e / CPR, c8 = (e % CPR) * 8;
-        bf16x8 x = {};
-        if (k0 + r < T) x = *reinterpret_cast<const bf16x8*>(K + base + (size_t)(k0 + r) * D + c8);
-        *reinterpret_cast<bf16x8*>(sm.kt + r * C::ROW + c8) = x;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) sm.kTp[(c8 + u) * C::TROW + ppos(r)] = x[u];
-      }
-    }
-    for (int e = tid; e < kTile * D; e += kThreads) {
-      const int i = e / D, j = e % D;
-      scratch[e] = k0 + i < T ? sm.bl[j] * (float)V[base + (size_t)(k0 + i) * D + j] : -INFINITY;
-    }
-    __syncthreads();
-    for (int j = tid; j < D; j += kThreads) {
-      float mxv = -INFINITY;
-      for (int i = 0; i < kTile; ++i) mxv = fmaxf(mxv, scratch[i * D + j]);
-      const bool sp = sm.split[j] != 0.f;
-      sm.c[j] = sp ? cg[bh * D + j] : mxv;
-      // plain channels: the running reference of their sums rises with the tiles
-      const float cold = sm.cref[j], cnew = sp ? cold : fmaxf(cold, mxv);
-      sm.resc[j] = cnew == cold ? 1.f : exp2_hw(cold - cnew);
-      sm.cref[j] = cnew;
-    }
-    __syncthreads();
-    // the plain channels' sums move to the new reference
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sat[b][r] *= sm.resc[b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3)];
-    // Y (row-major) into yh / yl for dP; for the sums (transposed copy, written
-    // once scratch is read) the plain channels take E 2^{c - cref} <= 1
-    float yv[kTile * D / kThreads];
-    for (int e = tid, u = 0; e < kTile * D; e += kThreads, ++u) {
-      const int i = e / D, j = e % D;
-      const float x = scratch[e] - sm.c[j];
-      float y = 0.f, ys = 0.f;
-      if (k0 + i < T) {
-        if (sm.split[j] != 0.f) {
-          y = ys = expm1f(x * kLn2);
-        } else {
-          y = exp2_hw(x);
-          ys = exp2_hw(scratch[e] - sm.cref[j]);
-        }
-      }
-      yv[u] = ys;
-      split_bf16(y, sm.yh[i * C::ROW + j], sm.yl[i * C::ROW + j]);
-    }
-    // W U for this key tile's shifts
-    {
-      const int t = tid >> 2, j0 = (tid & 3) * (D / 4);
-      const bool live = q0 + t < T;
-      for (int u = 0; u < D / 4; ++u) {
-        const int j = j0 + u;
-        float w = 0.f, x = 0.f;
-        if (live) {
-          w = G[base + (size_t)(q0 + t) * D + j] / beta[h * D + j];
-          x = sm.c[j] - sm.bl[j] * F[base + (size_t)(q0 + t) * D + j];
-          if (x > kGuard) bad = true;
-        }
-        split_bf16(w * exp2_hw(fminf(x, kGuard)), sm.wuh[t * C::ROW + j], sm.wul[t * C::ROW + j]);
-      }
-    }
-    __syncthreads();  // scratch fully read
-    for (int e = tid, u = 0; e < kTile * D; e += kThreads, ++u) {
-      const int i = e / D, j = e % D;
-      split_bf16(yv[u], sm.yTh[j * C::TROW + ppos(i)], sm.yTl[j * C::TROW + ppos(i)]);
-    }
-    __syncthreads();
+    wait_vmem();
+    __syncthreads();  // tile kb is in, and every wave is done with tile kb - 1
+    if (kb < qb) fetch(kb + 1);
+    const bf16* kt = &sm.key[kb & 1][0][0];
+    const bf16* ty = kt + kTile * D;   // Y hi
+    const bf16* tyl = ty + kTile * D;  // Y lo
 
     // S^T (keys x queries), p in fp32
-    const f32x16 s = score_block<D>(sm.kt, sm.qt, kh, qh);
-    const int t = qh * 32 + n;
+    f32x16 s = {};
+#pragma unroll
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      const bf16x8 a = frag_rows<D>(kt, kh * 32 + n, 2 * ks + hl);
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.qt + t * C::ROW + ks * 16 + hl * 8);
+      s = mfma(a, b, s);
+    }
+    const float l2 = sm.lse2[t];
+    const bool tlive = q0 + t < T;
     float p[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int i = kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = k0 + i <= q0 + t && q0 + t < T && k0 + i < T;
-      p[r] = ok ? exp2_hw(fmaf(s[r], scale2, -sm.lse2[t])) : 0.f;
+      const bool ok = k0 + i <= q0 + t && tlive && k0 + i < T;
+      p[r] = exp2_hw(ok ? fmaf(s[r], scale2, -l2) : -INFINITY);
       psum += p[r];
     }
     // dP^T = Y (W U)^T over j
     f32x16 dp = {};
 #pragma unroll
     for (int ks = 0; ks < C::NKS; ++ks) {
-      const int ao = (kh * 32 + n) * C::ROW + ks * 16 + hl * 8, bo = (qh * 32 + n) * C::ROW + ks * 16 + hl * 8;
-      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.yh + ao);
-      const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.yl + ao);
+      const int bo = t * C::ROW + ks * 16 + hl * 8;
+      const bf16x8 ah = frag_rows<D>(ty, kh * 32 + n, 2 * ks + hl);
+      const bf16x8 al = frag_rows<D>(tyl, kh * 32 + n, 2 * ks + hl);
       const bf16x8 bh8 = *reinterpret_cast<const bf16x8*>(sm.wuh + bo);
       const bf16x8 bl8 = *reinterpret_cast<const bf16x8*>(sm.wul + bo);
       dp = mfma(ah, bh8, dp);
@@ -963,11 +870,10 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
     for (int b = 0; b < NB; ++b) {
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
-        const int ao = (b * 32 + n) * C::TROW + kh * 32 + k2 * 16 + hl * 8;
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(sm.kTp + ao);
-        dqt[b] = mfma(ka, dsb[k2], dqt[b]);
-        const bf16x8 yh8 = *reinterpret_cast<const bf16x8*>(sm.yTh + ao);
-        const bf16x8 yl8 = *reinterpret_cast<const bf16x8*>(sm.yTl + ao);
+        const int p0 = kh * 32 + k2 * 16;
+        dqt[b] = mfma(frag_tr<D>(kt, b * 32, p0), dsb[k2], dqt[b]);
+        const bf16x8 yh8 = frag_tr<D>(ty, b * 32, p0);
+        const bf16x8 yl8 = frag_tr<D>(tyl, b * 32, p0);
         sat[b] = mfma(yh8, ph[k2], sat[b]);
         sat[b] = mfma(yl8, ph[k2], sat[b]);
         sat[b] = mfma(yh8, pl[k2], sat[b]);
@@ -978,10 +884,10 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
 
   // ---- combine the key halves (waves kh = 0, 1 of the same qh) and both lane halves of P
   __syncthreads();
-  // [2 qh][2 sets][NB][16][64] fp32 over qt, kt, kTp, yh; the G F terms go to wuh onwards
-  float* red = reinterpret_cast<float*>(sm.qt);
-  static_assert(4 * C::NCB * 16 * 64 * 4 <= offsetof(QFast<D>, wuh), "reduction area");
-  static_assert(offsetof(QFast<D>, wuh) + kTile * D * 4 <= offsetof(QFast<D>, cst), "G F area");
+  // [2 qh][2 sets][NB][16][64] fp32 and the [64 queries][D] G F terms, over the key buffers
+  float* red = reinterpret_cast<float*>(&sm.key[0][0][0]);
+  float* gfs = red + 4 * NB * 16 * 64;
+  static_assert((4 * C::NCB * 16 * 64 + kTile * D) * 4 <= sizeof(sm.key), "reduction area");
   auto slot = [&](int set, int b, int r) { return (((qh * 2 + set) * NB + b) * 16 + r) * 64 + lane; };
   psum += __shfl_xor(psum, 32);
   if (kh == 1) {
@@ -997,11 +903,11 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
     sm.pt[0][qh * 32 + n] = psum;
   }
   __syncthreads();
-  float* gfs = reinterpret_cast<float*>(sm.wuh);  // [64 queries][D] G F terms
   if (kh == 0) {
     const float rs = 1.f / sqrtf((float)D);
     const int tq = q0 + qh * 32 + n;
     const float P = sm.pt[0][qh * 32 + n] + sm.pt[1][qh * 32 + n];
+    bool under = false;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
 #pragma unroll
@@ -1013,15 +919,14 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
         if (tq < T) {
           dQ[base + (size_t)tq * D + row] = sq * rs;
           const float g = G[base + (size_t)tq * D + row], f = F[base + (size_t)tq * D + row];
-          float lz;  // ln(Z/P): F = F^ + ln(Z/P)/beta
+          const float x = sm.c[row] - sm.bl[row] * f;  // log2 U
+          float lz;                                     // ln(Z/P): F = F^ + ln(Z/P)/beta
           if (sm.split[row] != 0.f) {
-            // Z/P - 1 = (U - 1) + U SA / P, U = 2^{c - bl F^}
-            const float um1 = expm1f((cg[bh * D + row] - sm.bl[row] * f) * kLn2);
+            const float um1 = expm1f(x * kLn2);
             lz = log1pf(um1 + (um1 + 1.f) * sa / P);
           } else {
-            // Z = 2^{cref - bl F^} sum_tiles 2^{c_k - cref} sum_i p E_k
-            if (!(sa > 0x1p-100f * P)) flag[0] = 1;  // sums underflowed: exact pass
-            lz = (sm.cref[row] - sm.bl[row] * f) * kLn2 + logf(sa / P);
+            if (!(sa > 0x1p-120f * P)) under = true;
+            lz = x * kLn2 + logf(sa / P);
           }
           lnz[base + (size_t)tq * D + row] = lz;
           term = g * (f + lz / beta[h * D + row]);
@@ -1029,12 +934,274 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
         gfs[(qh * 32 + n) * D + row] = term;
       }
     }
+    if (under) flag[0] = 1;  // a plain channel's sum left fp32's range: exact pass
   }
   __syncthreads();
   for (int j = tid; j < D; j += kThreads) {
     float acc = 0.f;
     for (int i = 0; i < kTile; ++i) acc += gfs[i * D + j];
     gf[((size_t)bh * ntile + qb) * D + j] = acc;
+  }
+}
+
+// W U' row-major (hi and lo) for the kv pass, U' = U / (Z/P) normalising the
+// posterior, and the row constants sum_j (split ? W (U' - 1) : -W); zero past
+// T.  Thread e handles 8 channels of one row; the D/8 threads of a row are
+// adjacent lanes.
+template <int D>
+__global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
+    const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ G,
+    const float* __restrict__ lnz, const float* __restrict__ cg, const float* __restrict__ splitf,
+    bf16* __restrict__ wh, bf16* __restrict__ wl, float* __restrict__ cst,
+    int* __restrict__ flag, int H, int T, int ntile) {
+  __shared__ float c[D], split[D], bl[D];
+  constexpr int CPR = D / 8;
+  static_assert(kThreads % CPR == 0 && CPR <= 64, "a row's threads share a wave");
+  const int qb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
+  const int q0 = qb * kTile;
+  for (int j = threadIdx.x; j < D; j += kThreads) {
+    bl[j] = beta[h * D + j] * kLog2e;
+    split[j] = splitf[bh * D + j];
+    c[j] = cg[bh * D + j];
+  }
+  __syncthreads();
+  const size_t base = (size_t)bh * T * D;
+  const size_t rows = ((size_t)bh * ntile + qb) * kTile;
+  bool bad = false;
+  for (int e = threadIdx.x; e < kTile * CPR; e += kThreads) {
+    const int t = e / CPR, c8 = (e % CPR) * 8;
+    const bool live = q0 + t < T;
+    const size_t at = base + (size_t)(q0 + t) * D + c8;
+    bf16x8 hi, lo;
+    f32x4 g4[2] = {}, f4[2] = {}, z4[2] = {};
+    if (live) {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        g4[k] = *reinterpret_cast<const f32x4*>(G + at + 4 * k);
+        f4[k] = *reinterpret_cast<const f32x4*>(F + at + 4 * k);
+        z4[k] = *reinterpret_cast<const f32x4*>(lnz + at + 4 * k);
+      }
+    }
+    float cs = 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = c8 + u;
+      const float w = g4[u >> 2][u & 3] / beta[h * D + j];
+      const float x = live ? c[j] - bl[j] * f4[u >> 2][u & 3] : 0.f;
+      const float xu = fminf(x, kGuardU) - z4[u >> 2][u & 3] * kLog2e;  // log2 U'
+      const float wu = w * exp2_hw(xu);
+      if (!(x <= kGuardU && fabsf(wu) < kGuardW)) bad = true;
+      cs += split[j] != 0.f ? w * expm1f(xu * kLn2) : -w;
+      bf16 a, b;
+      split_bf16(wu, a, b);
+      hi[u] = a;
+      lo[u] = b;
+    }
+    *reinterpret_cast<bf16x8*>(wh + (rows + t) * D + c8) = hi;
+    *reinterpret_cast<bf16x8*>(wl + (rows + t) * D + c8) = lo;
+#pragma unroll
+    for (int o = 1; o < CPR; o <<= 1) cs += __shfl_xor(cs, o);
+    if (e % CPR == 0) cst[rows + t] = cs;
+  }
+  if (bad) flag[0] = 1;
+}
+
+// kv kernel, matrix-core form.  Wave (qh = w >> 1, kh = w & 1) owns the
+// 32 x 32 block (queries qh*32.., keys kh*32..) of each tile pair.
+template <int D>
+struct KvFast {
+  using C = Bw<D>;
+  bf16 qry[2][3][kTile * D];                    // [buffer][Q, W U' hi, W U' lo], swizzled [query][d or j]
+  bf16 kt[kTile * C::ROW];                      // K [key][d]
+  bf16 yh[kTile * C::ROW], yl[kTile * C::ROW];  // Y [key][j]
+  float cst[2][kTile], lse[2][kTile], c[D], split[D], bl[D];
+};
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    const float* __restrict__ beta, const float* __restrict__ lse, const float* __restrict__ cg,
+    const float* __restrict__ splitf, const bf16* __restrict__ wh, const bf16* __restrict__ wl,
+    const float* __restrict__ cst, float* __restrict__ dK, float* __restrict__ dV,
+    float* __restrict__ vdv, int H, int T, int ntile) {
+  using C = Bw<D>;
+  constexpr int NB = C::NCB;  // 32-row blocks of d (and of j)
+  __shared__ __align__(16) KvFast<D> sm;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
+  const int lb = xcd_order(blockIdx.x, gridDim.x);
+  const int kb = lb % ntile, bh = lb / ntile, h = bh % H;
+  const int k0 = kb * kTile;
+  const size_t base = (size_t)bh * T * D;
+  const size_t rows0 = (size_t)bh * ntile * kTile;
+  const int qh = wave >> 1, kh = wave & 1;
+  auto fetch = [&](int qb) {
+    const int q0 = qb * kTile;
+    bf16* dst = &sm.qry[qb & 1][0][0];
+    load_swz<D>(Q + base + (size_t)q0 * D, dst, T - 1 - q0);
+    load_swz<D>(wh + (rows0 + q0) * D, dst + kTile * D, kTile - 1);
+    load_swz<D>(wl + (rows0 + q0) * D, dst + 2 * kTile * D, kTile - 1);
+    // row constants and log-normalisers: one dword per lane (rows past T re-read row T - 1)
+    if (wave == 0)
+      __builtin_amdgcn_global_load_lds(cst + rows0 + q0 + lane, &sm.cst[qb & 1][0], 4, 0, 0);
+    if (wave == 1)
+      __builtin_amdgcn_global_load_lds(lse + (size_t)bh * T + min(q0 + lane, T - 1),
+                                       &sm.lse[qb & 1][0], 4, 0, 0);
+  };
+  fetch(kb);
+
+  for (int j = tid; j < D; j += kThreads) {
+    sm.bl[j] = beta[h * D + j] * kLog2e;
+    sm.split[j] = splitf[bh * D + j];
+    sm.c[j] = cg[bh * D + j];
+  }
+  stage_tile<D>(K + base, k0, T, sm.kt, nullptr);
+  __syncthreads();
+  // Y of this key tile (the q pass's rows of it, recomputed from V)
+  {
+    constexpr int CPR = D / 8;
+    for (int e = tid; e < kTile * CPR; e += kThreads) {
+      const int i = e / CPR, c8 = (e % CPR) * 8;
+      bf16x8 vx = {}, hi, lo;
+      if (k0 + i < T) vx = *reinterpret_cast<const bf16x8*>(V + base + (size_t)(k0 + i) * D + c8);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = c8 + u;
+        float y = 0.f;
+        if (k0 + i < T) {
+          const float x = fmaf(sm.bl[j], (float)vx[u], -sm.c[j]);
+          y = sm.split[j] != 0.f ? expm1f(x * kLn2) : exp2_hw(x);
+        }
+        bf16 a, b;
+        split_bf16(y, a, b);
+        hi[u] = a;
+        lo[u] = b;
+      }
+      *reinterpret_cast<bf16x8*>(sm.yh + i * C::ROW + c8) = hi;
+      *reinterpret_cast<bf16x8*>(sm.yl + i * C::ROW + c8) = lo;
+    }
+  }
+
+  f32x16 dvt[NB], dkt[NB];  // (j or d block) x keys kh*32.., partial over this wave's queries
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    dvt[b] = f32x16{};
+    dkt[b] = f32x16{};
+  }
+  const float scale2 = kLog2e / sqrtf((float)D);
+  const int qlast = (T - 1) / kTile;
+  const int i = kh * 32 + n;
+  for (int qb = kb; qb <= qlast; ++qb) {
+    const int q0 = qb * kTile;
+    wait_vmem();
+    __syncthreads();  // tile qb is in, and every wave is done with tile qb - 1
+    if (qb < qlast) fetch(qb + 1);
+    const bf16* tq = &sm.qry[qb & 1][0][0];
+    const bf16* tw = tq + kTile * D;   // W U' hi
+    const bf16* twl = tw + kTile * D;  // W U' lo
+    const float* lq = sm.lse[qb & 1];
+    const float* cq = sm.cst[qb & 1];
+
+    // S (queries x keys), p in fp32
+    f32x16 s = {};
+#pragma unroll
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      const bf16x8 a = frag_rows<D>(tq, qh * 32 + n, 2 * ks + hl);
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.kt + i * C::ROW + ks * 16 + hl * 8);
+      s = mfma(a, b, s);
+    }
+    float p[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+      const bool ok = k0 + i <= q0 + t && q0 + t < T && k0 + i < T;
+      p[r] = exp2_hw(ok ? fmaf(s[r], scale2, -lq[t] * kLog2e) : -INFINITY);
+    }
+    // dP = (W U') Y^T over j
+    f32x16 dp = {};
+#pragma unroll
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      const int bo = i * C::ROW + ks * 16 + hl * 8;
+      const bf16x8 ah = frag_rows<D>(tw, qh * 32 + n, 2 * ks + hl);
+      const bf16x8 al = frag_rows<D>(twl, qh * 32 + n, 2 * ks + hl);
+      const bf16x8 bh8 = *reinterpret_cast<const bf16x8*>(sm.yh + bo);
+      const bf16x8 bl8 = *reinterpret_cast<const bf16x8*>(sm.yl + bo);
+      dp = mfma(ah, bh8, dp);
+      dp = mfma(al, bh8, dp);
+      dp = mfma(ah, bl8, dp);
+    }
+    // dS = p (dP + const); p and dS as B operands (k = this wave's queries, accumulator order)
+    bf16x8 ph[2], pl[2], dsb[2];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+      const float ds = p[r] * (dp[r] + cq[t]);
+      bf16 a, b;
+      split_bf16(p[r], a, b);
+      ph[r >> 3][r & 7] = a;
+      pl[r >> 3][r & 7] = b;
+      dsb[r >> 3][r & 7] = (bf16)ds;
+    }
+    // dV^T(j block, keys) += (W U')^T P ;  dK^T(d block, keys) += Q^T dS
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int p0 = qh * 32 + k2 * 16;
+        const bf16x8 gh = frag_tr<D>(tw, b * 32, p0);
+        const bf16x8 gl = frag_tr<D>(twl, b * 32, p0);
+        dvt[b] = mfma(gh, ph[k2], dvt[b]);
+        dvt[b] = mfma(gl, ph[k2], dvt[b]);
+        dvt[b] = mfma(gh, pl[k2], dvt[b]);
+        dkt[b] = mfma(frag_tr<D>(tq, b * 32, p0), dsb[k2], dkt[b]);
+      }
+    }
+  }
+
+  // ---- combine the two query halves (waves qh = 0, 1 of the same kh)
+  __syncthreads();
+  // [2 kh][2 sets][NB][16][64] fp32 and the [64 keys][D] v dV terms, over the query buffers
+  float* red = reinterpret_cast<float*>(&sm.qry[0][0][0]);
+  float* vdvs = red + 4 * NB * 16 * 64;
+  static_assert((4 * C::NCB * 16 * 64 + kTile * D) * 4 <= sizeof(sm.qry), "reduction area");
+  auto slot = [&](int set, int b, int r) { return (((kh * 2 + set) * NB + b) * 16 + r) * 64 + lane; };
+  if (qh == 1) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        red[slot(0, b, r)] = dvt[b][r];
+        red[slot(1, b, r)] = dkt[b][r];
+      }
+  }
+  __syncthreads();
+  if (qh == 0) {
+    const float rs = 1.f / sqrtf((float)D);
+    const int key = k0 + i;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);  // j or d
+        const float sv = dvt[b][r] + red[slot(0, b, r)];
+        const float sk = dkt[b][r] + red[slot(1, b, r)];
+        float dvv = 0.f;
+        if (key < T) {
+          const float vv = (float)V[base + (size_t)key * D + row];
+          const float E = exp2_hw(fmaf(sm.bl[row], vv, -sm.c[row]));
+          dvv = E * beta[h * D + row] * sv;
+          dV[base + (size_t)key * D + row] = dvv;
+          dK[base + (size_t)key * D + row] = sk * rs;
+          dvv *= vv;
+        }
+        vdvs[i * D + row] = dvv;
+      }
+    }
+  }
+  __syncthreads();
+  for (int j = tid; j < D; j += kThreads) {
+    float acc = 0.f;
+    for (int k = 0; k < kTile; ++k) acc += vdvs[k * D + j];
+    vdv[((size_t)bh * ntile + kb) * D + j] = acc;
   }
 }
 
@@ -1068,11 +1235,16 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   const bf16* q = reinterpret_cast<const bf16*>(Q);
   const bf16* k = reinterpret_cast<const bf16*>(K);
   const bf16* v = reinterpret_cast<const bf16*>(V);
-  // workspace: flag | lse [nbh T] | c, split [nbh D] | vdv, gf, exact partials
-  // [nbh ntile D] | ln(Z/P) [nbh T D]
+  // workspace (fp32 unless noted): flag | lse [nbh T] | c, split [nbh D] |
+  // V max, V min, vdv, gf, exact partials [nbh ntile D] | ln(Z/P) [nbh T D] |
+  // row constants [nbh Tp] | two bf16 operand arrays [nbh Tp D], Tp = 64 ntile
+  // (Y hi and lo for the q pass, then W U' hi and lo for the kv pass)
+  const size_t tp = (size_t)ntile * kTile;
   const size_t nl = (size_t)nbh * T, nc = (size_t)nbh * D, np = (size_t)nbh * ntile * D;
-  const size_t nz = (size_t)nbh * T * D;
-  const size_t bytes = 256 + (nl + 2 * nc + 3 * np + nz) * sizeof(float);
+  const size_t nz = (size_t)nbh * T * D, nr = (size_t)nbh * tp, no = (size_t)nbh * tp * D;
+  const size_t fl = nl + 2 * nc + 5 * np + nz + nr;
+  const size_t fbytes = (fl * sizeof(float) + 255) & ~(size_t)255;
+  const size_t bytes = 256 + fbytes + 2 * no * sizeof(bf16);
   char* ws = nullptr;
   hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
   if (e != hipSuccess) return e;
@@ -1080,27 +1252,37 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   float* lse = reinterpret_cast<float*>(ws + 256);
   float* cg = lse + nl;
   float* splitf = cg + nc;
-  float* vdv = splitf + nc;
+  float* vmx = splitf + nc;
+  float* vmn = vmx + np;
+  float* vdv = vmn + np;
   float* gfp = vdv + np;
   float* exact = gfp + np;
   float* lnz = exact + np;
+  float* cst = lnz + nz;
+  bf16* o0 = reinterpret_cast<bf16*>(ws + 256 + fbytes);
+  bf16* o1 = o0 + no;
   const dim3 grid((unsigned)(nbh * ntile)), blk(kThreads);
-  hipLaunchKernelGGL(bwd_lse_kernel<D>, grid, blk, 0, stream, q, k, lse, T, ntile);
+  hipLaunchKernelGGL(bwd_lse_kernel<D>, grid, blk, 0, stream, q, k, v, lse, vmx, vmn, flag, T,
+                     ntile);
   e = hipGetLastError();
-  if (e == hipSuccess) {
-    hipLaunchKernelGGL(bwd_prep_kernel<D>, dim3((unsigned)nbh), blk, 0, stream, v, beta, cg, splitf,
-                       flag, H, T);
+  if (e == hipSuccess) {  // key side: Y
+    hipLaunchKernelGGL(bwd_prepk_kernel<D>, grid, blk, 0, stream, v, beta, vmx, vmn, cg, splitf, o0,
+                       o1, flag, H, T, ntile);
     e = hipGetLastError();
   }
-  // the q pass first: it forms ln(Z/P), which the kv pass uses
-  if (e == hipSuccess) {
-    hipLaunchKernelGGL(bwd_q_fast_kernel<D>, grid, blk, 0, stream, q, k, v, beta, out, lse, dout, cg,
-                       splitf, dQ, gfp, lnz, flag, H, T, ntile);
+  if (e == hipSuccess) {  // the q pass first: it forms ln(Z/P), which the kv pass uses
+    hipLaunchKernelGGL(bwd_q_fast_kernel<D>, grid, blk, 0, stream, q, k, beta, out, lse, dout, cg,
+                       splitf, o0, o1, dQ, gfp, lnz, flag, H, T, ntile);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) {  // query side: W U' over the same memory
+    hipLaunchKernelGGL(bwd_prepq_kernel<D>, grid, blk, 0, stream, beta, out, dout, lnz, cg, splitf,
+                       o0, o1, cst, flag, H, T, ntile);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(bwd_kv_fast_kernel<D>, grid, blk, 0, stream, q, k, v, beta, out, lse, dout,
-                       cg, splitf, lnz, dK, dV, vdv, flag, H, T, ntile);
+    hipLaunchKernelGGL(bwd_kv_fast_kernel<D>, grid, blk, 0, stream, q, k, v, beta, lse, cg, splitf,
+                       o0, o1, cst, dK, dV, vdv, H, T, ntile);
     e = hipGetLastError();
   }
   // exact element-wise passes: they return at once unless a block raised the flag

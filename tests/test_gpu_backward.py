@@ -7,8 +7,12 @@ bf16-rounded probabilities, a relative 2^-9 per term); each gradient within
 1e-4 (the posterior uses the forward's F, whose bf16 rounding moves beta F by
 at most 2^-8, and dS enters the dQ / dK products in bf16; the floor covers
 fp32 rounding of sum_j (G/beta) q - p sum_j G/beta, which cancels exactly
-where the gradient is zero, e.g. a single key).  Every case prints its name, shape
-and seed before touching the GPU.
+where the gradient is zero, e.g. a single key).  dbeta is the difference
+(sum_i v dV - sum_t G F) / beta of two terms of size sum |G v| / beta, whose
+products the matrix-core path forms from bf16 hi + lo parts (2^-16
+relative each); its floor adds 2^-14 sum_{b,t} |G v| / beta per (h, j), which
+matters only where dbeta itself is near zero (a single key: exactly zero).
+Every case prints its name, shape and seed before touching the GPU.
 """
 
 import math
@@ -51,13 +55,22 @@ def lse_ref(q, k):
     return torch.logsumexp(s, dim=-1).numpy()
 
 
-def check_grads(got, want, what):
+def dbeta_floor(v, b, g):
+    """2^-14 sum_{b,t} |G v| / beta per (h, j): the rounding scale of dbeta."""
+    gv = (np.abs(g.double().numpy()) * np.abs(v.double().numpy())).sum(axis=(0, 2))
+    return 2.0 ** -14 * gv / b.double().numpy()
+
+
+def check_grads(got, want, what, floor_db=None):
     for name, a, b in zip(("dq", "dk", "dv", "dbeta"), got, want):
         assert np.isfinite(a).all(), f"{what} {name}: non-finite"
         scale = np.abs(b).max()
         err = np.abs(a - b).max()
         say(f"{what} {name}: max err {err:.3e}, scale {scale:.3e} (tol {TOL} * scale + {ATOL})")
-        assert err <= TOL * scale + ATOL, f"{what} {name}: {err} > {TOL} * {scale} + {ATOL}"
+        tol = TOL * scale + ATOL
+        if name == "dbeta" and floor_db is not None:
+            tol = tol + floor_db
+        assert (np.abs(a - b) <= tol).all(), f"{what} {name}: {err} > {TOL} * {scale} + {ATOL} (+ floor)"
 
 
 def draw(seed, B, H, T, d, **kw):
@@ -78,7 +91,7 @@ def test_backward_shapes(fem, d, T):
     assert err <= 1e-2
     want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
                                     b.double().numpy(), g.double().numpy())
-    check_grads(grads, want, f"T{T} d{d}")
+    check_grads(grads, want, f"T{T} d{d}", dbeta_floor(v, b, g))
 
 
 def test_backward_forward_output_unchanged(fem):
@@ -98,7 +111,7 @@ def test_backward_beta_extremes(fem, beta):
     _, _, grads = run(fem, q, k, v, b, g)
     want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
                                     b.double().numpy(), g.double().numpy())
-    check_grads(grads, want, f"beta={beta}")
+    check_grads(grads, want, f"beta={beta}", dbeta_floor(v, b, g))
 
 
 def test_backward_longer_sequence(fem):
@@ -107,7 +120,7 @@ def test_backward_longer_sequence(fem):
     _, _, grads = run(fem, q, k, v, b, g)
     want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
                                     b.double().numpy(), g.double().numpy())
-    check_grads(grads, want, "T1024 d128")
+    check_grads(grads, want, "T1024 d128", dbeta_floor(v, b, g))
 
 
 def test_backward_deterministic(fem):
@@ -120,8 +133,9 @@ def test_backward_deterministic(fem):
 
 
 def test_backward_exact_fallback(fem):
-    """Values spread over [-5, 5] with beta = 16 put a row's F far below its
-    key tile's largest beta v, so blocks fall back to the element-wise pass."""
+    """Values spread over [-5, 5] with beta = 16 give channels a beta-scaled
+    range (16 log2(e) 10 = 231) beyond the matrix-core form's fp32 bound, so
+    the call reruns the element-wise pass."""
     say("backward fallback case: B1 H2 T300 d64, v in {-5, +5, N(0,1)}, beta 16, seed 13500")
     q, k, _, _, g = draw(13500, 1, 2, 300, 64)
     rng = np.random.default_rng(13501)
@@ -133,4 +147,4 @@ def test_backward_exact_fallback(fem):
     _, _, grads = run(fem, q, k, v, b, g)
     want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
                                     b.double().numpy(), g.double().numpy())
-    check_grads(grads, want, "fallback")
+    check_grads(grads, want, "fallback", dbeta_floor(v, b, g))
