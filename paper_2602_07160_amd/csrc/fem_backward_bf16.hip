@@ -514,6 +514,29 @@ __device__ __forceinline__ int swz_off(int row, int chunk) {  // byte offset
   return row * D * 2 + ((chunk ^ swz<D>(row)) << 4);
 }
 
+// LDS byte address of a generic pointer into shared memory.
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// Direct global -> LDS loads (lane l's bytes land at dst + l * size; dst is
+// the same for the whole wave).  Issued as inline assembly so the compiler
+// does not see an LDS write in flight: it would otherwise wait for the whole
+// load queue before every LDS read of the other buffer.  Completion is waited
+// for explicitly (wait_vmem) before the barrier that publishes the buffer.
+__device__ __forceinline__ void dma16(const void* src, void* dst) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const void* src, void* dst) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
+               : "memory", "m0");
+}
+
 // Direct global -> LDS copy of rows [0, 64) of a row-major [., D] bf16 source
 // into a swizzled tile; rows past lim re-read row lim (their keys or queries
 // are masked).  Wave w fills the 1 KiB blocks w, w + 4, ...: lane l of block
@@ -530,7 +553,7 @@ __device__ __forceinline__ void load_swz(const bf16* __restrict__ src, bf16* dst
     const int blk = wave + 4 * u;
     const int s = blk * 64 + lane, row = s / CPR, pos = s % CPR;
     const unsigned off = (unsigned)(min(row, lim) * D * 2 + ((pos ^ swz<D>(row)) << 4));
-    __builtin_amdgcn_global_load_lds(s8 + off, dst + blk * 512, 16, 0, 0);
+    dma16(s8 + off, dst + blk * 512);
   }
 }
 
@@ -815,57 +838,24 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
   float psum = 0.f;
   const float scale2 = kLog2e / sqrtf((float)D);
   const int t = qh * 32 + n;
-  for (int kb = 0; kb <= qb; ++kb) {
-    const int k0 = kb * kTile;
-    wait_vmem();
-    __syncthreads();  // tile kb is in, and every wave is done with tile kb - 1
-    if (kb < qb) fetch(kb + 1);
+  __syncthreads();  // Q, W U and the row constants are in LDS
+  // this wave's query rows as MFMA B fragments: Q (for S^T) and W U hi / lo
+  // (for dP^T), loop-invariant
+  bf16x8 qf[C::NKS], wf[C::NKS][2];
+#pragma unroll
+  for (int ks = 0; ks < C::NKS; ++ks) {
+    const int bo = t * C::ROW + ks * 16 + hl * 8;
+    qf[ks] = *reinterpret_cast<const bf16x8*>(sm.qt + bo);
+    wf[ks][0] = *reinterpret_cast<const bf16x8*>(sm.wuh + bo);
+    wf[ks][1] = *reinterpret_cast<const bf16x8*>(sm.wul + bo);
+  }
+  // dQ^T(d block, queries) += K^T dS^T ;  SA^T(j block, queries) += Y^T P^T
+  // for tile kb: the transposed operands come from transposing LDS reads
+  bf16x8 ph[2], pl[2], dsb[2];
+  auto phase3 = [&](int kb) {
     const bf16* kt = &sm.key[kb & 1][0][0];
-    const bf16* ty = kt + kTile * D;   // Y hi
-    const bf16* tyl = ty + kTile * D;  // Y lo
-
-    // S^T (keys x queries), p in fp32
-    f32x16 s = {};
-#pragma unroll
-    for (int ks = 0; ks < C::NKS; ++ks) {
-      const bf16x8 a = frag_rows<D>(kt, kh * 32 + n, 2 * ks + hl);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.qt + t * C::ROW + ks * 16 + hl * 8);
-      s = mfma(a, b, s);
-    }
-    const float l2 = sm.lse2[t];
-    const bool tlive = q0 + t < T;
-    float p[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int i = kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = k0 + i <= q0 + t && tlive && k0 + i < T;
-      p[r] = exp2_hw(ok ? fmaf(s[r], scale2, -l2) : -INFINITY);
-      psum += p[r];
-    }
-    // dP^T = Y (W U)^T over j
-    f32x16 dp = {};
-#pragma unroll
-    for (int ks = 0; ks < C::NKS; ++ks) {
-      const int bo = t * C::ROW + ks * 16 + hl * 8;
-      const bf16x8 ah = frag_rows<D>(ty, kh * 32 + n, 2 * ks + hl);
-      const bf16x8 al = frag_rows<D>(tyl, kh * 32 + n, 2 * ks + hl);
-      const bf16x8 bh8 = *reinterpret_cast<const bf16x8*>(sm.wuh + bo);
-      const bf16x8 bl8 = *reinterpret_cast<const bf16x8*>(sm.wul + bo);
-      dp = mfma(ah, bh8, dp);
-      dp = mfma(al, bh8, dp);
-      dp = mfma(ah, bl8, dp);
-    }
-    bf16x8 ph[2], pl[2], dsb[2];
-    const float ct = sm.cst[t];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      bf16 a, b;
-      split_bf16(p[r], a, b);
-      ph[r >> 3][r & 7] = a;
-      pl[r >> 3][r & 7] = b;
-      dsb[r >> 3][r & 7] = (bf16)(p[r] * (dp[r] + ct));
-    }
-    // dQ^T(d block, queries) += K^T dS^T ;  SA^T(j block, queries) += Y^T P^T
+    const bf16* ty = kt + kTile * D;
+    const bf16* tyl = ty + kTile * D;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
 #pragma unroll
@@ -879,6 +869,67 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
         sat[b] = mfma(yh8, pl[k2], sat[b]);
       }
     }
+  };
+  // Per iteration: tile kb's loads have landed and every wave is done with
+  // tile kb - 1, whose buffer tile kb + 1 now streams into.
+  for (int kb = 0; kb <= qb; ++kb) {
+    const int k0 = kb * kTile;
+    wait_vmem();
+    __syncthreads();
+    if (kb < qb) fetch(kb + 1);
+    const bf16* kt = &sm.key[kb & 1][0][0];
+    const bf16* ty = kt + kTile * D;   // Y hi
+    const bf16* tyl = ty + kTile * D;  // Y lo
+
+    // S^T (keys x queries) then dP^T = Y (W U)^T over j: 2 NKS steps whose
+    // key-side fragments are read two steps ahead (scheduling barriers keep
+    // the order, so each MFMA waits only for reads issued two steps before);
+    // the query-side fragments stay in registers for the whole loop
+    f32x16 s = {}, dp = {};
+    {
+      bf16x8 ring[3][2];
+      auto load_step = [&](int k, bf16x8* f) {
+        if (k < C::NKS) {
+          f[0] = frag_rows<D>(kt, kh * 32 + n, 2 * k + hl);
+        } else {
+          const int ks = k - C::NKS;
+          f[0] = frag_rows<D>(ty, kh * 32 + n, 2 * ks + hl);
+          f[1] = frag_rows<D>(tyl, kh * 32 + n, 2 * ks + hl);
+        }
+      };
+      load_step(0, ring[0]);
+      load_step(1, ring[1]);
+#pragma unroll
+      for (int k = 0; k < 2 * C::NKS; ++k) {
+        if (k + 2 < 2 * C::NKS) load_step(k + 2, ring[(k + 2) % 3]);
+        const bf16x8* f = ring[k % 3];
+        if (k < C::NKS) {
+          s = mfma(f[0], qf[k], s);
+        } else {
+          const int ks = k - C::NKS;
+          dp = mfma(f[0], wf[ks][0], dp);
+          dp = mfma(f[1], wf[ks][0], dp);
+          dp = mfma(f[0], wf[ks][1], dp);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    const float l2 = sm.lse2[t];
+    const bool tlive = q0 + t < T;
+    const float ct = sm.cst[t];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+      const bool ok = k0 + i <= q0 + t && tlive && k0 + i < T;
+      const float p = exp2_hw(ok ? fmaf(s[r], scale2, -l2) : -INFINITY);
+      psum += p;
+      bf16 a, b;
+      split_bf16(p, a, b);
+      ph[r >> 3][r & 7] = a;
+      pl[r >> 3][r & 7] = b;
+      dsb[r >> 3][r & 7] = (bf16)(p * (dp[r] + ct));
+    }
+    phase3(kb);
   }
   if (bad) flag[0] = 1;
 
@@ -1041,11 +1092,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
     load_swz<D>(wh + (rows0 + q0) * D, dst + kTile * D, kTile - 1);
     load_swz<D>(wl + (rows0 + q0) * D, dst + 2 * kTile * D, kTile - 1);
     // row constants and log-normalisers: one dword per lane (rows past T re-read row T - 1)
-    if (wave == 0)
-      __builtin_amdgcn_global_load_lds(cst + rows0 + q0 + lane, &sm.cst[qb & 1][0], 4, 0, 0);
-    if (wave == 1)
-      __builtin_amdgcn_global_load_lds(lse + (size_t)bh * T + min(q0 + lane, T - 1),
-                                       &sm.lse[qb & 1][0], 4, 0, 0);
+    if (wave == 0) dma4(cst + rows0 + q0 + lane, &sm.cst[qb & 1][0]);
+    if (wave == 1) dma4(lse + (size_t)bh * T + min(q0 + lane, T - 1), &sm.lse[qb & 1][0]);
   };
   fetch(kb);
 
@@ -1090,58 +1138,24 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
   const float scale2 = kLog2e / sqrtf((float)D);
   const int qlast = (T - 1) / kTile;
   const int i = kh * 32 + n;
-  for (int qb = kb; qb <= qlast; ++qb) {
-    const int q0 = qb * kTile;
-    wait_vmem();
-    __syncthreads();  // tile qb is in, and every wave is done with tile qb - 1
-    if (qb < qlast) fetch(qb + 1);
+  __syncthreads();
+  // this wave's key rows as MFMA B fragments: K (for S) and Y hi / lo (for
+  // dP), loop-invariant
+  bf16x8 kf[C::NKS], yf[C::NKS][2];
+#pragma unroll
+  for (int ks = 0; ks < C::NKS; ++ks) {
+    const int bo = i * C::ROW + ks * 16 + hl * 8;
+    kf[ks] = *reinterpret_cast<const bf16x8*>(sm.kt + bo);
+    yf[ks][0] = *reinterpret_cast<const bf16x8*>(sm.yh + bo);
+    yf[ks][1] = *reinterpret_cast<const bf16x8*>(sm.yl + bo);
+  }
+  // dV^T(j block, keys) += (W U')^T P ;  dK^T(d block, keys) += Q^T dS for
+  // query tile qb: the transposed operands come from transposing LDS reads
+  bf16x8 ph[2], pl[2], dsb[2];
+  auto phase3 = [&](int qb) {
     const bf16* tq = &sm.qry[qb & 1][0][0];
-    const bf16* tw = tq + kTile * D;   // W U' hi
-    const bf16* twl = tw + kTile * D;  // W U' lo
-    const float* lq = sm.lse[qb & 1];
-    const float* cq = sm.cst[qb & 1];
-
-    // S (queries x keys), p in fp32
-    f32x16 s = {};
-#pragma unroll
-    for (int ks = 0; ks < C::NKS; ++ks) {
-      const bf16x8 a = frag_rows<D>(tq, qh * 32 + n, 2 * ks + hl);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.kt + i * C::ROW + ks * 16 + hl * 8);
-      s = mfma(a, b, s);
-    }
-    float p[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = k0 + i <= q0 + t && q0 + t < T && k0 + i < T;
-      p[r] = exp2_hw(ok ? fmaf(s[r], scale2, -lq[t] * kLog2e) : -INFINITY);
-    }
-    // dP = (W U') Y^T over j
-    f32x16 dp = {};
-#pragma unroll
-    for (int ks = 0; ks < C::NKS; ++ks) {
-      const int bo = i * C::ROW + ks * 16 + hl * 8;
-      const bf16x8 ah = frag_rows<D>(tw, qh * 32 + n, 2 * ks + hl);
-      const bf16x8 al = frag_rows<D>(twl, qh * 32 + n, 2 * ks + hl);
-      const bf16x8 bh8 = *reinterpret_cast<const bf16x8*>(sm.yh + bo);
-      const bf16x8 bl8 = *reinterpret_cast<const bf16x8*>(sm.yl + bo);
-      dp = mfma(ah, bh8, dp);
-      dp = mfma(al, bh8, dp);
-      dp = mfma(ah, bl8, dp);
-    }
-    // dS = p (dP + const); p and dS as B operands (k = this wave's queries, accumulator order)
-    bf16x8 ph[2], pl[2], dsb[2];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const float ds = p[r] * (dp[r] + cq[t]);
-      bf16 a, b;
-      split_bf16(p[r], a, b);
-      ph[r >> 3][r & 7] = a;
-      pl[r >> 3][r & 7] = b;
-      dsb[r >> 3][r & 7] = (bf16)ds;
-    }
-    // dV^T(j block, keys) += (W U')^T P ;  dK^T(d block, keys) += Q^T dS
+    const bf16* tw = tq + kTile * D;
+    const bf16* twl = tw + kTile * D;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
 #pragma unroll
@@ -1155,6 +1169,66 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
         dkt[b] = mfma(frag_tr<D>(tq, b * 32, p0), dsb[k2], dkt[b]);
       }
     }
+  };
+  // Per iteration: query tile qb's loads have landed and every wave is done
+  // with tile qb - 1, whose buffer tile qb + 1 now streams into.
+  for (int qb = kb; qb <= qlast; ++qb) {
+    const int q0 = qb * kTile;
+    wait_vmem();
+    __syncthreads();
+    if (qb < qlast) fetch(qb + 1);
+    const bf16* tq = &sm.qry[qb & 1][0][0];
+    const bf16* tw = tq + kTile * D;   // W U' hi
+    const bf16* twl = tw + kTile * D;  // W U' lo
+    const float* lq = sm.lse[qb & 1];
+    const float* cq = sm.cst[qb & 1];
+
+    // S (queries x keys) then dP = (W U') Y^T over j: 2 NKS steps whose
+    // query-side fragments are read two steps ahead (scheduling barriers
+    // keep the order); the key-side fragments stay in registers
+    f32x16 s = {}, dp = {};
+    {
+      bf16x8 ring[3][2];
+      auto load_step = [&](int k, bf16x8* f) {
+        if (k < C::NKS) {
+          f[0] = frag_rows<D>(tq, qh * 32 + n, 2 * k + hl);
+        } else {
+          const int ks = k - C::NKS;
+          f[0] = frag_rows<D>(tw, qh * 32 + n, 2 * ks + hl);
+          f[1] = frag_rows<D>(twl, qh * 32 + n, 2 * ks + hl);
+        }
+      };
+      load_step(0, ring[0]);
+      load_step(1, ring[1]);
+#pragma unroll
+      for (int k = 0; k < 2 * C::NKS; ++k) {
+        if (k + 2 < 2 * C::NKS) load_step(k + 2, ring[(k + 2) % 3]);
+        const bf16x8* f = ring[k % 3];
+        if (k < C::NKS) {
+          s = mfma(f[0], kf[k], s);
+        } else {
+          const int ks = k - C::NKS;
+          dp = mfma(f[0], yf[ks][0], dp);
+          dp = mfma(f[1], yf[ks][0], dp);
+          dp = mfma(f[0], yf[ks][1], dp);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // p, and dS = p (dP + const); p and dS as B operands (k = this wave's
+    // queries, accumulator order)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+      const bool ok = k0 + i <= q0 + t && q0 + t < T && k0 + i < T;
+      const float p = exp2_hw(ok ? fmaf(s[r], scale2, -lq[t] * kLog2e) : -INFINITY);
+      bf16 a, b;
+      split_bf16(p, a, b);
+      ph[r >> 3][r & 7] = a;
+      pl[r >> 3][r & 7] = b;
+      dsb[r >> 3][r & 7] = (bf16)(p * (dp[r] + cq[t]));
+    }
+    phase3(qb);
   }
 
   // ---- combine the two query halves (waves qh = 0, 1 of the same kh)
