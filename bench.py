@@ -18,8 +18,8 @@ two-level gated read (fem_softmax_gated_fwd) on the headline shape under
 (fem_gla_fwd) on the linear workload's shape with seeded log-decays under
 "gla" (bytes = q, k, v, the fp32 decays and out, once each), and the
 backward pass (fem_softmax_bwd) on the headline shape under "backward": its
-matrix-core passes run 34*d FLOP per (t, i <= t) pair (Q K^T three times --
-log-normaliser, q and kv passes --, the posterior products dP in both passes
+matrix-core passes run 32*d FLOP per (t, i <= t) pair (Q K^T in the q and kv
+passes, the posterior products dP in both passes
 and the normaliser sums SA in the q pass with bf16 hi/lo operands, three
 products each, and dQ, dK, dV^T (hi/lo)), so its roofline is the bf16
 matrix peak.
@@ -200,14 +200,14 @@ def main():
                            generator=torch.Generator(device=dev).manual_seed(7))
         fnb = lambda: binding.fem_softmax_bwd(qd, kd, vd, bd, outt, lse, gout)
         msb = time_calls(fnb, args.backward_steps, 1)
-        flop_b = 34 * d * B * H * T * (T + 1) // 2
+        flop_b = 32 * d * B * H * T * (T + 1) // 2
         result["backward"] = {
             "workload": w.name + "_bwd", "ms": round(msb, 3), "steps": args.backward_steps,
             "flop_per_call": flop_b,
             "achieved_TFLOPs": round(flop_b / (msb * 1e-3) / 1e12, 2),
             "peak_TFLOPs": PEAK_BF16_TFLOPS,
             "frac": round(flop_b / (msb * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-            "kernels": ["bwd_q_fast_kernel<128>", "bwd_kv_fast_kernel<128>", "bwd_lse_kernel<128>", "bwd_prepk_kernel<128>", "bwd_prepq_kernel<128>"],
+            "kernels": ["bwd_q_fast_kernel<128>", "bwd_kv_fast_kernel<128>", "bwd_vstats_kernel<128>", "bwd_prepk_kernel<128>", "bwd_prepq_kernel<128>"],
         }
         del outt, lse, gout
     if not args.no_decode:

@@ -164,16 +164,17 @@ int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
  *   dQ, dK, dV     : [B, H, T, d] float32, overwritten
  *   dbeta          : [H, d] float32, overwritten (summed over batch and time)
  * The posterior ratio R = exp(beta (v_i - out_t)) is factorised as
- * E_i U_t per channel, so the sums over keys and channels run on the matrix
- * cores (bf16 hi + lo parts, ~2^-16 relative); channels whose beta-scaled
- * value range is at most 4 / log2(e) use the cancellation-free form
- * R - 1 = (E - 1) U + (U - 1).  Where a factor would leave fp32's range (a
- * row's out far below the largest beta v it is compared with) the whole call
- * reruns an element-wise pass that is exact in form for every beta > 0.
- * dbeta is formed from the normalised posterior sums, so the forward's
- * rounding of out cancels from it.  A workspace of about
- * 4 * B * H * T * (d + 1) + 12 * B * H * ceil(T / 64) * d bytes comes from
- * the library's pool as in fem_linear_fwd.  All pointers 16-byte aligned;
+ * E_i U_t per channel (one shift per channel over the sequence), so the sums
+ * over keys and channels run on the matrix cores (bf16 hi + lo parts,
+ * ~2^-16 relative); channels whose beta-scaled value range is at most
+ * 4 / log2(e) use the cancellation-free form R - 1 = (E - 1) U + (U - 1).
+ * A channel whose range beta (max v - min v) exceeds 110 / log2(e) would
+ * leave fp32's exponent range: the whole call then reruns an element-wise
+ * pass that is exact in form for every beta > 0 (~15x slower).  dbeta is
+ * formed from the normalised posterior sums, so the forward's rounding of
+ * out cancels from it.  A workspace of about 8 * B * H * T * d +
+ * 20 * B * H * ceil(T / 64) * d bytes comes from the library's pool as in
+ * fem_linear_fwd.  All pointers 16-byte aligned;
  * outputs must not alias inputs.  Returns a fem_status.
  */
 int fem_softmax_fwd_train(const void* Q, const void* K, const void* V,

@@ -13,6 +13,12 @@
 //              = sum_t G_tj (E_{q_tj}[v_j] - F_tj) / beta_j
 // with the posterior q_tj(i) = p_t(i) e^{beta_j (v_ij - F_tj)}.
 //
+// Two evaluations of these sums live here.  The default one (the matrix-core
+// path, below the element-wise kernels) factors the posterior ratio so that
+// every sum over keys or channels is an MFMA product; it covers every channel
+// whose beta-scaled value range fits fp32's exponent range.  Otherwise the
+// element-wise kernels, exact in form for every beta > 0, redo the call:
+//
 // The posterior is evaluated element by element in the exponent domain,
 //   q_tj(i) = 2^{(s_ti log2e - lse_t log2e) + (beta_j log2e)(v_ij - F_tj)},
 // from the forward's log-normaliser lse and output F: the exponent is at
@@ -437,8 +443,10 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
 // sum_t p G U are at most T max|G| 2^L).  A channel with a wider range, or a
 // row whose W U would leave that range, sets a device flag; the element-wise
 // kernels then redo the whole pass, and otherwise return at once.
-// p comes from an fp32 log-normaliser recomputed here (the forward's lse sums
-// bf16-rounded probabilities), so the rows of p sum to one to fp32 accuracy.
+// p comes from the forward's lse, which sums bf16-rounded probabilities and
+// so may be off by a few 2^-9: the q pass sums P = sum_i p per row exactly,
+// divides its products by P and hands lse + ln P to the kv pass, so both use
+// rows of p that sum to one to fp32 accuracy.
 //
 // Normalisation: R^ built from the forward's F^ gives sum_i p R^ = Z/P =
 // e^{beta (F - F^)} != 1 (the forward rounds p to bf16).  The q kernel, which
@@ -450,11 +458,11 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
 // small next to their parts (~ beta Var/2 at small beta, ~ KL/beta at large).
 //
 // Kernels, in stream order:
-//   lse:   fp32 lse per query; per 64-row tile, each channel's max and min v;
+//   vstats: per 64-row tile, each channel's max and min v;
 //   prepk: c_j and the channel form; Y row-major (hi and lo);
 //   q:     per 64-query tile over its key tiles: S^T, p, dP^T = Y (W U)^T,
-//          dS, dQ^T += K^T dS^T and SA^T += Y^T P^T; ln(Z/P) and the G F^
-//          terms of dbeta;
+//          dS, dQ^T += K^T dS^T and SA^T += Y^T P^T; ln(Z/P), lse + ln P and
+//          the G F^ terms of dbeta;
 //   prepq: W U' row-major (hi and lo) and the row constants;
 //   kv:    per 64-key tile over its query tiles: S, p, dP = (W U') Y^T, dS,
 //          dV^T += (W U')^T P (dV = beta E times it) and dK^T += Q^T dS; the
@@ -591,99 +599,38 @@ __device__ __forceinline__ bf16x8 frag_tr(const bf16* t, int col0, int p0) {
   return __builtin_bit_cast(bf16x8, x);
 }
 
-// The prior's log-normaliser in fp32 from unrounded probabilities:
-// lse_t = ln sum_{i<=t} exp(q_t.k_i / sqrt d).  One workgroup per (b, h,
-// 64-query tile); wave (kh, qh) takes the S^T block of keys kh*32.. and
-// queries qh*32..; lane (query n, half hl) keeps a running (max, sum).  The
-// workgroup also writes the max and min of each channel of V over its 64
-// rows, and the first one clears the fallback flag.
+// Per 64-row tile of V, the max and min of each channel (for the channel
+// shifts and forms); the first workgroup clears the fallback flag.
 template <int D>
-__global__ __launch_bounds__(kThreads) void bwd_lse_kernel(const bf16* __restrict__ Q,
-                                                           const bf16* __restrict__ K,
-                                                           const bf16* __restrict__ V,
-                                                           float* __restrict__ lse,
-                                                           float* __restrict__ vmx,
-                                                           float* __restrict__ vmn,
-                                                           int* __restrict__ flag, int T,
-                                                           int ntile) {
-  using C = Bw<D>;
-  __shared__ __align__(16) bf16 qt[kTile * C::ROW];
-  __shared__ __align__(16) bf16 kt[kTile * C::ROW];
-  __shared__ float rm[4][64], rs[4][64];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
-  const int qb = blockIdx.x % ntile, bh = blockIdx.x / ntile;
-  const int q0 = qb * kTile;
-  const size_t base = (size_t)bh * T * D;
-  const int kh = wave >> 1, qh = wave & 1;
-  const int t = qh * 32 + n;
+__global__ __launch_bounds__(kThreads) void bwd_vstats_kernel(const bf16* __restrict__ V,
+                                                              float* __restrict__ vmx,
+                                                              float* __restrict__ vmn,
+                                                              int* __restrict__ flag, int T,
+                                                              int ntile) {
+  constexpr int RG = kThreads / D;
+  __shared__ float sx[kThreads], sn[kThreads];
+  const int tid = threadIdx.x, j = tid % D, rg = tid / D;
+  const int tb = blockIdx.x % ntile, bh = blockIdx.x / ntile;
+  const int r0 = tb * kTile;
   if (blockIdx.x == 0 && tid == 0) flag[0] = 0;
-  {
-    constexpr int RG = kThreads / D;
-    const int j = tid % D, rg = tid / D;
-    float a = -INFINITY, b = INFINITY;
-    for (int r = rg; r < kTile; r += RG)
-      if (q0 + r < T) {
-        const float v = (float)V[base + (size_t)(q0 + r) * D + j];
-        a = fmaxf(a, v);
-        b = fminf(b, v);
-      }
-    float* sx = &rm[0][0];
-    float* sn = &rs[0][0];
-    sx[tid] = a;
-    sn[tid] = b;
-    __syncthreads();
-    if (rg == 0) {
-      for (int g = 1; g < RG; ++g) {
-        a = fmaxf(a, sx[g * D + j]);
-        b = fminf(b, sn[g * D + j]);
-      }
-      vmx[((size_t)bh * ntile + qb) * D + j] = a;
-      vmn[((size_t)bh * ntile + qb) * D + j] = b;
+  const bf16* Vh = V + (size_t)bh * T * D;
+  float a = -INFINITY, b = INFINITY;
+  for (int r = rg; r < kTile; r += RG)
+    if (r0 + r < T) {
+      const float v = (float)Vh[(size_t)(r0 + r) * D + j];
+      a = fmaxf(a, v);
+      b = fminf(b, v);
     }
-  }
-  stage_tile<D>(Q + base, q0, T, qt, nullptr);
-  const float scale2 = kLog2e / sqrtf((float)D);
-  float m = -INFINITY, sum = 0.f;
-  for (int kb = 0; kb <= qb; ++kb) {
-    const int k0 = kb * kTile;
-    __syncthreads();
-    stage_tile<D>(K + base, k0, T, kt, nullptr);
-    __syncthreads();
-    const f32x16 acc = score_block<D>(kt, qt, kh, qh);  // M = keys, N = queries
-    float x[16], bm = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int i = kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = k0 + i <= q0 + t && k0 + i < T;
-      x[r] = ok ? acc[r] * scale2 : -INFINITY;
-      bm = fmaxf(bm, x[r]);
-    }
-    const float mn = fmaxf(m, bm);
-    if (mn != -INFINITY) {
-      float a = sum * exp2_hw(m - mn);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) a += exp2_hw(x[r] - mn);
-      sum = a;
-      m = mn;
-    }
-  }
+  sx[tid] = a;
+  sn[tid] = b;
   __syncthreads();
-  rm[wave][lane] = m;
-  rs[wave][lane] = sum;
-  __syncthreads();
-  if (tid < kTile) {
-    const int qq = tid >> 5, nn = tid & 31;  // query qq*32 + nn: waves (0, qq), (1, qq), both halves
-    float M = -INFINITY, S = 0.f;
-    for (int k2 = 0; k2 < 2; ++k2)
-      for (int h2 = 0; h2 < 2; ++h2) {
-        const float mm = rm[k2 * 2 + qq][h2 * 32 + nn], ss = rs[k2 * 2 + qq][h2 * 32 + nn];
-        const float mx = fmaxf(M, mm);
-        if (mx != -INFINITY) {
-          S = S * exp2_hw(M - mx) + ss * exp2_hw(mm - mx);
-          M = mx;
-        }
-      }
-    if (q0 + tid < T) lse[(size_t)bh * T + q0 + tid] = (M + log2_hw(S)) * kLn2;
+  if (rg == 0) {
+    for (int g = 1; g < RG; ++g) {
+      a = fmaxf(a, sx[g * D + j]);
+      b = fminf(b, sn[g * D + j]);
+    }
+    vmx[((size_t)bh * ntile + tb) * D + j] = a;
+    vmn[((size_t)bh * ntile + tb) * D + j] = b;
   }
 }
 
@@ -772,7 +719,8 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
     const float* __restrict__ F, const float* __restrict__ lse, const float* __restrict__ G,
     const float* __restrict__ cg, const float* __restrict__ splitf, const bf16* __restrict__ yh,
     const bf16* __restrict__ yl, float* __restrict__ dQ, float* __restrict__ gf,
-    float* __restrict__ lnz, int* __restrict__ flag, int H, int T, int ntile) {
+    float* __restrict__ lnz, float* __restrict__ lse_p, int* __restrict__ flag, int H, int T,
+    int ntile) {
   using C = Bw<D>;
   constexpr int NB = C::NCB;
   __shared__ __align__(16) QFast<D> sm;
@@ -955,9 +903,12 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
   }
   __syncthreads();
   if (kh == 0) {
-    const float rs = 1.f / sqrtf((float)D);
     const int tq = q0 + qh * 32 + n;
     const float P = sm.pt[0][qh * 32 + n] + sm.pt[1][qh * 32 + n];
+    // p was formed from the forward's lse, whose sum of bf16-rounded terms
+    // may differ from the exact one by a few 2^-9: P = sum_i p rescales it
+    const float rs = 1.f / (sqrtf((float)D) * P);
+    if (hl == 0 && tq < T) lse_p[(size_t)bh * T + tq] = lse[(size_t)bh * T + tq] + logf(P);
     bool under = false;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -1280,21 +1231,30 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
 }
 
 // dbeta from the per-tile partial sums: the exact pass's when it ran, else
-// (sum v dV - sum G F) / beta from the matrix-core pass.
+// (sum v dV - sum G F) / beta from the matrix-core pass.  One workgroup per
+// (h, 32 channels); its 8 thread rows split the (b, tile) partials and meet
+// in LDS.
 template <int D>
-__global__ void dbeta_kernel(const float* __restrict__ exact, const float* __restrict__ vdv,
-                             const float* __restrict__ gf, const float* __restrict__ beta,
-                             const int* __restrict__ flag, float* __restrict__ dbeta, int B, int H,
-                             int ntile) {
-  const int h = blockIdx.x;
+__global__ __launch_bounds__(256) void dbeta_kernel(const float* __restrict__ exact,
+                                                    const float* __restrict__ vdv,
+                                                    const float* __restrict__ gf,
+                                                    const float* __restrict__ beta,
+                                                    const int* __restrict__ flag,
+                                                    float* __restrict__ dbeta, int B, int H,
+                                                    int ntile) {
+  __shared__ double part[8][32];
+  const int h = blockIdx.x, j = blockIdx.y * 32 + (threadIdx.x & 31), row = threadIdx.x >> 5;
   const bool ex = flag[0] != 0;
-  for (int j = threadIdx.x; j < D; j += blockDim.x) {
-    double s = 0.0;
-    for (int b = 0; b < B; ++b)
-      for (int c = 0; c < ntile; ++c) {
-        const size_t at = (((size_t)b * H + h) * ntile + c) * D + j;
-        s += ex ? (double)exact[at] : (double)vdv[at] - (double)gf[at];
-      }
+  double s = 0.0;
+  for (int u = row; u < B * ntile; u += 8) {
+    const int b = u / ntile, c = u % ntile;
+    const size_t at = (((size_t)b * H + h) * ntile + c) * D + j;
+    s += ex ? (double)exact[at] : (double)vdv[at] - (double)gf[at];
+  }
+  part[row][threadIdx.x & 31] = s;
+  __syncthreads();
+  if (row == 0) {
+    for (int r = 1; r < 8; ++r) s += part[r][threadIdx.x & 31];
     dbeta[h * D + j] = (float)(ex ? s : s / (double)beta[h * D + j]);
   }
 }
@@ -1303,13 +1263,13 @@ template <int D>
 hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* beta,
                       const float* out, const float* lse_fwd, const float* dout, float* dQ,
                       float* dK, float* dV, float* dbeta, int B, int H, int T, hipStream_t stream) {
-  (void)lse_fwd;  // the passes use the fp32 log-normaliser recomputed below
   const int nbh = B * H;
   const int ntile = (T + kTile - 1) / kTile;
   const bf16* q = reinterpret_cast<const bf16*>(Q);
   const bf16* k = reinterpret_cast<const bf16*>(K);
   const bf16* v = reinterpret_cast<const bf16*>(V);
-  // workspace (fp32 unless noted): flag | lse [nbh T] | c, split [nbh D] |
+  // workspace (fp32 unless noted): flag | lse renormalised by the q pass
+  // [nbh T] | c, split [nbh D] |
   // V max, V min, vdv, gf, exact partials [nbh ntile D] | ln(Z/P) [nbh T D] |
   // row constants [nbh Tp] | two bf16 operand arrays [nbh Tp D], Tp = 64 ntile
   // (Y hi and lo for the q pass, then W U' hi and lo for the kv pass)
@@ -1336,8 +1296,7 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   bf16* o0 = reinterpret_cast<bf16*>(ws + 256 + fbytes);
   bf16* o1 = o0 + no;
   const dim3 grid((unsigned)(nbh * ntile)), blk(kThreads);
-  hipLaunchKernelGGL(bwd_lse_kernel<D>, grid, blk, 0, stream, q, k, v, lse, vmx, vmn, flag, T,
-                     ntile);
+  hipLaunchKernelGGL(bwd_vstats_kernel<D>, grid, blk, 0, stream, v, vmx, vmn, flag, T, ntile);
   e = hipGetLastError();
   if (e == hipSuccess) {  // key side: Y
     hipLaunchKernelGGL(bwd_prepk_kernel<D>, grid, blk, 0, stream, v, beta, vmx, vmn, cg, splitf, o0,
@@ -1345,8 +1304,8 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
     e = hipGetLastError();
   }
   if (e == hipSuccess) {  // the q pass first: it forms ln(Z/P), which the kv pass uses
-    hipLaunchKernelGGL(bwd_q_fast_kernel<D>, grid, blk, 0, stream, q, k, beta, out, lse, dout, cg,
-                       splitf, o0, o1, dQ, gfp, lnz, flag, H, T, ntile);
+    hipLaunchKernelGGL(bwd_q_fast_kernel<D>, grid, blk, 0, stream, q, k, beta, out, lse_fwd, dout,
+                       cg, splitf, o0, o1, dQ, gfp, lnz, lse, flag, H, T, ntile);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {  // query side: W U' over the same memory
@@ -1371,8 +1330,8 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(dbeta_kernel<D>, dim3((unsigned)H), dim3(128), 0, stream, exact, vdv, gfp,
-                       beta, flag, dbeta, B, H, ntile);
+    hipLaunchKernelGGL(dbeta_kernel<D>, dim3((unsigned)H, D / 32), dim3(256), 0, stream, exact, vdv,
+                       gfp, beta, flag, dbeta, B, H, ntile);
     e = hipGetLastError();
   }
   const hipError_t f = workspace_free(ws, stream);
