@@ -567,6 +567,12 @@ __device__ __forceinline__ void load_swz(const bf16* __restrict__ src, bf16* dst
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Make the compiler complete the loads of x here: a use before the main loop
+// keeps its wait for them out of the loop, where it would also wait for the
+// direct loads in flight.
+__device__ __forceinline__ void settle(const bf16x8& x) { asm volatile("" ::"v"(x)); }
+__device__ __forceinline__ void settle(float x) { asm volatile("" ::"v"(x)); }
+
 // Row-major MFMA fragment of a swizzled tile: 8 bf16 of row `row`, chunk `chunk`.
 template <int D>
 __device__ __forceinline__ bf16x8 frag_rows(const bf16* t, int row, int chunk) {
@@ -663,70 +669,100 @@ __device__ __forceinline__ void channel_consts(const float* __restrict__ beta,
   }
 }
 
-// Y of each key: A = E - 1 (split) or E (plain), E = 2^{bl v - c}, row-major
-// hi and lo parts, zero past T.  One thread per 8 channels of a row.
+// Per 64-row tile of a (b, h): the channel constants (the first tile publishes
+// them); for the rows as keys, Y = A (split) or E (plain), E = 2^{bl v - c};
+// for the rows as queries of the q pass, W U with U = 2^{c - bl F} and the
+// row constants sum_j (split ? W (U - 1) : -W).  Y and W U row-major, hi and
+// lo parts, zero past T.  Thread e handles 8 channels of one row; the D/8
+// threads of a row are adjacent lanes.
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_prepk_kernel(
-    const bf16* __restrict__ V, const float* __restrict__ beta, const float* __restrict__ vmx,
-    const float* __restrict__ vmn, float* __restrict__ cg, float* __restrict__ splitf,
-    bf16* __restrict__ yh, bf16* __restrict__ yl, int* __restrict__ flag, int H, int T,
-    int ntile) {
+    const bf16* __restrict__ V, const float* __restrict__ beta, const float* __restrict__ F,
+    const float* __restrict__ G, const float* __restrict__ vmx, const float* __restrict__ vmn,
+    float* __restrict__ cg, float* __restrict__ splitf, bf16* __restrict__ yh,
+    bf16* __restrict__ yl, bf16* __restrict__ wh, bf16* __restrict__ wl,
+    float* __restrict__ cst, int* __restrict__ flag, int H, int T, int ntile) {
   __shared__ float c[D], split[D], bl[D];
+  constexpr int CPR = D / 8;
+  static_assert(kThreads % CPR == 0 && CPR <= 64, "a row's threads share a wave");
   const int kb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
   const int k0 = kb * kTile;
   channel_consts<D>(beta, vmx, vmn, bh, h, ntile, c, split, bl, kb == 0, cg, splitf, flag);
   __syncthreads();
   const size_t base = (size_t)bh * T * D;
   const size_t rows = ((size_t)bh * ntile + kb) * kTile;  // first row in the padded [., D] arrays
-  constexpr int CPR = D / 8;
+  bool bad = false;
   for (int e = threadIdx.x; e < kTile * CPR; e += kThreads) {
     const int i = e / CPR, c8 = (e % CPR) * 8;
     const bool live = k0 + i < T;
-    bf16x8 vx = {}, hi, lo;
-    if (live) vx = *reinterpret_cast<const bf16x8*>(V + base + (size_t)(k0 + i) * D + c8);
+    const size_t at = base + (size_t)(k0 + i) * D + c8;
+    bf16x8 vx = {}, hi, lo, whi, wlo;
+    f32x4 g4[2] = {}, f4[2] = {};
+    if (live) {
+      vx = *reinterpret_cast<const bf16x8*>(V + at);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        g4[k] = *reinterpret_cast<const f32x4*>(G + at + 4 * k);
+        f4[k] = *reinterpret_cast<const f32x4*>(F + at + 4 * k);
+      }
+    }
+    float cs = 0.f;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int j = c8 + u;
+      const bool sp = split[j] != 0.f;
       float y = 0.f;
       if (live) {
-        const float x = fmaf(bl[j], (float)vx[u], -c[j]);
-        y = split[j] != 0.f ? expm1f(x * kLn2) : exp2_hw(x);
+        const float xv = fmaf(bl[j], (float)vx[u], -c[j]);
+        y = sp ? expm1f(xv * kLn2) : exp2_hw(xv);
       }
       bf16 a, b;
       split_bf16(y, a, b);
       hi[u] = a;
       lo[u] = b;
+      const float w = g4[u >> 2][u & 3] / beta[h * D + j];
+      const float x = live ? c[j] - bl[j] * f4[u >> 2][u & 3] : 0.f;  // log2 U
+      const float wu = w * exp2_hw(fminf(x, kGuardU));
+      if (!(x <= kGuardU && fabsf(wu) < kGuardW)) bad = true;
+      cs += sp ? w * expm1f(x * kLn2) : -w;
+      split_bf16(wu, a, b);
+      whi[u] = a;
+      wlo[u] = b;
     }
-    *reinterpret_cast<bf16x8*>(yh + (rows + i) * D + c8) = hi;
-    *reinterpret_cast<bf16x8*>(yl + (rows + i) * D + c8) = lo;
+    const size_t o = (rows + i) * D + c8;
+    *reinterpret_cast<bf16x8*>(yh + o) = hi;
+    *reinterpret_cast<bf16x8*>(yl + o) = lo;
+    *reinterpret_cast<bf16x8*>(wh + o) = whi;
+    *reinterpret_cast<bf16x8*>(wl + o) = wlo;
+#pragma unroll
+    for (int m = 1; m < CPR; m <<= 1) cs += __shfl_xor(cs, m);
+    if (e % CPR == 0) cst[rows + i] = cs;
   }
+  if (bad) flag[0] = 1;
 }
 
 // q kernel, matrix-core form.  Wave (kh = w >> 1, qh = w & 1) owns the
-// S^T block (keys kh*32.., queries qh*32..) of each tile pair.
+// S^T block (keys kh*32.., queries qh*32..) of each tile pair; its query
+// rows' operands (Q and W U hi / lo as MFMA B fragments), row constant and
+// log-normaliser stay in registers.
 template <int D>
 struct QFast {
-  using C = Bw<D>;
-  bf16 key[2][3][kTile * D];                      // [buffer][K, Y hi, Y lo], swizzled [key][d or j]
-  bf16 qt[kTile * C::ROW];                        // Q [query][d]
-  bf16 wuh[kTile * C::ROW], wul[kTile * C::ROW];  // W U [query][j]
-  float cst[kTile], lse2[kTile], c[D], split[D], bl[D], pt[2][kTile];
+  bf16 key[2][3][kTile * D];  // [buffer][K, Y hi, Y lo], swizzled [key][d or j]
+  float pt[2][kTile];         // row sums of p from the two key halves
 };
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ K, const float* __restrict__ beta,
-    const float* __restrict__ F, const float* __restrict__ lse, const float* __restrict__ G,
-    const float* __restrict__ cg, const float* __restrict__ splitf, const bf16* __restrict__ yh,
-    const bf16* __restrict__ yl, float* __restrict__ dQ, float* __restrict__ gf,
-    float* __restrict__ lnz, float* __restrict__ lse_p, int* __restrict__ flag, int H, int T,
-    int ntile) {
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const float* __restrict__ lse,
+    const bf16* __restrict__ yh, const bf16* __restrict__ yl, const bf16* __restrict__ wh,
+    const bf16* __restrict__ wl, const float* __restrict__ cst, float* __restrict__ dQ,
+    float* __restrict__ sap, float* __restrict__ lse_p, int H, int T, int ntile) {
   using C = Bw<D>;
   constexpr int NB = C::NCB;
   __shared__ __align__(16) QFast<D> sm;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
   const int lb = xcd_order(blockIdx.x, gridDim.x);
-  const int qb = ntile - 1 - lb % ntile, bh = lb / ntile, h = bh % H;
+  const int qb = ntile - 1 - lb % ntile, bh = lb / ntile;
   const int q0 = qb * kTile;
   const size_t base = (size_t)bh * T * D;
   const size_t rows0 = (size_t)bh * ntile * kTile;
@@ -740,42 +776,30 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
   };
   fetch(0);
 
-  for (int j = tid; j < D; j += kThreads) {
-    sm.bl[j] = beta[h * D + j] * kLog2e;
-    sm.split[j] = splitf[bh * D + j];
-    sm.c[j] = cg[bh * D + j];
-  }
-  if (tid < kTile) sm.lse2[tid] = q0 + tid < T ? lse[(size_t)bh * T + q0 + tid] * kLog2e : 0.f;
-  stage_tile<D>(Q + base, q0, T, sm.qt, nullptr);
-  __syncthreads();
-  // W U and the row constants sum_j (split ? W (U - 1) : -W); thread (row
-  // tid >> 2, channel quarter tid & 3)
-  bool bad = false;
+  const int t = qh * 32 + n;
+  // this wave's query rows as MFMA B fragments: Q (for S^T; rows past T
+  // re-read row T - 1, their p is masked) and W U hi / lo (for dP^T, zero
+  // past T), loop-invariant
+  bf16x8 qf[C::NKS], wf[C::NKS][2];
   {
-    const int t = tid >> 2, j0 = (tid & 3) * (D / 4);
-    const bool live = q0 + t < T;
-    float cs = 0.f;
-    for (int u = 0; u < D / 4; u += 4) {
-      f32x4 g4 = {}, f4 = {};
-      if (live) {
-        g4 = *reinterpret_cast<const f32x4*>(G + base + (size_t)(q0 + t) * D + j0 + u);
-        f4 = *reinterpret_cast<const f32x4*>(F + base + (size_t)(q0 + t) * D + j0 + u);
-      }
+    const size_t qr = base + (size_t)min(q0 + t, T - 1) * D, wr = (rows0 + q0 + t) * D;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int j = j0 + u + v;
-        const float w = g4[v] / beta[h * D + j];
-        const float x = live ? sm.c[j] - sm.bl[j] * f4[v] : 0.f;
-        const float wu = w * exp2_hw(fminf(x, kGuardU));
-        if (!(x <= kGuardU && fabsf(wu) < kGuardW)) bad = true;
-        cs += sm.split[j] != 0.f ? w * expm1f(x * kLn2) : -w;
-        split_bf16(wu, sm.wuh[t * C::ROW + j], sm.wul[t * C::ROW + j]);
-      }
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      qf[ks] = *reinterpret_cast<const bf16x8*>(Q + qr + ks * 16 + hl * 8);
+      wf[ks][0] = *reinterpret_cast<const bf16x8*>(wh + wr + ks * 16 + hl * 8);
+      wf[ks][1] = *reinterpret_cast<const bf16x8*>(wl + wr + ks * 16 + hl * 8);
     }
-    cs += __shfl_xor(cs, 1);
-    cs += __shfl_xor(cs, 2);
-    if ((tid & 3) == 0) sm.cst[t] = cs;
   }
+  const float ct = cst[rows0 + q0 + t];
+  const float l2 = q0 + t < T ? lse[(size_t)bh * T + q0 + t] * kLog2e : 0.f;
+#pragma unroll
+  for (int ks = 0; ks < C::NKS; ++ks) {
+    settle(qf[ks]);
+    settle(wf[ks][0]);
+    settle(wf[ks][1]);
+  }
+  settle(ct);
+  settle(l2);
 
   f32x16 dqt[NB], sat[NB];  // (d or j block) x queries qh*32.., partial over this wave's keys
 #pragma unroll
@@ -785,18 +809,6 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
   }
   float psum = 0.f;
   const float scale2 = kLog2e / sqrtf((float)D);
-  const int t = qh * 32 + n;
-  __syncthreads();  // Q, W U and the row constants are in LDS
-  // this wave's query rows as MFMA B fragments: Q (for S^T) and W U hi / lo
-  // (for dP^T), loop-invariant
-  bf16x8 qf[C::NKS], wf[C::NKS][2];
-#pragma unroll
-  for (int ks = 0; ks < C::NKS; ++ks) {
-    const int bo = t * C::ROW + ks * 16 + hl * 8;
-    qf[ks] = *reinterpret_cast<const bf16x8*>(sm.qt + bo);
-    wf[ks][0] = *reinterpret_cast<const bf16x8*>(sm.wuh + bo);
-    wf[ks][1] = *reinterpret_cast<const bf16x8*>(sm.wul + bo);
-  }
   // dQ^T(d block, queries) += K^T dS^T ;  SA^T(j block, queries) += Y^T P^T
   // for tile kb: the transposed operands come from transposing LDS reads
   bf16x8 ph[2], pl[2], dsb[2];
@@ -804,18 +816,27 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
     const bf16* kt = &sm.key[kb & 1][0][0];
     const bf16* ty = kt + kTile * D;
     const bf16* tyl = ty + kTile * D;
+    // groups g = (b, k2), their three transposed fragments read two groups ahead
+    constexpr int NG = 2 * NB;
+    bf16x8 ring[3][3];
+    auto load_group = [&](int g, bf16x8* f) {
+      const int b = g >> 1, p0 = kh * 32 + (g & 1) * 16;
+      f[0] = frag_tr<D>(kt, b * 32, p0);
+      f[1] = frag_tr<D>(ty, b * 32, p0);
+      f[2] = frag_tr<D>(tyl, b * 32, p0);
+    };
+    load_group(0, ring[0]);
+    if (NG > 1) load_group(1, ring[1]);
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const int p0 = kh * 32 + k2 * 16;
-        dqt[b] = mfma(frag_tr<D>(kt, b * 32, p0), dsb[k2], dqt[b]);
-        const bf16x8 yh8 = frag_tr<D>(ty, b * 32, p0);
-        const bf16x8 yl8 = frag_tr<D>(tyl, b * 32, p0);
-        sat[b] = mfma(yh8, ph[k2], sat[b]);
-        sat[b] = mfma(yl8, ph[k2], sat[b]);
-        sat[b] = mfma(yh8, pl[k2], sat[b]);
-      }
+    for (int g = 0; g < NG; ++g) {
+      if (g + 2 < NG) load_group(g + 2, ring[(g + 2) % 3]);
+      const bf16x8* f = ring[g % 3];
+      const int b = g >> 1, k2 = g & 1;
+      dqt[b] = mfma(f[0], dsb[k2], dqt[b]);
+      sat[b] = mfma(f[1], ph[k2], sat[b]);
+      sat[b] = mfma(f[2], ph[k2], sat[b]);
+      sat[b] = mfma(f[1], pl[k2], sat[b]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   // Per iteration: tile kb's loads have landed and every wave is done with
@@ -830,12 +851,13 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
     const bf16* tyl = ty + kTile * D;  // Y lo
 
     // S^T (keys x queries) then dP^T = Y (W U)^T over j: 2 NKS steps whose
-    // key-side fragments are read two steps ahead (scheduling barriers keep
-    // the order, so each MFMA waits only for reads issued two steps before);
+    // key-side fragments are read four steps ahead (scheduling barriers keep
+    // the order, so each MFMA waits only for reads issued four steps before);
     // the query-side fragments stay in registers for the whole loop
     f32x16 s = {}, dp = {};
     {
-      bf16x8 ring[3][2];
+      constexpr int LA = 4;  // steps of lookahead
+      bf16x8 ring[LA + 1][2];
       auto load_step = [&](int k, bf16x8* f) {
         if (k < C::NKS) {
           f[0] = frag_rows<D>(kt, kh * 32 + n, 2 * k + hl);
@@ -845,12 +867,12 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
           f[1] = frag_rows<D>(tyl, kh * 32 + n, 2 * ks + hl);
         }
       };
-      load_step(0, ring[0]);
-      load_step(1, ring[1]);
+#pragma unroll
+      for (int k = 0; k < LA; ++k) load_step(k, ring[k]);
 #pragma unroll
       for (int k = 0; k < 2 * C::NKS; ++k) {
-        if (k + 2 < 2 * C::NKS) load_step(k + 2, ring[(k + 2) % 3]);
-        const bf16x8* f = ring[k % 3];
+        if (k + LA < 2 * C::NKS) load_step(k + LA, ring[(k + LA) % (LA + 1)]);
+        const bf16x8* f = ring[k % (LA + 1)];
         if (k < C::NKS) {
           s = mfma(f[0], qf[k], s);
         } else {
@@ -862,9 +884,7 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    const float l2 = sm.lse2[t];
     const bool tlive = q0 + t < T;
-    const float ct = sm.cst[t];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int i = kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
@@ -879,86 +899,75 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
     }
     phase3(kb);
   }
-  if (bad) flag[0] = 1;
 
-  // ---- combine the key halves (waves kh = 0, 1 of the same qh) and both lane halves of P
+  // ---- epilogue.  The key halves (waves kh = 0, 1 of the same qh) meet in
+  // LDS as [64 queries][D + 1] totals of dQ^T and SA^T; then every thread
+  // takes (query, channel) elements with the channel fastest (coalesced
+  // global writes): dQ and SA / P.
   __syncthreads();
-  // [2 qh][2 sets][NB][16][64] fp32 and the [64 queries][D] G F terms, over the key buffers
-  float* red = reinterpret_cast<float*>(&sm.key[0][0][0]);
-  float* gfs = red + 4 * NB * 16 * 64;
-  static_assert((4 * C::NCB * 16 * 64 + kTile * D) * 4 <= sizeof(sm.key), "reduction area");
-  auto slot = [&](int set, int b, int r) { return (((qh * 2 + set) * NB + b) * 16 + r) * 64 + lane; };
+  constexpr int SR = D + 1;
+  float* dqs = reinterpret_cast<float*>(&sm.key[0][0][0]);  // [64][SR]
+  float* sas = dqs + kTile * SR;                             // [64][SR]
+  static_assert(2 * kTile * (D + 1) * 4 <= sizeof(sm.key), "epilogue area");
   psum += __shfl_xor(psum, 32);
   if (kh == 1) {
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        red[slot(0, b, r)] = dqt[b][r];
-        red[slot(1, b, r)] = sat[b][r];
+        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+        dqs[t * SR + row] = dqt[b][r];
+        sas[t * SR + row] = sat[b][r];
       }
-    if (hl == 0) sm.pt[1][qh * 32 + n] = psum;
+    if (hl == 0) sm.pt[1][t] = psum;
   } else if (hl == 0) {
-    sm.pt[0][qh * 32 + n] = psum;
+    sm.pt[0][t] = psum;
   }
   __syncthreads();
   if (kh == 0) {
-    const int tq = q0 + qh * 32 + n;
-    const float P = sm.pt[0][qh * 32 + n] + sm.pt[1][qh * 32 + n];
-    // p was formed from the forward's lse, whose sum of bf16-rounded terms
-    // may differ from the exact one by a few 2^-9: P = sum_i p rescales it
-    const float rs = 1.f / (sqrtf((float)D) * P);
-    if (hl == 0 && tq < T) lse_p[(size_t)bh * T + tq] = lse[(size_t)bh * T + tq] + logf(P);
-    bool under = false;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);  // d or j
-        const float sq = dqt[b][r] + red[slot(0, b, r)];
-        const float sa = sat[b][r] + red[slot(1, b, r)];
-        float term = 0.f;
-        if (tq < T) {
-          dQ[base + (size_t)tq * D + row] = sq * rs;
-          const float g = G[base + (size_t)tq * D + row], f = F[base + (size_t)tq * D + row];
-          const float x = sm.c[row] - sm.bl[row] * f;  // log2 U
-          float lz;                                     // ln(Z/P): F = F^ + ln(Z/P)/beta
-          if (sm.split[row] != 0.f) {
-            const float um1 = expm1f(x * kLn2);
-            lz = log1pf(um1 + (um1 + 1.f) * sa / P);
-          } else {
-            if (!(sa > 0x1p-120f * P)) under = true;
-            lz = x * kLn2 + logf(sa / P);
-          }
-          lnz[base + (size_t)tq * D + row] = lz;
-          term = g * (f + lz / beta[h * D + row]);
-        }
-        gfs[(qh * 32 + n) * D + row] = term;
+        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+        dqs[t * SR + row] += dqt[b][r];
+        sas[t * SR + row] += sat[b][r];
       }
-    }
-    if (under) flag[0] = 1;  // a plain channel's sum left fp32's range: exact pass
   }
   __syncthreads();
-  for (int j = tid; j < D; j += kThreads) {
-    float acc = 0.f;
-    for (int i = 0; i < kTile; ++i) acc += gfs[i * D + j];
-    gf[((size_t)bh * ntile + qb) * D + j] = acc;
+  {
+    // p was formed from the forward's lse, whose sum of bf16-rounded terms
+    // may differ from the exact one by a few 2^-9: P = sum_i p rescales it
+    const int j = tid % D;
+    const float rs = 1.f / sqrtf((float)D);
+    for (int r = tid / D; r < kTile && q0 + r < T; r += kThreads / D) {
+      const float rP = 1.f / (sm.pt[0][r] + sm.pt[1][r]);
+      const size_t at = base + (size_t)(q0 + r) * D + j;
+      dQ[at] = dqs[r * SR + j] * rs * rP;
+      sap[at] = sas[r * SR + j] * rP;
+    }
+    if (tid < kTile && q0 + tid < T)
+      lse_p[(size_t)bh * T + q0 + tid] =
+          lse[(size_t)bh * T + q0 + tid] + logf(sm.pt[0][tid] + sm.pt[1][tid]);
   }
 }
 
-// W U' row-major (hi and lo) for the kv pass, U' = U / (Z/P) normalising the
-// posterior, and the row constants sum_j (split ? W (U' - 1) : -W); zero past
-// T.  Thread e handles 8 channels of one row; the D/8 threads of a row are
-// adjacent lanes.
+// For the kv pass, per 64-query tile: ln(Z/P) per (t, j) from the q pass's
+// SA / P (split: log1p((U - 1) + U SA / P); plain: log2 U + log2(SA / P),
+// in nats), the normalised posterior's U' = U / (Z/P), W U' row-major (hi
+// and lo) and the row constants sum_j (split ? W (U' - 1) : -W), zero past T;
+// and the tile's partial sums of G (F^ + ln(Z/P) / beta) per channel, the
+// G F terms of dbeta.  Thread e handles 8 channels of one row; the D/8
+// threads of a row are adjacent lanes and keep their channels throughout.
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
     const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ G,
-    const float* __restrict__ lnz, const float* __restrict__ cg, const float* __restrict__ splitf,
-    bf16* __restrict__ wh, bf16* __restrict__ wl, float* __restrict__ cst,
+    const float* __restrict__ sap, const float* __restrict__ cg, const float* __restrict__ splitf,
+    bf16* __restrict__ wh, bf16* __restrict__ wl, float* __restrict__ cst, float* __restrict__ gf,
     int* __restrict__ flag, int H, int T, int ntile) {
-  __shared__ float c[D], split[D], bl[D];
-  constexpr int CPR = D / 8;
+  constexpr int CPR = D / 8, RG = kThreads / CPR;
   static_assert(kThreads % CPR == 0 && CPR <= 64, "a row's threads share a wave");
+  __shared__ float c[D], split[D], bl[D], part[RG][D];
   const int qb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
   const int q0 = qb * kTile;
   for (int j = threadIdx.x; j < D; j += kThreads) {
@@ -969,9 +978,11 @@ __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
   __syncthreads();
   const size_t base = (size_t)bh * T * D;
   const size_t rows = ((size_t)bh * ntile + qb) * kTile;
-  bool bad = false;
+  const int c8 = (threadIdx.x % CPR) * 8;
+  float gacc[8] = {};
+  bool bad = false, under = false;
   for (int e = threadIdx.x; e < kTile * CPR; e += kThreads) {
-    const int t = e / CPR, c8 = (e % CPR) * 8;
+    const int t = e / CPR;
     const bool live = q0 + t < T;
     const size_t at = base + (size_t)(q0 + t) * D + c8;
     bf16x8 hi, lo;
@@ -981,19 +992,32 @@ __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
       for (int k = 0; k < 2; ++k) {
         g4[k] = *reinterpret_cast<const f32x4*>(G + at + 4 * k);
         f4[k] = *reinterpret_cast<const f32x4*>(F + at + 4 * k);
-        z4[k] = *reinterpret_cast<const f32x4*>(lnz + at + 4 * k);
+        z4[k] = *reinterpret_cast<const f32x4*>(sap + at + 4 * k);
       }
     }
     float cs = 0.f;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int j = c8 + u;
-      const float w = g4[u >> 2][u & 3] / beta[h * D + j];
-      const float x = live ? c[j] - bl[j] * f4[u >> 2][u & 3] : 0.f;
-      const float xu = fminf(x, kGuardU) - z4[u >> 2][u & 3] * kLog2e;  // log2 U'
+      const bool sp = split[j] != 0.f;
+      const float g = g4[u >> 2][u & 3], f = f4[u >> 2][u & 3], sa = z4[u >> 2][u & 3];
+      const float rb = 1.f / beta[h * D + j], w = g * rb;
+      const float x = live ? c[j] - bl[j] * f : 0.f;  // log2 U
+      float lz = 0.f;                                 // ln(Z/P): F = F^ + ln(Z/P)/beta
+      if (live) {
+        if (sp) {
+          const float um1 = expm1f(x * kLn2);
+          lz = log1pf(um1 + (um1 + 1.f) * sa);
+        } else {
+          if (!(sa > 0x1p-120f)) under = true;
+          lz = (x + log2_hw(sa)) * kLn2;
+        }
+      }
+      gacc[u] += g * (f + lz * rb);
+      const float xu = fminf(x, kGuardU) - lz * kLog2e;  // log2 U'
       const float wu = w * exp2_hw(xu);
       if (!(x <= kGuardU && fabsf(wu) < kGuardW)) bad = true;
-      cs += split[j] != 0.f ? w * expm1f(xu * kLn2) : -w;
+      cs += sp ? w * expm1f(xu * kLn2) : -w;
       bf16 a, b;
       split_bf16(wu, a, b);
       hi[u] = a;
@@ -1002,30 +1026,36 @@ __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
     *reinterpret_cast<bf16x8*>(wh + (rows + t) * D + c8) = hi;
     *reinterpret_cast<bf16x8*>(wl + (rows + t) * D + c8) = lo;
 #pragma unroll
-    for (int o = 1; o < CPR; o <<= 1) cs += __shfl_xor(cs, o);
+    for (int m = 1; m < CPR; m <<= 1) cs += __shfl_xor(cs, m);
     if (e % CPR == 0) cst[rows + t] = cs;
   }
-  if (bad) flag[0] = 1;
+  if (bad || under) flag[0] = 1;  // a factor or a plain channel's sum left fp32's range
+#pragma unroll
+  for (int u = 0; u < 8; ++u) part[threadIdx.x / CPR][c8 + u] = gacc[u];
+  __syncthreads();
+  for (int j = threadIdx.x; j < D; j += kThreads) {
+    float acc = 0.f;
+    for (int g = 0; g < RG; ++g) acc += part[g][j];
+    gf[((size_t)bh * ntile + qb) * D + j] = acc;
+  }
 }
 
 // kv kernel, matrix-core form.  Wave (qh = w >> 1, kh = w & 1) owns the
-// 32 x 32 block (queries qh*32.., keys kh*32..) of each tile pair.
+// 32 x 32 block (queries qh*32.., keys kh*32..) of each tile pair; its key
+// rows' operands (K and Y hi / lo as MFMA B fragments) stay in registers.
 template <int D>
 struct KvFast {
-  using C = Bw<D>;
-  bf16 qry[2][3][kTile * D];                    // [buffer][Q, W U' hi, W U' lo], swizzled [query][d or j]
-  bf16 kt[kTile * C::ROW];                      // K [key][d]
-  bf16 yh[kTile * C::ROW], yl[kTile * C::ROW];  // Y [key][j]
-  float cst[2][kTile], lse[2][kTile], c[D], split[D], bl[D];
+  bf16 qry[2][3][kTile * D];  // [buffer][Q, W U' hi, W U' lo], swizzled [query][d or j]
+  float cst[2][kTile], lse[2][kTile], c[D], bl[D];
 };
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ beta, const float* __restrict__ lse, const float* __restrict__ cg,
-    const float* __restrict__ splitf, const bf16* __restrict__ wh, const bf16* __restrict__ wl,
-    const float* __restrict__ cst, float* __restrict__ dK, float* __restrict__ dV,
-    float* __restrict__ vdv, int H, int T, int ntile) {
+    const bf16* __restrict__ yh, const bf16* __restrict__ yl, const bf16* __restrict__ wh,
+    const bf16* __restrict__ wl, const float* __restrict__ cst, float* __restrict__ dK,
+    float* __restrict__ dV, float* __restrict__ vdv, int H, int T, int ntile) {
   using C = Bw<D>;
   constexpr int NB = C::NCB;  // 32-row blocks of d (and of j)
   __shared__ __align__(16) KvFast<D> sm;
@@ -1050,33 +1080,26 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
 
   for (int j = tid; j < D; j += kThreads) {
     sm.bl[j] = beta[h * D + j] * kLog2e;
-    sm.split[j] = splitf[bh * D + j];
     sm.c[j] = cg[bh * D + j];
   }
-  stage_tile<D>(K + base, k0, T, sm.kt, nullptr);
-  __syncthreads();
-  // Y of this key tile (the q pass's rows of it, recomputed from V)
+  const int i = kh * 32 + n;
+  // this wave's key rows as MFMA B fragments: K (for S; rows past T re-read
+  // row T - 1, their p is masked) and Y hi / lo (for dP, zero past T),
+  // loop-invariant
+  bf16x8 kf[C::NKS], yf[C::NKS][2];
   {
-    constexpr int CPR = D / 8;
-    for (int e = tid; e < kTile * CPR; e += kThreads) {
-      const int i = e / CPR, c8 = (e % CPR) * 8;
-      bf16x8 vx = {}, hi, lo;
-      if (k0 + i < T) vx = *reinterpret_cast<const bf16x8*>(V + base + (size_t)(k0 + i) * D + c8);
+    const size_t kr = base + (size_t)min(k0 + i, T - 1) * D, yr = (rows0 + k0 + i) * D;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = c8 + u;
-        float y = 0.f;
-        if (k0 + i < T) {
-          const float x = fmaf(sm.bl[j], (float)vx[u], -sm.c[j]);
-          y = sm.split[j] != 0.f ? expm1f(x * kLn2) : exp2_hw(x);
-        }
-        bf16 a, b;
-        split_bf16(y, a, b);
-        hi[u] = a;
-        lo[u] = b;
-      }
-      *reinterpret_cast<bf16x8*>(sm.yh + i * C::ROW + c8) = hi;
-      *reinterpret_cast<bf16x8*>(sm.yl + i * C::ROW + c8) = lo;
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      kf[ks] = *reinterpret_cast<const bf16x8*>(K + kr + ks * 16 + hl * 8);
+      yf[ks][0] = *reinterpret_cast<const bf16x8*>(yh + yr + ks * 16 + hl * 8);
+      yf[ks][1] = *reinterpret_cast<const bf16x8*>(yl + yr + ks * 16 + hl * 8);
+    }
+#pragma unroll
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      settle(kf[ks]);
+      settle(yf[ks][0]);
+      settle(yf[ks][1]);
     }
   }
 
@@ -1088,18 +1111,6 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
   }
   const float scale2 = kLog2e / sqrtf((float)D);
   const int qlast = (T - 1) / kTile;
-  const int i = kh * 32 + n;
-  __syncthreads();
-  // this wave's key rows as MFMA B fragments: K (for S) and Y hi / lo (for
-  // dP), loop-invariant
-  bf16x8 kf[C::NKS], yf[C::NKS][2];
-#pragma unroll
-  for (int ks = 0; ks < C::NKS; ++ks) {
-    const int bo = i * C::ROW + ks * 16 + hl * 8;
-    kf[ks] = *reinterpret_cast<const bf16x8*>(sm.kt + bo);
-    yf[ks][0] = *reinterpret_cast<const bf16x8*>(sm.yh + bo);
-    yf[ks][1] = *reinterpret_cast<const bf16x8*>(sm.yl + bo);
-  }
   // dV^T(j block, keys) += (W U')^T P ;  dK^T(d block, keys) += Q^T dS for
   // query tile qb: the transposed operands come from transposing LDS reads
   bf16x8 ph[2], pl[2], dsb[2];
@@ -1107,18 +1118,27 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
     const bf16* tq = &sm.qry[qb & 1][0][0];
     const bf16* tw = tq + kTile * D;
     const bf16* twl = tw + kTile * D;
+    // groups g = (b, k2), their three transposed fragments read two groups ahead
+    constexpr int NG = 2 * NB;
+    bf16x8 ring[3][3];
+    auto load_group = [&](int g, bf16x8* f) {
+      const int b = g >> 1, p0 = qh * 32 + (g & 1) * 16;
+      f[0] = frag_tr<D>(tw, b * 32, p0);
+      f[1] = frag_tr<D>(twl, b * 32, p0);
+      f[2] = frag_tr<D>(tq, b * 32, p0);
+    };
+    load_group(0, ring[0]);
+    if (NG > 1) load_group(1, ring[1]);
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const int p0 = qh * 32 + k2 * 16;
-        const bf16x8 gh = frag_tr<D>(tw, b * 32, p0);
-        const bf16x8 gl = frag_tr<D>(twl, b * 32, p0);
-        dvt[b] = mfma(gh, ph[k2], dvt[b]);
-        dvt[b] = mfma(gl, ph[k2], dvt[b]);
-        dvt[b] = mfma(gh, pl[k2], dvt[b]);
-        dkt[b] = mfma(frag_tr<D>(tq, b * 32, p0), dsb[k2], dkt[b]);
-      }
+    for (int g = 0; g < NG; ++g) {
+      if (g + 2 < NG) load_group(g + 2, ring[(g + 2) % 3]);
+      const bf16x8* f = ring[g % 3];
+      const int b = g >> 1, k2 = g & 1;
+      dvt[b] = mfma(f[0], ph[k2], dvt[b]);
+      dvt[b] = mfma(f[1], ph[k2], dvt[b]);
+      dvt[b] = mfma(f[0], pl[k2], dvt[b]);
+      dkt[b] = mfma(f[2], dsb[k2], dkt[b]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   // Per iteration: query tile qb's loads have landed and every wave is done
@@ -1135,11 +1155,12 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
     const float* cq = sm.cst[qb & 1];
 
     // S (queries x keys) then dP = (W U') Y^T over j: 2 NKS steps whose
-    // query-side fragments are read two steps ahead (scheduling barriers
+    // query-side fragments are read four steps ahead (scheduling barriers
     // keep the order); the key-side fragments stay in registers
     f32x16 s = {}, dp = {};
     {
-      bf16x8 ring[3][2];
+      constexpr int LA = 4;  // steps of lookahead
+      bf16x8 ring[LA + 1][2];
       auto load_step = [&](int k, bf16x8* f) {
         if (k < C::NKS) {
           f[0] = frag_rows<D>(tq, qh * 32 + n, 2 * k + hl);
@@ -1149,12 +1170,12 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
           f[1] = frag_rows<D>(twl, qh * 32 + n, 2 * ks + hl);
         }
       };
-      load_step(0, ring[0]);
-      load_step(1, ring[1]);
+#pragma unroll
+      for (int k = 0; k < LA; ++k) load_step(k, ring[k]);
 #pragma unroll
       for (int k = 0; k < 2 * C::NKS; ++k) {
-        if (k + 2 < 2 * C::NKS) load_step(k + 2, ring[(k + 2) % 3]);
-        const bf16x8* f = ring[k % 3];
+        if (k + LA < 2 * C::NKS) load_step(k + LA, ring[(k + LA) % (LA + 1)]);
+        const bf16x8* f = ring[k % (LA + 1)];
         if (k < C::NKS) {
           s = mfma(f[0], kf[k], s);
         } else {
@@ -1182,51 +1203,59 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
     phase3(qb);
   }
 
-  // ---- combine the two query halves (waves qh = 0, 1 of the same kh)
+  // ---- epilogue.  The query halves (waves qh = 0, 1 of the same kh) meet
+  // in LDS as [64 keys][D + 1] totals of dV^T and dK^T; then every thread
+  // takes (key, channel) elements with the channel fastest (coalesced global
+  // access).  Thread tid keeps channel tid % D throughout.
   __syncthreads();
-  // [2 kh][2 sets][NB][16][64] fp32 and the [64 keys][D] v dV terms, over the query buffers
-  float* red = reinterpret_cast<float*>(&sm.qry[0][0][0]);
-  float* vdvs = red + 4 * NB * 16 * 64;
-  static_assert((4 * C::NCB * 16 * 64 + kTile * D) * 4 <= sizeof(sm.qry), "reduction area");
-  auto slot = [&](int set, int b, int r) { return (((kh * 2 + set) * NB + b) * 16 + r) * 64 + lane; };
+  constexpr int SR = D + 1;
+  float* dvs = reinterpret_cast<float*>(&sm.qry[0][0][0]);  // [64][SR]
+  float* dks = dvs + kTile * SR;                             // [64][SR]
+  float* vpart = dks + kTile * SR;                           // [kThreads]
+  static_assert((2 * kTile * (D + 1) + kThreads) * 4 <= sizeof(sm.qry), "epilogue area");
   if (qh == 1) {
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        red[slot(0, b, r)] = dvt[b][r];
-        red[slot(1, b, r)] = dkt[b][r];
+        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+        dvs[i * SR + row] = dvt[b][r];
+        dks[i * SR + row] = dkt[b][r];
       }
   }
   __syncthreads();
   if (qh == 0) {
-    const float rs = 1.f / sqrtf((float)D);
-    const int key = k0 + i;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);  // j or d
-        const float sv = dvt[b][r] + red[slot(0, b, r)];
-        const float sk = dkt[b][r] + red[slot(1, b, r)];
-        float dvv = 0.f;
-        if (key < T) {
-          const float vv = (float)V[base + (size_t)key * D + row];
-          const float E = exp2_hw(fmaf(sm.bl[row], vv, -sm.c[row]));
-          dvv = E * beta[h * D + row] * sv;
-          dV[base + (size_t)key * D + row] = dvv;
-          dK[base + (size_t)key * D + row] = sk * rs;
-          dvv *= vv;
-        }
-        vdvs[i * D + row] = dvv;
+        const int row = b * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+        dvs[i * SR + row] += dvt[b][r];
+        dks[i * SR + row] += dkt[b][r];
       }
-    }
   }
   __syncthreads();
-  for (int j = tid; j < D; j += kThreads) {
+  {
+    const int j = tid % D;
+    const float cj = sm.c[j], blj = sm.bl[j], bj = beta[h * D + j];
+    const float rs = 1.f / sqrtf((float)D);
+    float vacc = 0.f;
+    for (int r = tid / D; r < kTile && k0 + r < T; r += kThreads / D) {
+      const size_t at = base + (size_t)(k0 + r) * D + j;
+      const float vv = (float)V[at];
+      // dV = beta E sum_t p (W U'), E = 2^{bl v - c}
+      const float dvv = exp2_hw(fmaf(blj, vv, -cj)) * bj * dvs[r * SR + j];
+      dV[at] = dvv;
+      dK[at] = dks[r * SR + j] * rs;
+      vacc += dvv * vv;
+    }
+    vpart[tid] = vacc;
+  }
+  __syncthreads();
+  if (tid < D) {
     float acc = 0.f;
-    for (int k = 0; k < kTile; ++k) acc += vdvs[k * D + j];
-    vdv[((size_t)bh * ntile + kb) * D + j] = acc;
+    for (int g = 0; g < kThreads / D; ++g) acc += vpart[g * D + tid];
+    vdv[((size_t)bh * ntile + kb) * D + tid] = acc;
   }
 }
 
@@ -1269,16 +1298,16 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   const bf16* k = reinterpret_cast<const bf16*>(K);
   const bf16* v = reinterpret_cast<const bf16*>(V);
   // workspace (fp32 unless noted): flag | lse renormalised by the q pass
-  // [nbh T] | c, split [nbh D] |
-  // V max, V min, vdv, gf, exact partials [nbh ntile D] | ln(Z/P) [nbh T D] |
-  // row constants [nbh Tp] | two bf16 operand arrays [nbh Tp D], Tp = 64 ntile
-  // (Y hi and lo for the q pass, then W U' hi and lo for the kv pass)
+  // [nbh T] | c, split [nbh D] | V max, V min, vdv, gf, exact partials
+  // [nbh ntile D] | SA / P [nbh T D] | row constants [nbh Tp] | four bf16
+  // operand arrays [nbh Tp D], Tp = 64 ntile: Y hi, Y lo, and W U hi, lo
+  // (the q pass's, then the kv pass's W U')
   const size_t tp = (size_t)ntile * kTile;
   const size_t nl = (size_t)nbh * T, nc = (size_t)nbh * D, np = (size_t)nbh * ntile * D;
   const size_t nz = (size_t)nbh * T * D, nr = (size_t)nbh * tp, no = (size_t)nbh * tp * D;
   const size_t fl = nl + 2 * nc + 5 * np + nz + nr;
   const size_t fbytes = (fl * sizeof(float) + 255) & ~(size_t)255;
-  const size_t bytes = 256 + fbytes + 2 * no * sizeof(bf16);
+  const size_t bytes = 256 + fbytes + 4 * no * sizeof(bf16);
   char* ws = nullptr;
   hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
   if (e != hipSuccess) return e;
@@ -1291,31 +1320,33 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   float* vdv = vmn + np;
   float* gfp = vdv + np;
   float* exact = gfp + np;
-  float* lnz = exact + np;
-  float* cst = lnz + nz;
-  bf16* o0 = reinterpret_cast<bf16*>(ws + 256 + fbytes);
-  bf16* o1 = o0 + no;
+  float* sap = exact + np;
+  float* cst = sap + nz;
+  bf16* yh = reinterpret_cast<bf16*>(ws + 256 + fbytes);
+  bf16* yl = yh + no;
+  bf16* wh = yl + no;
+  bf16* wl = wh + no;
   const dim3 grid((unsigned)(nbh * ntile)), blk(kThreads);
   hipLaunchKernelGGL(bwd_vstats_kernel<D>, grid, blk, 0, stream, v, vmx, vmn, flag, T, ntile);
   e = hipGetLastError();
-  if (e == hipSuccess) {  // key side: Y
-    hipLaunchKernelGGL(bwd_prepk_kernel<D>, grid, blk, 0, stream, v, beta, vmx, vmn, cg, splitf, o0,
-                       o1, flag, H, T, ntile);
+  if (e == hipSuccess) {  // channel constants; Y (key side) and the q pass's W U
+    hipLaunchKernelGGL(bwd_prepk_kernel<D>, grid, blk, 0, stream, v, beta, out, dout, vmx, vmn, cg,
+                       splitf, yh, yl, wh, wl, cst, flag, H, T, ntile);
     e = hipGetLastError();
   }
-  if (e == hipSuccess) {  // the q pass first: it forms ln(Z/P), which the kv pass uses
-    hipLaunchKernelGGL(bwd_q_fast_kernel<D>, grid, blk, 0, stream, q, k, beta, out, lse_fwd, dout,
-                       cg, splitf, o0, o1, dQ, gfp, lnz, lse, flag, H, T, ntile);
+  if (e == hipSuccess) {  // the q pass first: its SA / P give ln(Z/P), which the kv pass uses
+    hipLaunchKernelGGL(bwd_q_fast_kernel<D>, grid, blk, 0, stream, q, k, lse_fwd, yh, yl, wh, wl,
+                       cst, dQ, sap, lse, H, T, ntile);
     e = hipGetLastError();
   }
-  if (e == hipSuccess) {  // query side: W U' over the same memory
-    hipLaunchKernelGGL(bwd_prepq_kernel<D>, grid, blk, 0, stream, beta, out, dout, lnz, cg, splitf,
-                       o0, o1, cst, flag, H, T, ntile);
+  if (e == hipSuccess) {  // ln(Z/P), the kv pass's W U' and row constants, the G F sums
+    hipLaunchKernelGGL(bwd_prepq_kernel<D>, grid, blk, 0, stream, beta, out, dout, sap, cg, splitf,
+                       wh, wl, cst, gfp, flag, H, T, ntile);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(bwd_kv_fast_kernel<D>, grid, blk, 0, stream, q, k, v, beta, lse, cg, splitf,
-                       o0, o1, cst, dK, dV, vdv, H, T, ntile);
+    hipLaunchKernelGGL(bwd_kv_fast_kernel<D>, grid, blk, 0, stream, q, k, v, beta, lse, cg, yh, yl,
+                       wh, wl, cst, dK, dV, vdv, H, T, ntile);
     e = hipGetLastError();
   }
   // exact element-wise passes: they return at once unless a block raised the flag
