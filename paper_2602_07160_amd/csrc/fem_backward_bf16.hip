@@ -522,29 +522,6 @@ __device__ __forceinline__ int swz_off(int row, int chunk) {  // byte offset
   return row * D * 2 + ((chunk ^ swz<D>(row)) << 4);
 }
 
-// LDS byte address of a generic pointer into shared memory.
-__device__ __forceinline__ unsigned lds_addr(const void* p) {
-  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
-}
-
-// Direct global -> LDS loads (lane l's bytes land at dst + l * size; dst is
-// the same for the whole wave).  Issued as inline assembly so the compiler
-// does not see an LDS write in flight: it would otherwise wait for the whole
-// load queue before every LDS read of the other buffer.  Completion is waited
-// for explicitly (wait_vmem) before the barrier that publishes the buffer.
-__device__ __forceinline__ void dma16(const void* src, void* dst) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
-               : "memory", "m0");
-}
-__device__ __forceinline__ void dma4(const void* src, void* dst) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
-               :
-               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
-               : "memory", "m0");
-}
-
 // Direct global -> LDS copy of rows [0, 64) of a row-major [., D] bf16 source
 // into a swizzled tile; rows past lim re-read row lim (their keys or queries
 // are masked).  Wave w fills the 1 KiB blocks w, w + 4, ...: lane l of block

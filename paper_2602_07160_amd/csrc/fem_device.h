@@ -52,6 +52,31 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// LDS byte address of a generic pointer into shared memory.
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// Direct global -> LDS loads (lane l's bytes land at dst + l * size; dst is
+// the same for the whole wave).  Issued as inline assembly so the compiler
+// does not see an LDS write in flight: with one in flight it treats LDS
+// reads as completing out of order (every read then waits for all earlier
+// ones) and waits for the whole load queue before transposing reads.  The
+// caller waits for completion explicitly (s_waitcnt vmcnt(0)) before the
+// barrier that publishes the buffer.
+__device__ __forceinline__ void dma16(const void* src, void* dst) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const void* src, void* dst) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
+               : "memory", "m0");
+}
+
 // Streaming log2-sum-exp2 accumulator: value = m + log2(s).
 struct Lse2 {
   float m = -INFINITY;

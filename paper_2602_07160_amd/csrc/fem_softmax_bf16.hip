@@ -425,7 +425,7 @@ __device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned
   for (int u = 0; u < BPW; ++u) {
     const int blk = wave + NW * u;
     if (BLOCKS % NW == 0 || blk < BLOCKS)
-      __builtin_amdgcn_global_load_lds(base + off[u], dst + blk * 1024, 16, 0, 0);
+      dma16(base + off[u], dst + blk * 1024);
   }
 }
 
