@@ -47,6 +47,7 @@
 #include "fem_internal.h"
 
 #include <cstddef>
+#include <type_traits>
 #include <mutex>
 
 namespace fem {
@@ -486,6 +487,33 @@ __device__ __forceinline__ void split_bf16(float x, bf16& hi, bf16& lo) {
   lo = (bf16)(x - (float)hi);
 }
 
+// p and dS of a 32 x 32 block as MFMA B operands (k = the accumulator's
+// rows): hi / lo parts of p and bf16 dS, two values per conversion.
+// pc(r) gives accumulator row r's p and row constant c_r; dS = p (dP + c_r).
+template <class PC>
+__device__ __forceinline__ void pack_p_ds(PC&& pc, const f32x16& dp, bf16x8 (&ph)[2],
+                                          bf16x8 (&pl)[2], bf16x8 (&ds)[2]) {
+  typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
+  u32x4 h[2], l[2], d[2];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const f32x2 x = pc(2 * k), y = pc(2 * k + 1);  // (p, c)
+    const float a = x[0], b = y[0];
+    const unsigned hu = __builtin_bit_cast(unsigned, to_bf16x2(a, b));
+    const float ha = __uint_as_float(hu << 16), hb = __uint_as_float(hu & 0xffff0000u);
+    h[k >> 2][k & 3] = hu;
+    l[k >> 2][k & 3] = __builtin_bit_cast(unsigned, to_bf16x2(a - ha, b - hb));
+    d[k >> 2][k & 3] = __builtin_bit_cast(
+        unsigned, to_bf16x2(a * (dp[2 * k] + x[1]), b * (dp[2 * k + 1] + y[1])));
+  }
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    ph[g] = __builtin_bit_cast(bf16x8, h[g]);
+    pl[g] = __builtin_bit_cast(bf16x8, l[g]);
+    ds[g] = __builtin_bit_cast(bf16x8, d[g]);
+  }
+}
+
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -724,7 +752,7 @@ __global__ __launch_bounds__(kThreads) void bwd_prepk_kernel(
 // log-normaliser stay in registers.
 template <int D>
 struct QFast {
-  bf16 key[2][3][kTile * D];  // [buffer][K, Y hi, Y lo], swizzled [key][d or j]
+  bf16 key[3][3][kTile * D];  // [buffer][K, Y hi, Y lo], swizzled [key][d or j]
   float pt[2][kTile];         // row sums of p from the two key halves
 };
 
@@ -746,7 +774,7 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
   const int kh = wave >> 1, qh = wave & 1;
   auto fetch = [&](int kb) {
     const int k0 = kb * kTile;
-    bf16* dst = &sm.key[kb & 1][0][0];
+    bf16* dst = &sm.key[kb % 3][0][0];
     load_swz<D>(K + base + (size_t)k0 * D, dst, T - 1 - k0);
     load_swz<D>(yh + (rows0 + k0) * D, dst + kTile * D, kTile - 1);
     load_swz<D>(yl + (rows0 + k0) * D, dst + 2 * kTile * D, kTile - 1);
@@ -786,96 +814,85 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
   }
   float psum = 0.f;
   const float scale2 = kLog2e / sqrtf((float)D);
-  // dQ^T(d block, queries) += K^T dS^T ;  SA^T(j block, queries) += Y^T P^T
-  // for tile kb: the transposed operands come from transposing LDS reads
-  bf16x8 ph[2], pl[2], dsb[2];
-  auto phase3 = [&](int kb) {
-    const bf16* kt = &sm.key[kb & 1][0][0];
+  // Software pipeline over the key tiles, three LDS buffers.  Iteration kb
+  // runs the row-major products of tile kb (S^T = K Q^T, dP^T = Y (W U)^T)
+  // and the transposed products of tile kb - 1 (dQ^T += K^T dS^T,
+  // SA^T += Y^T P^T, with that tile's p and dS) in one basic block of
+  // independent MFMA chains, then forms p and dS of tile kb: the scheduler
+  // interleaves the chains, so the matrix pipe stays busy while operands
+  // arrive and while the vector units form p and dS.
+  constexpr int NG = 2 * NB;  // groups (d or j block, k-step) of the transposed products
+  bf16x8 ph[2] = {}, pl[2] = {}, dsb[2] = {};  // p hi / lo and dS of the tile before
+  auto tr_products = [&](int kb, int g0, int g1) {
+    const bf16* kt = &sm.key[kb % 3][0][0];
     const bf16* ty = kt + kTile * D;
     const bf16* tyl = ty + kTile * D;
-    // groups g = (b, k2), their three transposed fragments read two groups ahead
-    constexpr int NG = 2 * NB;
-    bf16x8 ring[3][3];
-    auto load_group = [&](int g, bf16x8* f) {
-      const int b = g >> 1, p0 = kh * 32 + (g & 1) * 16;
-      f[0] = frag_tr<D>(kt, b * 32, p0);
-      f[1] = frag_tr<D>(ty, b * 32, p0);
-      f[2] = frag_tr<D>(tyl, b * 32, p0);
-    };
-    load_group(0, ring[0]);
-    if (NG > 1) load_group(1, ring[1]);
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      if (g + 2 < NG) load_group(g + 2, ring[(g + 2) % 3]);
-      const bf16x8* f = ring[g % 3];
-      const int b = g >> 1, k2 = g & 1;
-      dqt[b] = mfma(f[0], dsb[k2], dqt[b]);
-      sat[b] = mfma(f[1], ph[k2], sat[b]);
-      sat[b] = mfma(f[2], ph[k2], sat[b]);
-      sat[b] = mfma(f[1], pl[k2], sat[b]);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int g = g0; g < g1; ++g) {
+      const int b = g >> 1, k2 = g & 1, p0 = kh * 32 + k2 * 16;
+      const bf16x8 fk = frag_tr<D>(kt, b * 32, p0);
+      const bf16x8 fh = frag_tr<D>(ty, b * 32, p0);
+      const bf16x8 fl = frag_tr<D>(tyl, b * 32, p0);
+      dqt[b] = mfma(fk, dsb[k2], dqt[b]);
+      sat[b] = mfma(fh, ph[k2], sat[b]);
+      sat[b] = mfma(fl, ph[k2], sat[b]);
+      sat[b] = mfma(fh, pl[k2], sat[b]);
     }
   };
-  // Per iteration: tile kb's loads have landed and every wave is done with
-  // tile kb - 1, whose buffer tile kb + 1 now streams into.
-  for (int kb = 0; kb <= qb; ++kb) {
+  // one iteration; prev: whether tile kb - 1's transposed products run in
+  // it; masked: whether the tile pair needs the causal and length masks (only
+  // the diagonal tile, or a query tile that runs past T)
+  auto iteration = [&](int kb, auto prev, auto masked) {
     const int k0 = kb * kTile;
     wait_vmem();
-    __syncthreads();
+    __syncthreads();  // tile kb is in; every wave is done with tile kb - 2
     if (kb < qb) fetch(kb + 1);
-    const bf16* kt = &sm.key[kb & 1][0][0];
+    const bf16* kt = &sm.key[kb % 3][0][0];
     const bf16* ty = kt + kTile * D;   // Y hi
     const bf16* tyl = ty + kTile * D;  // Y lo
-
-    // S^T (keys x queries) then dP^T = Y (W U)^T over j: 2 NKS steps whose
-    // key-side fragments are read four steps ahead (scheduling barriers keep
-    // the order, so each MFMA waits only for reads issued four steps before);
-    // the query-side fragments stay in registers for the whole loop
     f32x16 s = {}, dp = {};
-    {
-      constexpr int LA = 4;  // steps of lookahead
-      bf16x8 ring[LA + 1][2];
-      auto load_step = [&](int k, bf16x8* f) {
-        if (k < C::NKS) {
-          f[0] = frag_rows<D>(kt, kh * 32 + n, 2 * k + hl);
-        } else {
-          const int ks = k - C::NKS;
-          f[0] = frag_rows<D>(ty, kh * 32 + n, 2 * ks + hl);
-          f[1] = frag_rows<D>(tyl, kh * 32 + n, 2 * ks + hl);
-        }
-      };
 #pragma unroll
-      for (int k = 0; k < LA; ++k) load_step(k, ring[k]);
+    for (int k = 0; k < C::NKS; ++k) s = mfma(frag_rows<D>(kt, kh * 32 + n, 2 * k + hl), qf[k], s);
+    if constexpr (decltype(prev)::value) tr_products(kb - 1, 0, NG / 2);
 #pragma unroll
-      for (int k = 0; k < 2 * C::NKS; ++k) {
-        if (k + LA < 2 * C::NKS) load_step(k + LA, ring[(k + LA) % (LA + 1)]);
-        const bf16x8* f = ring[k % (LA + 1)];
-        if (k < C::NKS) {
-          s = mfma(f[0], qf[k], s);
-        } else {
-          const int ks = k - C::NKS;
-          dp = mfma(f[0], wf[ks][0], dp);
-          dp = mfma(f[1], wf[ks][0], dp);
-          dp = mfma(f[0], wf[ks][1], dp);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      const bf16x8 ah = frag_rows<D>(ty, kh * 32 + n, 2 * ks + hl);
+      const bf16x8 al = frag_rows<D>(tyl, kh * 32 + n, 2 * ks + hl);
+      dp = mfma(ah, wf[ks][0], dp);
+      dp = mfma(al, wf[ks][0], dp);
+      dp = mfma(ah, wf[ks][1], dp);
     }
+    if constexpr (decltype(prev)::value) tr_products(kb - 1, NG / 2, NG);
     const bool tlive = q0 + t < T;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int i = kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = k0 + i <= q0 + t && tlive && k0 + i < T;
-      const float p = exp2_hw(ok ? fmaf(s[r], scale2, -l2) : -INFINITY);
-      psum += p;
-      bf16 a, b;
-      split_bf16(p, a, b);
-      ph[r >> 3][r & 7] = a;
-      pl[r >> 3][r & 7] = b;
-      dsb[r >> 3][r & 7] = (bf16)(p * (dp[r] + ct));
-    }
-    phase3(kb);
+    pack_p_ds(
+        [&](int r) {
+          const float x = fmaf(s[r], scale2, -l2);
+          float pr;
+          if constexpr (decltype(masked)::value) {
+            const int i = kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+            const bool ok = k0 + i <= q0 + t && tlive && k0 + i < T;
+            pr = exp2_hw(ok ? x : -INFINITY);
+          } else {
+            pr = exp2_hw(x);
+          }
+          psum += pr;
+          return f32x2{pr, ct};
+        },
+        dp, ph, pl, dsb);
+  };
+  const std::true_type yes;
+  const std::false_type no;
+  if (qb == 0) {
+    iteration(0, no, yes);
+  } else if (q0 + kTile <= T) {
+    iteration(0, no, no);
+    for (int kb = 1; kb < qb; ++kb) iteration(kb, yes, no);
+    iteration(qb, yes, yes);
+  } else {  // the query tile runs past T: every tile pair masks its rows
+    iteration(0, no, yes);
+    for (int kb = 1; kb <= qb; ++kb) iteration(kb, yes, yes);
   }
+  tr_products(qb, 0, NG);
 
   // ---- epilogue.  The key halves (waves kh = 0, 1 of the same qh) meet in
   // LDS as [64 queries][D + 1] totals of dQ^T and SA^T; then every thread
@@ -1022,8 +1039,8 @@ __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
 // rows' operands (K and Y hi / lo as MFMA B fragments) stay in registers.
 template <int D>
 struct KvFast {
-  bf16 qry[2][3][kTile * D];  // [buffer][Q, W U' hi, W U' lo], swizzled [query][d or j]
-  float cst[2][kTile], lse[2][kTile], c[D], bl[D];
+  bf16 qry[3][3][kTile * D];  // [buffer][Q, W U' hi, W U' lo], swizzled [query][d or j]
+  float cst[3][kTile], lse[3][kTile], c[D], bl[D];
 };
 
 template <int D>
@@ -1045,13 +1062,13 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
   const int qh = wave >> 1, kh = wave & 1;
   auto fetch = [&](int qb) {
     const int q0 = qb * kTile;
-    bf16* dst = &sm.qry[qb & 1][0][0];
+    bf16* dst = &sm.qry[qb % 3][0][0];
     load_swz<D>(Q + base + (size_t)q0 * D, dst, T - 1 - q0);
     load_swz<D>(wh + (rows0 + q0) * D, dst + kTile * D, kTile - 1);
     load_swz<D>(wl + (rows0 + q0) * D, dst + 2 * kTile * D, kTile - 1);
     // row constants and log-normalisers: one dword per lane (rows past T re-read row T - 1)
-    if (wave == 0) dma4(cst + rows0 + q0 + lane, &sm.cst[qb & 1][0]);
-    if (wave == 1) dma4(lse + (size_t)bh * T + min(q0 + lane, T - 1), &sm.lse[qb & 1][0]);
+    if (wave == 0) dma4(cst + rows0 + q0 + lane, &sm.cst[qb % 3][0]);
+    if (wave == 1) dma4(lse + (size_t)bh * T + min(q0 + lane, T - 1), &sm.lse[qb % 3][0]);
   };
   fetch(kb);
 
@@ -1088,97 +1105,79 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
   }
   const float scale2 = kLog2e / sqrtf((float)D);
   const int qlast = (T - 1) / kTile;
-  // dV^T(j block, keys) += (W U')^T P ;  dK^T(d block, keys) += Q^T dS for
-  // query tile qb: the transposed operands come from transposing LDS reads
-  bf16x8 ph[2], pl[2], dsb[2];
-  auto phase3 = [&](int qb) {
-    const bf16* tq = &sm.qry[qb & 1][0][0];
+  // Software pipeline over the query tiles, three LDS buffers, as in the q
+  // pass: iteration qb runs S = Q K^T and dP = (W U') Y^T of tile qb and the
+  // transposed products of tile qb - 1 (dV^T += (W U')^T P, dK^T += Q^T dS)
+  // in one basic block, then forms p and dS of tile qb.
+  constexpr int NG = 2 * NB;
+  bf16x8 ph[2] = {}, pl[2] = {}, dsb[2] = {};  // p hi / lo and dS of the tile before
+  auto tr_products = [&](int qb, int g0, int g1) {
+    const bf16* tq = &sm.qry[qb % 3][0][0];
     const bf16* tw = tq + kTile * D;
     const bf16* twl = tw + kTile * D;
-    // groups g = (b, k2), their three transposed fragments read two groups ahead
-    constexpr int NG = 2 * NB;
-    bf16x8 ring[3][3];
-    auto load_group = [&](int g, bf16x8* f) {
-      const int b = g >> 1, p0 = qh * 32 + (g & 1) * 16;
-      f[0] = frag_tr<D>(tw, b * 32, p0);
-      f[1] = frag_tr<D>(twl, b * 32, p0);
-      f[2] = frag_tr<D>(tq, b * 32, p0);
-    };
-    load_group(0, ring[0]);
-    if (NG > 1) load_group(1, ring[1]);
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      if (g + 2 < NG) load_group(g + 2, ring[(g + 2) % 3]);
-      const bf16x8* f = ring[g % 3];
-      const int b = g >> 1, k2 = g & 1;
-      dvt[b] = mfma(f[0], ph[k2], dvt[b]);
-      dvt[b] = mfma(f[1], ph[k2], dvt[b]);
-      dvt[b] = mfma(f[0], pl[k2], dvt[b]);
-      dkt[b] = mfma(f[2], dsb[k2], dkt[b]);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int g = g0; g < g1; ++g) {
+      const int b = g >> 1, k2 = g & 1, p0 = qh * 32 + k2 * 16;
+      const bf16x8 gh = frag_tr<D>(tw, b * 32, p0);
+      const bf16x8 gl = frag_tr<D>(twl, b * 32, p0);
+      const bf16x8 fq = frag_tr<D>(tq, b * 32, p0);
+      dvt[b] = mfma(gh, ph[k2], dvt[b]);
+      dvt[b] = mfma(gl, ph[k2], dvt[b]);
+      dvt[b] = mfma(gh, pl[k2], dvt[b]);
+      dkt[b] = mfma(fq, dsb[k2], dkt[b]);
     }
   };
-  // Per iteration: query tile qb's loads have landed and every wave is done
-  // with tile qb - 1, whose buffer tile qb + 1 now streams into.
-  for (int qb = kb; qb <= qlast; ++qb) {
+  // one iteration; prev: whether tile qb - 1's transposed products run in
+  // it; masked: whether the tile pair needs the causal and length masks (the
+  // diagonal tile, or a tile that runs past T)
+  auto iteration = [&](int qb, auto prev, auto masked) {
     const int q0 = qb * kTile;
     wait_vmem();
-    __syncthreads();
+    __syncthreads();  // tile qb is in; every wave is done with tile qb - 2
     if (qb < qlast) fetch(qb + 1);
-    const bf16* tq = &sm.qry[qb & 1][0][0];
+    const bf16* tq = &sm.qry[qb % 3][0][0];
     const bf16* tw = tq + kTile * D;   // W U' hi
     const bf16* twl = tw + kTile * D;  // W U' lo
-    const float* lq = sm.lse[qb & 1];
-    const float* cq = sm.cst[qb & 1];
-
-    // S (queries x keys) then dP = (W U') Y^T over j: 2 NKS steps whose
-    // query-side fragments are read four steps ahead (scheduling barriers
-    // keep the order); the key-side fragments stay in registers
+    const float* lq = sm.lse[qb % 3];
+    const float* cq = sm.cst[qb % 3];
     f32x16 s = {}, dp = {};
-    {
-      constexpr int LA = 4;  // steps of lookahead
-      bf16x8 ring[LA + 1][2];
-      auto load_step = [&](int k, bf16x8* f) {
-        if (k < C::NKS) {
-          f[0] = frag_rows<D>(tq, qh * 32 + n, 2 * k + hl);
-        } else {
-          const int ks = k - C::NKS;
-          f[0] = frag_rows<D>(tw, qh * 32 + n, 2 * ks + hl);
-          f[1] = frag_rows<D>(twl, qh * 32 + n, 2 * ks + hl);
-        }
-      };
 #pragma unroll
-      for (int k = 0; k < LA; ++k) load_step(k, ring[k]);
+    for (int k = 0; k < C::NKS; ++k) s = mfma(frag_rows<D>(tq, qh * 32 + n, 2 * k + hl), kf[k], s);
+    if constexpr (decltype(prev)::value) tr_products(qb - 1, 0, NG / 2);
 #pragma unroll
-      for (int k = 0; k < 2 * C::NKS; ++k) {
-        if (k + LA < 2 * C::NKS) load_step(k + LA, ring[(k + LA) % (LA + 1)]);
-        const bf16x8* f = ring[k % (LA + 1)];
-        if (k < C::NKS) {
-          s = mfma(f[0], kf[k], s);
-        } else {
-          const int ks = k - C::NKS;
-          dp = mfma(f[0], yf[ks][0], dp);
-          dp = mfma(f[1], yf[ks][0], dp);
-          dp = mfma(f[0], yf[ks][1], dp);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
+    for (int ks = 0; ks < C::NKS; ++ks) {
+      const bf16x8 ah = frag_rows<D>(tw, qh * 32 + n, 2 * ks + hl);
+      const bf16x8 al = frag_rows<D>(twl, qh * 32 + n, 2 * ks + hl);
+      dp = mfma(ah, yf[ks][0], dp);
+      dp = mfma(al, yf[ks][0], dp);
+      dp = mfma(ah, yf[ks][1], dp);
     }
-    // p, and dS = p (dP + const); p and dS as B operands (k = this wave's
-    // queries, accumulator order)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = k0 + i <= q0 + t && q0 + t < T && k0 + i < T;
-      const float p = exp2_hw(ok ? fmaf(s[r], scale2, -lq[t] * kLog2e) : -INFINITY);
-      bf16 a, b;
-      split_bf16(p, a, b);
-      ph[r >> 3][r & 7] = a;
-      pl[r >> 3][r & 7] = b;
-      dsb[r >> 3][r & 7] = (bf16)(p * (dp[r] + cq[t]));
-    }
-    phase3(qb);
+    if constexpr (decltype(prev)::value) tr_products(qb - 1, NG / 2, NG);
+    pack_p_ds(
+        [&](int r) {
+          const int t = qh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+          const float x = fmaf(s[r], scale2, -lq[t] * kLog2e);
+          float pr;
+          if constexpr (decltype(masked)::value) {
+            const bool ok = k0 + i <= q0 + t && q0 + t < T && k0 + i < T;
+            pr = exp2_hw(ok ? x : -INFINITY);
+          } else {
+            pr = exp2_hw(x);
+          }
+          return f32x2{pr, cq[t]};
+        },
+        dp, ph, pl, dsb);
+  };
+  const std::true_type yes;
+  const std::false_type no;
+  const bool ragged = qlast * kTile + kTile > T;  // the last query tile runs past T
+  iteration(kb, no, yes);
+  for (int qb = kb + 1; qb < qlast; ++qb) iteration(qb, yes, no);
+  if (qlast > kb) {
+    if (ragged) iteration(qlast, yes, yes);
+    else iteration(qlast, yes, no);
   }
+  tr_products(qlast, 0, NG);
 
   // ---- epilogue.  The query halves (waves qh = 0, 1 of the same kh) meet
   // in LDS as [64 keys][D + 1] totals of dV^T and dK^T; then every thread
