@@ -475,13 +475,6 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
 // operands (K^T, Y^T; Q^T, (W U')^T) are read from the same row-major tiles
 // by transposing LDS reads (ds_read_b64_tr_b16).
 
-__host__ __device__ constexpr int epos32(int r) {
-  return (r & 16) + (((r >> 2) & 1) << 3) + (((r >> 3) & 1) << 2) + (r & 3);
-}
-// Storage position of contraction index x (0..63) in a row whose 32-blocks
-// feed MFMA A operands against B operands taken from an accumulator's rows.
-__host__ __device__ constexpr int ppos(int x) { return (x & 32) + epos32(x & 31); }
-
 __device__ __forceinline__ void split_bf16(float x, bf16& hi, bf16& lo) {
   hi = (bf16)x;
   lo = (bf16)(x - (float)hi);
@@ -532,24 +525,6 @@ __device__ __forceinline__ int xcd_order(int b, int nblk) {
 }
 
 
-// ---- swizzled tiles ----------------------------------------------------------
-//
-// A streamed [64][D] bf16 tile sits in LDS unpadded, 16-byte chunk c of row r
-// at chunk position c ^ swz(r).  swz makes both read patterns bank-conflict
-// free: a row-major MFMA fragment (16 lanes, 16 consecutive rows, one chunk
-// each) and a transposing read (4 consecutive rows, 32 consecutive columns).
-template <int D>
-__host__ __device__ constexpr int swz(int r) {
-  return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3))
-       : D == 64  ? ((((r >> 1) & 1) << 2) | ((r >> 2) & 3))
-                  : ((r >> 2) & 3);
-}
-
-template <int D>
-__device__ __forceinline__ int swz_off(int row, int chunk) {  // byte offset
-  return row * D * 2 + ((chunk ^ swz<D>(row)) << 4);
-}
-
 // Direct global -> LDS copy of rows [0, 64) of a row-major [., D] bf16 source
 // into a swizzled tile; rows past lim re-read row lim (their keys or queries
 // are masked).  Wave w fills the 1 KiB blocks w, w + 4, ...: lane l of block
@@ -578,37 +553,6 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 __device__ __forceinline__ void settle(const bf16x8& x) { asm volatile("" ::"v"(x)); }
 __device__ __forceinline__ void settle(float x) { asm volatile("" ::"v"(x)); }
 
-// Row-major MFMA fragment of a swizzled tile: 8 bf16 of row `row`, chunk `chunk`.
-template <int D>
-__device__ __forceinline__ bf16x8 frag_rows(const bf16* t, int row, int chunk) {
-  return *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(t) + swz_off<D>(row, chunk));
-}
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
-// Transposed MFMA A fragment of a swizzled tile: A[m][k] = tile[row(p0 + k)][col0 + m]
-// for m < 32, k < 16, with the contraction positions p0 + k in permuted
-// order (row(p) = ppos(p)).  Two transposing reads: in each 16-lane group,
-// lanes 4r..4r+3 read 4 columns each of row r, and lane c gets column c of
-// the 4 rows.  Group g = lane / 16 takes columns col0 + 16 (g & 1) .. and
-// positions p0 + 8 (g >> 1) ..: the A layout of v_mfma_f32_32x32x16_bf16.
-template <int D>
-__device__ __forceinline__ bf16x8 frag_tr(const bf16* t, int col0, int p0) {
-  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
-  const int r = i >> 2, q = i & 3;
-  const int col = col0 + 16 * (g & 1) + 4 * q;
-  const int p = p0 + 8 * (g >> 1);
-  const char* b = reinterpret_cast<const char*>(t);
-  const int r0 = ppos(p) + r, r1 = ppos(p + 4) + r;
-  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_s16x4*)(b + swz_off<D>(r0, col >> 3) + (col & 7) * 2));
-  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_s16x4*)(b + swz_off<D>(r1, col >> 3) + (col & 7) * 2));
-  typedef short s16x8 __attribute__((ext_vector_type(8)));
-  const s16x8 x = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-  return __builtin_bit_cast(bf16x8, x);
-}
 
 // Per 64-row tile of V, the max and min of each channel (for the channel
 // shifts and forms); the first workgroup clears the fallback flag.

@@ -103,10 +103,9 @@ typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 
 struct LinSmem {
   bf16 fq[CH * ROW];    // phi(Q) [token][d_k]
-  bf16 fk[CH * ROW];    // phi(K) [token][d_k]
-  bf16 fkt[DK * ROW];   // phi(K)^T [d_k][key, MFMA order]
-  // V^T [d_v][key, MFMA order] while the waves form E; then S^T hi [d_v][d_k]
-  bf16 vt_sh[DV * ROW];
+  bf16 fk[CH * DK];     // phi(K) [key][d_k], swizzled; phi(K)^T comes from transposing reads
+  bf16 vs[CH * DV];     // V [key][d_v], swizzled; V^T comes from transposing reads
+  bf16 sh[DV * SROW];   // S^T hi [d_v][d_k]
   bf16 sl[DV * SROW];   // S^T lo
   float c[DV];          // running shift (published for the epilogue)
   float bl[DV];         // beta log2 e
@@ -121,12 +120,14 @@ struct GlaSmem {
   float b[CH * DK];
   float bq[4 * DK];
   float zr[DK];
+  bf16 fk2[CH * DK];  // k~ e^{B_last - B} [key][d_k], swizzled (the state update's operand)
 };
 template <int PRIOR>
 struct ScanSmem : LinSmem {
   __device__ float* gb() { return nullptr; }
   __device__ float* gbq() { return nullptr; }
   __device__ float* gzr() { return nullptr; }
+  __device__ bf16* fku() { return fk; }  // the state update's key features
 };
 template <>
 struct ScanSmem<kGla> : LinSmem {
@@ -134,8 +135,14 @@ struct ScanSmem<kGla> : LinSmem {
   __device__ float* gb() { return gla.b; }
   __device__ float* gbq() { return gla.bq; }
   __device__ float* gzr() { return gla.zr; }
+  __device__ bf16* fku() { return gla.fk2; }
 };
-static_assert(ROW == SROW, "S^T hi shares the V^T rows");
+
+// Element (row, col) of a swizzled [64][64] tile.
+__device__ __forceinline__ float swz_elem(const bf16* t, int row, int col) {
+  return (float)*reinterpret_cast<const bf16*>(reinterpret_cast<const char*>(t) +
+                                               swz_off<DK>(row, col >> 3) + (col & 7) * 2);
+}
 
 // Key r of a chunk -> position inside an MFMA-ordered row (see the softmax
 // kernel: the B operand taken from a transposed accumulator holds keys
@@ -143,14 +150,6 @@ static_assert(ROW == SROW, "S^T hi shares the V^T rows");
 __device__ __forceinline__ int e_pos(int r) {
   const int g = r & 15;
   return (r & ~15) + (((g >> 2) & 1) << 3) + (((g >> 3) & 1) << 2) + (g & 3);
-}
-
-// phi(K)^T and V^T rows are written one bf16 at a time down a column of
-// eight rows per lane group; the 16-byte chunk of a row is XORed with the
-// row's group of eight so that those writes spread over the banks.  Readers
-// of 16-byte MFMA fragments apply the same map.
-__device__ __forceinline__ int tpos(int row, int pos) {
-  return row * ROW + ((((pos >> 3) ^ (row >> 3)) & 7) << 3) + (pos & 7);
 }
 
 // Workgroup barrier that orders LDS only: every wave's LDS accesses complete
@@ -352,8 +351,9 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     lds_barrier();
   }
 
-  // ---- stage phi(Q), phi(K), phi(K)^T and V^T; phi in fp32, rounded to bf16.
-  // GLA: phi(Q) = q~ e^{B - R}, phi(K) = k~ e^{R - B}, phi(K)^T = k~ e^{B_last - B}.
+  // ---- stage phi(Q), phi(K) and V, row-major; phi in fp32, rounded to bf16.
+  // GLA: phi(Q) = q~ e^{B - R}, phi(K) = k~ e^{R - B}, and for the state
+  // update k~ e^{B_last - B}.
 #pragma unroll
   for (int i = 0; i < SLOTS; ++i) {
     const int e = tid + NTH * i, r = e >> 3, c8 = (e & 7) * 8;
@@ -362,6 +362,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     bf16x8 pk, pq;
     if (PRIOR == kGla) {
       float kx[8], qx[8];
+      bf16x8 pu;
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         kx[u] = (float)cr.k[i][u];
@@ -379,19 +380,18 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
         const float bl = sm.gb()[(CH - 1) * DK + c8 + u];
         pk[u] = (bf16)(kx[u] * exp2_hw((R - b) * kLog2e) * okf);
         if (OUT) pq[u] = (bf16)(qx[u] * exp2_hw((b - R) * kLog2e) * okf);
-        sm.fkt[tpos(c8 + u, e_pos(r))] = (bf16)(kx[u] * exp2_hw((bl - b) * kLog2e) * okf);
-        sm.vt_sh[tpos(c8 + u, e_pos(r))] = cr.v[i][u];
+        pu[u] = (bf16)(kx[u] * exp2_hw((bl - b) * kLog2e) * okf);
       }
+      *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.fku()) + swz_off<DK>(r, c8 >> 3)) = pu;
     } else {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         pk[u] = (bf16)(phi((float)cr.k[i][u]) * okf);
         if (OUT) pq[u] = (bf16)(phi((float)cr.q[i][u]) * okf);
-        sm.fkt[tpos(c8 + u, e_pos(r))] = pk[u];
-        sm.vt_sh[tpos(c8 + u, e_pos(r))] = cr.v[i][u];
       }
     }
-    *reinterpret_cast<bf16x8*>(sm.fk + r * ROW + c8) = pk;
+    *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.fk) + swz_off<DK>(r, c8 >> 3)) = pk;
+    *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.vs) + swz_off<DV>(r, c8 >> 3)) = cr.v[i];
     if (OUT) *reinterpret_cast<bf16x8*>(sm.fq + r * ROW + c8) = pq;
   }
   // the next chunk's loads run while this one is processed
@@ -405,8 +405,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
   {
     bf16x8 vr[4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-      vr[ks] = *reinterpret_cast<const bf16x8*>(sm.vt_sh + tpos(ch, ks * 16 + hl * 8));
+    for (int ks = 0; ks < 4; ++ks) vr[ks] = frag_tr<DV>(sm.vs, dvb * 32, ks * 16);
     // keys at or past T (last chunk only) stay out of the max and give E = 0
     const bool full = t0 + CH <= T;
     float vmax = -INFINITY;
@@ -450,8 +449,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     float s = 0.f;
 #pragma unroll
     for (int r = 0; r < CH / 4; ++r)
-      s += PRIOR == kGla ? (float)sm.fkt[tpos(dkc, q4 * (CH / 4) + r)]
-                         : (float)sm.fk[(q4 * (CH / 4) + r) * ROW + dkc];
+      s += swz_elem(sm.fku(), q4 * (CH / 4) + r, dkc);
     sm.zc[q4 * DK + dkc] = s;
     // GLA: the inter-chunk normaliser reads e^{R} z
     if (PRIOR == kGla && q4 == 0)
@@ -464,7 +462,6 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     for (int i = 0; i < 16; ++i) st[i] *= __shfl(gj, (i >> 2) * 8 + hl * 4 + (i & 3));
   }
   if (OUT) {
-    lds_barrier();  // every wave has read V^T before S^T hi replaces it
     const float eR =
         PRIOR == kGla ? exp2_hw(sm.gb()[(CH / 2 - 1) * DK + sub * 32 + n] * kLog2e) : 1.f;
 #pragma unroll
@@ -473,7 +470,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
       const int col = sub * 32 + n;
       const float sv = st[i] * eR;
       const bf16 hi = (bf16)sv;
-      sm.vt_sh[row * SROW + col] = hi;
+      sm.sh[row * SROW + col] = hi;
       sm.sl[row * SROW + col] = (bf16)(sv - (float)hi);
     }
     if (sub == 0 && hl == 0) sm.c[ch] = cj;
@@ -492,7 +489,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
       f32x16 at = f32x16{};
 #pragma unroll
       for (int ks = 0; ks < DK / 16; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(sm.fk + (kb * 32 + n) * ROW + ks * 16 + hl * 8);
+        const bf16x8 a = frag_rows<DK>(sm.fk, kb * 32 + n, 2 * ks + hl);
         const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + (qb * 32 + n) * ROW + ks * 16 + hl * 8);
         at = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, at, 0, 0, 0);
       }
@@ -527,7 +524,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     float dz[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < DK / 16; ++ks) {
-      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.vt_sh + soff + ks * 16);
+      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.sh + soff + ks * 16);
       const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.sl + soff + ks * 16);
       const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + (qb * 32 + n) * ROW + ks * 16 + hl * 8);
       num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
@@ -590,8 +587,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     }
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const bf16x8 b =
-          *reinterpret_cast<const bf16x8*>(sm.fkt + tpos(sub * 32 + n, ks * 16 + hl * 8));
+      const bf16x8 b = frag_tr<DK>(sm.fku(), sub * 32, ks * 16);
       st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eh[ks], b, st, 0, 0, 0);
       st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el[ks], b, st, 0, 0, 0);
     }
