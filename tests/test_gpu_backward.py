@@ -123,6 +123,19 @@ def test_backward_longer_sequence(fem):
     check_grads(grads, want, "T1024 d128", dbeta_floor(v, b, g))
 
 
+@pytest.mark.parametrize("d,T", [(32, 700), (64, 1000)])
+def test_backward_longer_small_d(fem, d, T):
+    """Many tile pairs (pipelined passes, unmasked off-diagonal pairs, a
+    ragged last tile) for the narrower head widths."""
+    seed = 13600 + d
+    say(f"backward B1 H2 T{T} d{d}, seed {seed}")
+    q, k, v, b, g = draw(seed, 1, 2, T, d)
+    _, _, grads = run(fem, q, k, v, b, g)
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, f"T{T} d{d}", dbeta_floor(v, b, g))
+
+
 def test_backward_deterministic(fem):
     say("backward determinism: B2 H2 T500 d64, seed 13400")
     q, k, v, b, g = draw(13400, 2, 2, 500, 64)
