@@ -705,7 +705,7 @@ __global__ __launch_bounds__(kThreads) void bwd_q_fast_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const float* __restrict__ lse,
     const bf16* __restrict__ yh, const bf16* __restrict__ yl, const bf16* __restrict__ wh,
     const bf16* __restrict__ wl, const float* __restrict__ cst, float* __restrict__ dQ,
-    float* __restrict__ sap, float* __restrict__ lse_p, int H, int T, int ntile) {
+    float* __restrict__ sap, float* __restrict__ lse_p, int T, int ntile) {
   using C = Bw<D>;
   constexpr int NB = C::NCB;
   __shared__ __align__(16) QFast<D> sm;
@@ -1256,7 +1256,7 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   }
   if (e == hipSuccess) {  // the q pass first: its SA / P give ln(Z/P), which the kv pass uses
     hipLaunchKernelGGL(bwd_q_fast_kernel<D>, grid, blk, 0, stream, q, k, lse_fwd, yh, yl, wh, wl,
-                       cst, dQ, sap, lse, H, T, ntile);
+                       cst, dQ, sap, lse, T, ntile);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {  // ln(Z/P), the kv pass's W U' and row constants, the G F sums

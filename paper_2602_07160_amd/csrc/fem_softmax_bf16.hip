@@ -459,7 +459,7 @@ __device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, in
   constexpr int NV = QKT ? C::RPL * 4 : 0;    // tilt values of the lane
   constexpr int C0 = PVA ? 2 : 0;             // slot of the column max
   constexpr int NSLOT = NS > C0 + 2 + NV ? NS : C0 + 2 + NV;
-  auto vslot = [&](int x) { return C0 + 2 + (x * (NSLOT - C0 - 2)) / NV; };
+  auto vslot = [&](int x) { return C0 + 2 + (x * (NSLOT - C0 - 2)) / (NV > 0 ? NV : 1); };
   if (QKT) tl.read(sm, k, wave, lane);
   const unsigned char* kt = sm.base + pin(C::OFF_K + (k & 1) * C::KB + kofs);
   const unsigned char* eb = sm.base + (PVA ? pin(C::OFF_EH + ((k - 1) & 1) * C::EB + eofs) : 0u);
