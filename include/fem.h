@@ -168,9 +168,13 @@ int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
  * over keys and channels run on the matrix cores (bf16 hi + lo parts,
  * ~2^-16 relative); channels whose beta-scaled value range is at most
  * 4 / log2(e) use the cancellation-free form R - 1 = (E - 1) U + (U - 1).
- * A channel whose range beta (max v - min v) exceeds 110 / log2(e) would
- * leave fp32's exponent range: the whole call then reruns an element-wise
- * pass that is exact in form for every beta > 0 (~15x slower).  dbeta is
+ * A channel (b, h, j) whose range beta (max v - min v) over the sequence
+ * exceeds 110 / log2(e) would leave fp32's exponent range: an element-wise
+ * pass, exact in form for every beta > 0, takes that channel and adds its
+ * part of dQ and dK (at B8 H16 T4096 d128, one such channel in every batch
+ * of one head costs ~8 ms on top of ~6.4 ms).  Should a factor of another
+ * channel still leave fp32's range (an output gradient near 2^100), the
+ * element-wise pass redoes the whole call (~34x slower).  dbeta is
  * formed from the normalised posterior sums, so the forward's rounding of
  * out cancels from it.  A workspace of about 8 * B * H * T * d +
  * 20 * B * H * ceil(T / 64) * d bytes comes from the library's pool as in

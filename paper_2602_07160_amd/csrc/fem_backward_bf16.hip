@@ -57,6 +57,23 @@ constexpr int kTile = 64;   // queries and keys per tile
 constexpr int kThreads = 256;
 constexpr int kJG = 4;      // channel quarters per key (kv) or query (q)
 
+// Form of a channel (b, h, j), set from the range of beta log2e v over the
+// sequence: the matrix-core pass uses R - 1 = E U - 1 (plain) or A U + (U - 1)
+// with A = E - 1 (split, small ranges); a wide channel's factors leave fp32's
+// range, so the element-wise kernels take that channel instead.
+constexpr float kPlainForm = 0.f;
+constexpr float kSplitForm = 1.f;
+constexpr float kWide = 2.f;
+
+// What the element-wise kernels do, from the flags the matrix-core pass set:
+// nothing; the wide channels only, added to the matrix-core gradients
+// (flag[1]); or every channel, replacing them (flag[0]: a factor of some
+// other channel left fp32's range).
+constexpr int kExactNone = 0, kExactWide = 1, kExactAll = 2;
+__device__ __forceinline__ int exact_mode(const int* flag) {
+  return flag[0] ? kExactAll : flag[1] ? kExactWide : kExactNone;
+}
+
 template <int D>
 struct Bw {
   static constexpr int JPT = D / kJG;     // channels per thread in the posterior loop
@@ -78,14 +95,23 @@ __device__ __forceinline__ void stage_tile(const bf16* __restrict__ src, int r0,
                                            bf16* rowm, bf16* trn) {
   using C = Bw<D>;
   constexpr int CPR = D / 8;  // 16-byte chunks per row
-  for (int e = threadIdx.x; e < kTile * CPR; e += kThreads) {
-    const int r = e / CPR, c8 = (e % CPR) * 8;
-    bf16x8 x = {};
-    if (r0 + r < T) x = *reinterpret_cast<const bf16x8*>(src + (size_t)(r0 + r) * D + c8);
-    *reinterpret_cast<bf16x8*>(rowm + r * C::ROW + c8) = x;
+  constexpr int N = kTile * CPR / kThreads;
+  static_assert(N * kThreads == kTile * CPR, "whole rounds");
+  // every load of the tile is in flight before the first store
+  bf16x8 x[N];
+#pragma unroll
+  for (int it = 0; it < N; ++it) {
+    const int e = threadIdx.x + it * kThreads, r = e / CPR, c8 = (e % CPR) * 8;
+    x[it] = bf16x8{};
+    if (r0 + r < T) x[it] = *reinterpret_cast<const bf16x8*>(src + (size_t)(r0 + r) * D + c8);
+  }
+#pragma unroll
+  for (int it = 0; it < N; ++it) {
+    const int e = threadIdx.x + it * kThreads, r = e / CPR, c8 = (e % CPR) * 8;
+    *reinterpret_cast<bf16x8*>(rowm + r * C::ROW + c8) = x[it];
     if (trn) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) trn[(c8 + u) * C::TROW + r] = x[u];
+      for (int u = 0; u < 8; ++u) trn[(c8 + u) * C::TROW + r] = x[it][u];
     }
   }
 }
@@ -156,18 +182,29 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ lse,
     const float* __restrict__ G, float* __restrict__ dK, float* __restrict__ dV, int H, int T,
-    int ntile, const int* __restrict__ run_if) {
+    int ntile, const int* __restrict__ flag, const float* __restrict__ splitf) {
   using C = Bw<D>;
-  if (run_if && *run_if == 0) return;  // the matrix-core pass needed no fallback
+  static_assert(D <= kThreads && C::JPT <= 32, "channel masks");
+  const int mode = exact_mode(flag);
+  if (mode == kExactNone) return;  // the matrix-core pass took every channel
+  const bool all = mode == kExactAll;
+  const int tid = threadIdx.x;
+  const int kb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
+  // wide channels only: nothing to do for a (b, h) without one
+  if (!all && !__syncthreads_or(tid < D && splitf[bh * D + tid] == kWide)) return;
   __shared__ __align__(16) KvSmem<D> sm;
   __shared__ float lse2[kTile];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
-  const int kb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
+  const int wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
   const int k0 = kb * kTile;
   const size_t base = (size_t)bh * T * D;
 
-  // posterior-loop mapping: key ki, channels jg*JPT ..
+  // posterior-loop mapping: key ki, channels jg*JPT ..; bit u of act: channel
+  // j0 + u is taken here
   const int ki = tid >> 2, jg = tid & 3, j0 = jg * C::JPT;
+  unsigned act = 0;
+#pragma unroll
+  for (int u = 0; u < C::JPT; ++u)
+    if (all || splitf[bh * D + j0 + u] == kWide) act |= 1u << u;
   float bv[C::JPT], ib[C::JPT], dv[C::JPT];
 #pragma unroll
   for (int u = 0; u < C::JPT; ++u) {
@@ -191,18 +228,35 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
     const int q0 = qb * kTile;
     __syncthreads();  // the previous block's readers are done with the tiles
     stage_tile<D>(Q + base, q0, T, sm.qt, sm.qT);
-    for (int e = tid; e < kTile * D / 4; e += kThreads) {
-      const int t = e / (D / 4), c4 = (e % (D / 4)) * 4;
-      f32x4 g = {}, f = {};
-      if (q0 + t < T) {
-        g = *reinterpret_cast<const f32x4*>(G + base + (size_t)(q0 + t) * D + c4);
-        f = *reinterpret_cast<const f32x4*>(F + base + (size_t)(q0 + t) * D + c4);
-      }
-      f32x4 fbv;
+    {
+      // thread tid handles channels c4.. of rows tid / (D/4) + it * (kThreads / (D/4));
+      // the G and F loads of a round are all in flight before its stores
+      constexpr int N = kTile * D / 4 / kThreads, RPI = kThreads / (D / 4), NB = N >= 4 ? 4 : N;
+      static_assert(N * kThreads == kTile * D / 4 && N % NB == 0, "whole rounds");
+      const int c4 = (tid % (D / 4)) * 4, t0 = tid / (D / 4);
+      f32x4 bl4;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) fbv[u] = beta[h * D + c4 + u] * kLog2e * f[u];
-      *reinterpret_cast<f32x4*>(sm.gq + t * D + c4) = g;
-      *reinterpret_cast<f32x4*>(sm.fb + t * D + c4) = fbv;
+      for (int u = 0; u < 4; ++u) bl4[u] = beta[h * D + c4 + u] * kLog2e;
+#pragma unroll
+      for (int i0 = 0; i0 < N; i0 += NB) {
+        f32x4 g[NB], f[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const int t = t0 + (i0 + i) * RPI;
+          g[i] = f32x4{};
+          f[i] = f32x4{};
+          if (q0 + t < T) {
+            g[i] = *reinterpret_cast<const f32x4*>(G + base + (size_t)(q0 + t) * D + c4);
+            f[i] = *reinterpret_cast<const f32x4*>(F + base + (size_t)(q0 + t) * D + c4);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const int t = t0 + (i0 + i) * RPI;
+          *reinterpret_cast<f32x4*>(sm.gq + t * D + c4) = g[i];
+          *reinterpret_cast<f32x4*>(sm.fb + t * D + c4) = bl4 * f[i];
+        }
+      }
     }
     if (tid < kTile) lse2[tid] = q0 + tid < T ? lse[(size_t)bh * T + q0 + tid] * kLog2e : 0.f;
     __syncthreads();
@@ -210,7 +264,14 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
     {
       const int t = tid >> 2;
       float s = 0.f;
-      for (int u = 0; u < C::JPT; ++u) s += sm.gq[t * D + j0 + u] / beta[h * D + j0 + u];
+      // (t, j0..) is also this thread's posterior channel range: ib holds 1/beta
+#pragma unroll
+      for (int u4 = 0; u4 < C::JPT; u4 += 4) {
+        const f32x4 g4 = *reinterpret_cast<const f32x4*>(sm.gq + t * D + j0 + u4);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          s += ((act >> (u4 + u)) & 1) ? g4[u] * ib[u4 + u] : 0.f;
+      }
       s += __shfl_xor(s, 1);
       s += __shfl_xor(s, 2);
       if (jg == 0) sm.dsum[t] = s;
@@ -226,11 +287,13 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
         float part = 0.f;
 #pragma unroll
         for (int u4 = 0; u4 < C::JPT; u4 += 4) {
+          if (!((act >> u4) & 0xfu)) continue;
           const f32x4 fb4 = *reinterpret_cast<const f32x4*>(sm.fb + t * D + j0 + u4);
           const f32x4 g4 = *reinterpret_cast<const f32x4*>(sm.gq + t * D + j0 + u4);
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float gqv = g4[u] * exp2_hw(lp + (bv[u4 + u] - fb4[u]));
+            const float gqv =
+                ((act >> (u4 + u)) & 1) ? g4[u] * exp2_hw(lp + (bv[u4 + u] - fb4[u])) : 0.f;
             dv[u4 + u] += gqv;
             part = fmaf(gqv, ib[u4 + u], part);
           }
@@ -260,12 +323,18 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
     }
   }
 
-  // dV: thread (key ki, channels j0..)
+  // dV: thread (key ki, channels j0..); the columns taken here only
   if (k0 + ki < T) {
 #pragma unroll
     for (int u4 = 0; u4 < C::JPT; u4 += 4) {
-      const f32x4 o = {dv[u4], dv[u4 + 1], dv[u4 + 2], dv[u4 + 3]};
-      *reinterpret_cast<f32x4*>(dV + base + (size_t)(k0 + ki) * D + j0 + u4) = o;
+      float* at = dV + base + (size_t)(k0 + ki) * D + j0 + u4;
+      if (all) {
+        *reinterpret_cast<f32x4*>(at) = f32x4{dv[u4], dv[u4 + 1], dv[u4 + 2], dv[u4 + 3]};
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if ((act >> (u4 + u)) & 1) at[u] = dv[u4 + u];
+      }
     }
   }
   // dK = dS^T Q / sqrt d: lane (n, hl) holds d column cb*32 + n, keys kh*32 + 8(r/4) + 4hl + r%4
@@ -277,7 +346,9 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int key = k0 + kh * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      if (key < T) dK[base + (size_t)key * D + cb * 32 + n] = dk[c][r] * rs;
+      if (key >= T) continue;
+      float* at = dK + base + (size_t)key * D + cb * 32 + n;
+      *at = all ? dk[c][r] * rs : *at + dk[c][r] * rs;  // wide only: add to the matrix-core dK
     }
   }
 }
@@ -289,9 +360,15 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ lse,
     const float* __restrict__ G, float* __restrict__ dQ, float* __restrict__ dbp, int H, int T,
-    int ntile, const int* __restrict__ run_if) {
+    int ntile, const int* __restrict__ flag, const float* __restrict__ splitf) {
   using C = Bw<D>;
-  if (run_if && *run_if == 0) return;
+  static_assert(D <= kThreads && C::JPT <= 32, "channel masks");
+  const int mode = exact_mode(flag);
+  if (mode == kExactNone) return;
+  const bool all = mode == kExactAll;
+  if (!all && !__syncthreads_or(threadIdx.x < D &&
+                                splitf[(blockIdx.x / ntile) * D + threadIdx.x] == kWide))
+    return;
   __shared__ __align__(16) QSmem<D> sm;
   __shared__ float lse2[kTile];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hl = lane >> 5;
@@ -300,15 +377,20 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
   const int q0 = qb * kTile;
   const size_t base = (size_t)bh * T * D;
 
-  // posterior-loop mapping: query qi, channels j0..
+  // posterior-loop mapping: query qi, channels j0..; bit u of act: channel
+  // j0 + u is taken here (a channel not taken has W = 0 and no posterior)
   const int qi = tid >> 2, jg = tid & 3, j0 = jg * C::JPT;
+  unsigned act = 0;
+#pragma unroll
+  for (int u = 0; u < C::JPT; ++u)
+    if (all || splitf[bh * D + j0 + u] == kWide) act |= 1u << u;
   float fb[C::JPT], w[C::JPT], dsum = 0.f;
   float zs[C::JPT], xs[C::JPT];  // sum_i q^, sum_i q^ (beta log2e)(v - F^)
   float ps = 0.f;                // sum_i p^
 #pragma unroll
   for (int u = 0; u < C::JPT; ++u) {
     const float b = beta[h * D + j0 + u];
-    const bool ok = q0 + qi < T;
+    const bool ok = q0 + qi < T && ((act >> u) & 1);
     const float g = ok ? G[base + (size_t)(q0 + qi) * D + j0 + u] : 0.f;
     const float f = ok ? F[base + (size_t)(q0 + qi) * D + j0 + u] : 0.f;
     fb[u] = b * kLog2e * f;
@@ -331,12 +413,25 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
     const int k0 = kb * kTile;
     __syncthreads();
     stage_tile<D>(K + base, k0, T, sm.kt, sm.kT);
-    for (int e = tid; e < kTile * D / 8; e += kThreads) {
-      const int i = e / (D / 8), c8 = (e % (D / 8)) * 8;
-      bf16x8 x = {};
-      if (k0 + i < T) x = *reinterpret_cast<const bf16x8*>(V + base + (size_t)(k0 + i) * D + c8);
+    {
+      // thread tid handles channels c8.. of rows tid / (D/8) + it * (kThreads / (D/8))
+      constexpr int N = kTile * D / 8 / kThreads, RPI = kThreads / (D / 8);
+      static_assert(N * kThreads == kTile * D / 8, "whole rounds");
+      const int c8 = (tid % (D / 8)) * 8, i0 = tid / (D / 8);
+      bf16x8 x[N];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) sm.bv[i * D + c8 + u] = beta[h * D + c8 + u] * kLog2e * (float)x[u];
+      for (int it = 0; it < N; ++it) {
+        const int i = i0 + it * RPI;
+        x[it] = bf16x8{};
+        if (k0 + i < T) x[it] = *reinterpret_cast<const bf16x8*>(V + base + (size_t)(k0 + i) * D + c8);
+      }
+#pragma unroll
+      for (int it = 0; it < N; ++it) {
+        const int i = i0 + it * RPI;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          sm.bv[i * D + c8 + u] = beta[h * D + c8 + u] * kLog2e * (float)x[it][u];
+      }
     }
     __syncthreads();
     block_logp<D>(sm, lse2, q0, k0, T);
@@ -350,11 +445,12 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
         ps += exp2_hw(lp);
 #pragma unroll
         for (int u4 = 0; u4 < C::JPT; u4 += 4) {
+          if (!((act >> u4) & 0xfu)) continue;
           const f32x4 bv4 = *reinterpret_cast<const f32x4*>(sm.bv + i * D + j0 + u4);
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const float x = bv4[u] - fb[u4 + u];
-            const float e = exp2_hw(lp + x);
+            const float e = ((act >> (u4 + u)) & 1) ? exp2_hw(lp + x) : 0.f;
             part = fmaf(w[u4 + u], e, part);
             zs[u4 + u] += e;
             xs[u4 + u] = fmaf(e, x, xs[u4 + u]);
@@ -393,7 +489,9 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int t = q0 + th * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-      if (t < T) dQ[base + (size_t)t * D + cb * 32 + n] = dq[c][r] * rs;
+      if (t >= T) continue;
+      float* at = dQ + base + (size_t)t * D + cb * 32 + n;
+      *at = all ? dq[c][r] * rs : *at + dq[c][r] * rs;  // wide only: add to the matrix-core dQ
     }
   }
 
@@ -555,7 +653,7 @@ __device__ __forceinline__ void settle(float x) { asm volatile("" ::"v"(x)); }
 
 
 // Per 64-row tile of V, the max and min of each channel (for the channel
-// shifts and forms); the first workgroup clears the fallback flag.
+// shifts and forms); the first workgroup clears the fallback flags.
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_vstats_kernel(const bf16* __restrict__ V,
                                                               float* __restrict__ vmx,
@@ -567,7 +665,7 @@ __global__ __launch_bounds__(kThreads) void bwd_vstats_kernel(const bf16* __rest
   const int tid = threadIdx.x, j = tid % D, rg = tid / D;
   const int tb = blockIdx.x % ntile, bh = blockIdx.x / ntile;
   const int r0 = tb * kTile;
-  if (blockIdx.x == 0 && tid == 0) flag[0] = 0;
+  if (blockIdx.x == 0 && tid < 2) flag[tid] = 0;
   const bf16* Vh = V + (size_t)bh * T * D;
   float a = -INFINITY, b = INFINITY;
   for (int r = rg; r < kTile; r += RG)
@@ -590,8 +688,9 @@ __global__ __launch_bounds__(kThreads) void bwd_vstats_kernel(const bf16* __rest
 }
 
 // Channel constants of a (b, h) from the per-tile max / min of V: c_j, the
-// form, and bl_j, into LDS; with publish, also to global memory, and a
-// channel whose range is beyond the matrix-core form raises the flag.
+// form (kSplitForm, kPlainForm, or kWide for a channel whose range is beyond
+// the matrix-core form: the element-wise pass takes it), and bl_j, into LDS;
+// with publish, also to global memory, and a wide channel raises flag[1].
 template <int D>
 __device__ __forceinline__ void channel_consts(const float* __restrict__ beta,
                                                const float* __restrict__ vmx,
@@ -606,14 +705,14 @@ __device__ __forceinline__ void channel_consts(const float* __restrict__ beta,
       b = fminf(b, vmn[((size_t)bh * ntile + k) * D + j]);
     }
     const float l = beta[h * D + j] * kLog2e, range = l * (a - b);
-    const float sp = range <= kSplit ? 1.f : 0.f;
+    const float sp = !(range <= kRange) ? kWide : range <= kSplit ? kSplitForm : kPlainForm;
     c[j] = l * a;
     split[j] = sp;
     bl[j] = l;
     if (publish) {
       cg[bh * D + j] = l * a;
       splitf[bh * D + j] = sp;
-      if (!(range <= kRange)) flag[0] = 1;
+      if (sp == kWide) flag[1] = 1;
     }
   }
 }
@@ -659,9 +758,10 @@ __global__ __launch_bounds__(kThreads) void bwd_prepk_kernel(
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int j = c8 + u;
-      const bool sp = split[j] != 0.f;
+      // a wide channel contributes nothing here: Y = 0, W U = 0
+      const bool sp = split[j] == kSplitForm, on = live && split[j] != kWide;
       float y = 0.f;
-      if (live) {
+      if (on) {
         const float xv = fmaf(bl[j], (float)vx[u], -c[j]);
         y = sp ? expm1f(xv * kLn2) : exp2_hw(xv);
       }
@@ -669,8 +769,8 @@ __global__ __launch_bounds__(kThreads) void bwd_prepk_kernel(
       split_bf16(y, a, b);
       hi[u] = a;
       lo[u] = b;
-      const float w = g4[u >> 2][u & 3] / beta[h * D + j];
-      const float x = live ? c[j] - bl[j] * f4[u >> 2][u & 3] : 0.f;  // log2 U
+      const float w = on ? g4[u >> 2][u & 3] / beta[h * D + j] : 0.f;
+      const float x = on ? c[j] - bl[j] * f4[u >> 2][u & 3] : 0.f;  // log2 U
       const float wu = w * exp2_hw(fminf(x, kGuardU));
       if (!(x <= kGuardU && fabsf(wu) < kGuardW)) bad = true;
       cs += sp ? w * expm1f(x * kLn2) : -w;
@@ -937,12 +1037,13 @@ __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int j = c8 + u;
-      const bool sp = split[j] != 0.f;
-      const float g = g4[u >> 2][u & 3], f = f4[u >> 2][u & 3], sa = z4[u >> 2][u & 3];
+      // a wide channel contributes nothing here (W U' = 0, no G F term)
+      const bool sp = split[j] == kSplitForm, on = live && split[j] != kWide;
+      const float g = on ? g4[u >> 2][u & 3] : 0.f, f = f4[u >> 2][u & 3], sa = z4[u >> 2][u & 3];
       const float rb = 1.f / beta[h * D + j], w = g * rb;
-      const float x = live ? c[j] - bl[j] * f : 0.f;  // log2 U
-      float lz = 0.f;                                 // ln(Z/P): F = F^ + ln(Z/P)/beta
-      if (live) {
+      const float x = on ? c[j] - bl[j] * f : 0.f;  // log2 U
+      float lz = 0.f;                               // ln(Z/P): F = F^ + ln(Z/P)/beta
+      if (on) {
         if (sp) {
           const float um1 = expm1f(x * kLn2);
           lz = log1pf(um1 + (um1 + 1.f) * sa);
@@ -1179,7 +1280,8 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_fast_kernel(
   }
 }
 
-// dbeta from the per-tile partial sums: the exact pass's when it ran, else
+// dbeta from the per-tile partial sums: the element-wise pass's for the
+// channels it took (every channel, or the wide ones of a (b, h)), else
 // (sum v dV - sum G F) / beta from the matrix-core pass.  One workgroup per
 // (h, 32 channels); its 8 thread rows split the (b, tile) partials and meet
 // in LDS.
@@ -1189,22 +1291,27 @@ __global__ __launch_bounds__(256) void dbeta_kernel(const float* __restrict__ ex
                                                     const float* __restrict__ gf,
                                                     const float* __restrict__ beta,
                                                     const int* __restrict__ flag,
+                                                    const float* __restrict__ splitf,
                                                     float* __restrict__ dbeta, int B, int H,
                                                     int ntile) {
   __shared__ double part[8][32];
   const int h = blockIdx.x, j = blockIdx.y * 32 + (threadIdx.x & 31), row = threadIdx.x >> 5;
-  const bool ex = flag[0] != 0;
-  double s = 0.0;
+  const bool all = flag[0] != 0;
+  double se = 0.0, sm = 0.0;  // element-wise partials; matrix-core partials (times beta)
   for (int u = row; u < B * ntile; u += 8) {
     const int b = u / ntile, c = u % ntile;
     const size_t at = (((size_t)b * H + h) * ntile + c) * D + j;
-    s += ex ? (double)exact[at] : (double)vdv[at] - (double)gf[at];
+    if (all || splitf[((size_t)b * H + h) * D + j] == kWide)
+      se += (double)exact[at];
+    else
+      sm += (double)vdv[at] - (double)gf[at];
   }
+  double s = se + sm / (double)beta[h * D + j];
   part[row][threadIdx.x & 31] = s;
   __syncthreads();
   if (row == 0) {
     for (int r = 1; r < 8; ++r) s += part[r][threadIdx.x & 31];
-    dbeta[h * D + j] = (float)(ex ? s : s / (double)beta[h * D + j]);
+    dbeta[h * D + j] = (float)s;
   }
 }
 
@@ -1269,20 +1376,22 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
                        wh, wl, cst, dK, dV, vdv, H, T, ntile);
     e = hipGetLastError();
   }
-  // exact element-wise passes: they return at once unless a block raised the flag
+  // element-wise passes: they return at once unless a wide channel or a
+  // failed guard raised a flag; wide channels only add to dQ / dK and write
+  // their own dV columns, a failed guard replaces every gradient
   if (e == hipSuccess) {
     hipLaunchKernelGGL(bwd_kv_kernel<D>, grid, blk, 0, stream, q, k, v, beta, out, lse, dout, dK, dV,
-                       H, T, ntile, flag);
+                       H, T, ntile, flag, splitf);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
     hipLaunchKernelGGL(bwd_q_kernel<D>, grid, blk, 0, stream, q, k, v, beta, out, lse, dout, dQ,
-                       exact, H, T, ntile, flag);
+                       exact, H, T, ntile, flag, splitf);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
     hipLaunchKernelGGL(dbeta_kernel<D>, dim3((unsigned)H, D / 32), dim3(256), 0, stream, exact, vdv,
-                       gfp, beta, flag, dbeta, B, H, ntile);
+                       gfp, beta, flag, splitf, dbeta, B, H, ntile);
     e = hipGetLastError();
   }
   const hipError_t f = workspace_free(ws, stream);

@@ -146,9 +146,9 @@ def test_backward_deterministic(fem):
 
 
 def test_backward_exact_fallback(fem):
-    """Values spread over [-5, 5] with beta = 16 give channels a beta-scaled
-    range (16 log2(e) 10 = 231) beyond the matrix-core form's fp32 bound, so
-    the call reruns the element-wise pass."""
+    """Values spread over [-5, 5] with beta = 16 give every channel a
+    beta-scaled range (16 log2(e) 10 = 231) beyond the matrix-core form's
+    fp32 bound, so the element-wise kernels take every channel."""
     say("backward fallback case: B1 H2 T300 d64, v in {-5, +5, N(0,1)}, beta 16, seed 13500")
     q, k, _, _, g = draw(13500, 1, 2, 300, 64)
     rng = np.random.default_rng(13501)
@@ -161,3 +161,48 @@ def test_backward_exact_fallback(fem):
     want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
                                     b.double().numpy(), g.double().numpy())
     check_grads(grads, want, "fallback", dbeta_floor(v, b, g))
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_backward_some_wide_channels(fem, d):
+    """A few channels per head get beta = 16 and values spread over [-5, 5]
+    (range 231 in log2 units): the element-wise kernels take those channels
+    only and add their part to the matrix-core dQ and dK; the other channels
+    (beta log-uniform in [0.1, 8]) stay on the matrix cores."""
+    seed = 13700 + d
+    say(f"backward mixed wide channels: B2 H2 T333 d{d}, seed {seed}")
+    q, k, v, b, g = draw(seed, 2, 2, 333, d)
+    wide = {0: [3, 17], 1: [d - 1]}
+    v = v.float().numpy().copy()
+    b = b.clone()
+    for h, chans in wide.items():
+        for j in chans:
+            v[:, h, ::7, j] = 5.0
+            v[:, h, 3::11, j] = -5.0
+            b[h, j] = 16.0
+    v = torch.from_numpy(v).to(torch.bfloat16)
+    _, _, grads = run(fem, q, k, v, b, g)
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, f"mixed d{d}", dbeta_floor(v, b, g))
+    # the wide channels' dV columns, against their own scale
+    for h, chans in wide.items():
+        for j in chans:
+            err = np.abs(grads[2][:, h, :, j] - want[2][:, h, :, j]).max()
+            scale = np.abs(want[2][:, h, :, j]).max()
+            say(f"wide channel h{h} j{j} dv: max err {err:.3e}, scale {scale:.3e}")
+            assert err <= TOL * scale + ATOL
+
+
+def test_backward_guard_fallback(fem):
+    """Output gradients of size 2^98 push W U = (G / beta) 2^{c - bl F} past
+    2^124 (the matrix-core form's fp32 guard) on early rows, so the whole call
+    is redone by the element-wise kernels; every gradient stays inside fp32."""
+    say("backward guard fallback: B1 H2 T200 d64, beta 8, G * 2^98, seed 13800")
+    q, k, v, _, g = draw(13800, 1, 2, 200, 64)
+    b = torch.full((2, 64), 8.0)
+    g = g * 2.0 ** 98
+    _, _, grads = run(fem, q, k, v, b, g)
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, "guard fallback", dbeta_floor(v, b, g))
