@@ -66,6 +66,10 @@ __device__ __forceinline__ unsigned lds_addr(const void* p) {
 // barrier that publishes the buffer.  The compiler reserves m0 and ignores
 // its clobber here: the kernels that use these loads contain no other
 // instruction that reads m0 (their assembly shows m0 written only here).
+// The clobber stays as documentation; its "reserved register" warning is
+// silenced for these two functions only.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const void* src, void* dst) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :
@@ -78,6 +82,7 @@ __device__ __forceinline__ void dma4(const void* src, void* dst) {
                : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
                : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 // ---- permuted contraction order and swizzled tiles ------------------------
 //

@@ -55,7 +55,7 @@
 //            tile k on the vector pipe;
 //   phase 2: PV(k-1) (hi, lo and the row-sum product)  ||  softmax of tile k
 //            (the scores phase 1 just produced).
-// The instruction mix of each phase is pinned with scheduling groups.  Row
+// The instruction order of each phase is pinned with scheduling barriers.  Row
 // and column rescales of the accumulator are rare; they are deferred to just
 // before the next PV so that neither phase needs a branch.  softmax(k)
 // overwrites the P registers behind PV(k-1) as it issues.  K(k+1) and
@@ -81,11 +81,6 @@ constexpr float kUnderflow = 0x1p-64f;
 constexpr int kFem = 0;    // F at beta
 constexpr int kMean = 1;   // mu
 constexpr int kGated = 2;  // g * ((1 - lam) mu + lam F), mu read from out
-
-// Instruction classes of __builtin_amdgcn_sched_group_barrier.
-constexpr int kSgVALU = 0x002 | 0x400;  // vector ALU, transcendental included
-constexpr int kSgMFMA = 0x008;
-constexpr int kSgDSRead = 0x100;
 
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
