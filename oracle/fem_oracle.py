@@ -51,7 +51,7 @@ def elu_plus_one(x: np.ndarray) -> np.ndarray:
     """phi(x) = elu(x) + 1: x + 1 for x > 0, exp(x) for x <= 0.
 
     The paper leaves the nonnegative feature map of the linear prior open
-    (Appendix "Selection distributions ..."); this build fixes phi = elu + 1.
+    (Appendix "Selection distributions ..."); the oracle fixes phi = elu + 1.
     """
     x = np.asarray(x, dtype=np.float64)
     return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))
