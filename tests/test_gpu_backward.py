@@ -163,7 +163,7 @@ def test_backward_exact_fallback(fem):
     check_grads(grads, want, "fallback", dbeta_floor(v, b, g))
 
 
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("d", [32, 64, 128])
 def test_backward_some_wide_channels(fem, d):
     """A few channels per head get beta = 16 and values spread over [-5, 5]
     (range 231 in log2 units): the element-wise kernels take those channels
@@ -206,3 +206,20 @@ def test_backward_guard_fallback(fem):
     want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
                                     b.double().numpy(), g.double().numpy())
     check_grads(grads, want, "guard fallback", dbeta_floor(v, b, g))
+
+
+def test_backward_wide_deterministic(fem):
+    """The element-wise kernels that add the wide channels' part write with
+    plain stores in a fixed order: two calls give the same bits."""
+    say("backward wide-channel determinism: B1 H2 T257 d64, seed 13900")
+    q, k, v, b, g = draw(13900, 1, 2, 257, 64)
+    v = v.float().numpy().copy()
+    v[:, 1, ::5, 9] = 5.0
+    v[:, 1, 2::9, 9] = -5.0
+    v = torch.from_numpy(v).to(torch.bfloat16)
+    b = b.clone()
+    b[1, 9] = 16.0
+    a = run(fem, q, k, v, b, g)[2]
+    c = run(fem, q, k, v, b, g)[2]
+    for x, y in zip(a, c):
+        assert np.array_equal(x, y)
