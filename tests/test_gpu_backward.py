@@ -223,3 +223,26 @@ def test_backward_wide_deterministic(fem):
     c = run(fem, q, k, v, b, g)[2]
     for x, y in zip(a, c):
         assert np.array_equal(x, y)
+
+
+def test_backward_wide_in_one_batch(fem):
+    """beta = 16 on one channel of head 1; in batch 0 its values spread over
+    [-5, 5] (wide), in batch 1 they are scaled to a range of ~2 (beta-scaled
+    ~45, matrix cores), so dbeta of that channel adds the element-wise pass's
+    partial sums of batch 0 to the matrix-core sums of batch 1."""
+    say("backward wide in one batch: B2 H2 T300 d64, seed 14000")
+    q, k, v, b, g = draw(14000, 2, 2, 300, 64)
+    v = v.float().numpy().copy()
+    v[0, 1, ::6, 20] = 5.0
+    v[0, 1, 1::10, 20] = -5.0
+    v[1, 1, :, 20] *= 0.3
+    v = torch.from_numpy(v).to(torch.bfloat16)
+    b = b.clone()
+    b[1, 20] = 16.0
+    _, _, grads = run(fem, q, k, v, b, g)
+    want = oracle.fem_softmax_grads(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                    b.double().numpy(), g.double().numpy())
+    check_grads(grads, want, "wide in batch 0 only", dbeta_floor(v, b, g))
+    err = abs(grads[3][1, 20] - want[3][1, 20])
+    say(f"dbeta[1, 20]: {grads[3][1, 20]:.6e} vs {want[3][1, 20]:.6e} (err {err:.3e})")
+    assert err <= TOL * abs(want[3][1, 20]) + dbeta_floor(v, b, g)[1, 20] + ATOL
