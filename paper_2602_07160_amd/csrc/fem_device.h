@@ -63,26 +63,39 @@ __device__ __forceinline__ unsigned lds_addr(const void* p) {
 // reads as completing out of order (every read then waits for all earlier
 // ones) and waits for the whole load queue before transposing reads.  The
 // caller waits for completion explicitly (s_waitcnt vmcnt(0)) before the
-// barrier that publishes the buffer.  The compiler reserves m0 and ignores
-// its clobber here: the kernels that use these loads contain no other
-// instruction that reads m0 (their assembly shows m0 written only here).
-// The clobber stays as documentation; its "reserved register" warning is
-// silenced for these two functions only.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
+// barrier that publishes the buffer.
+//
+// The load takes its LDS address from m0.  An SALU write of m0 needs one
+// wait state before an LDS-DMA load reads it, and the hazard recognizer
+// does not look inside inline assembly, so the block carries its own
+// s_nop.  The compiler also treats m0 as reserved and ignores a clobber of
+// it, so the block saves m0 into a scratch SGPR and restores it after the
+// load has issued (the load reads m0 at issue): whatever the compiler keeps
+// in m0 survives the block.
 __device__ __forceinline__ void dma16(const void* src, void* dst) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
-               : "memory", "m0");
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
+      : "memory");
 }
 __device__ __forceinline__ void dma4(const void* src, void* dst) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
-               :
-               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
-               : "memory", "m0");
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
+      : "memory");
 }
-#pragma clang diagnostic pop
 
 // ---- permuted contraction order and swizzled tiles ------------------------
 //
