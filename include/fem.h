@@ -25,6 +25,15 @@
  *   - Every tensor argument is a DEVICE pointer (HIP device memory, e.g.
  *     torch tensors' data_ptr()).  The caller owns every buffer; the library
  *     keeps no pointer after the call returns.
+ *   - The library allocates no memory and holds no global state, so calls
+ *     are thread-safe and re-entrant.  An entry point that needs scratch
+ *     memory takes a caller-provided workspace `ws` of `ws_bytes` bytes
+ *     (device memory, 256-byte aligned) and has a query,
+ *     fem_*_workspace_bytes(...), that returns the exact size it needs for
+ *     the given sizes (0: none, and `ws` may be NULL).  The workspace holds
+ *     intermediate results only until the call's kernels have run on
+ *     `stream`; it needs no initialisation, and calls that run at the same
+ *     time need workspaces of their own.
  *   - Layout: contiguous row-major [B, H, T, width] (width fastest); Q, K, V
  *     16-byte aligned.  beta is [H, width_v] float32, shared over B and T.
  *   - out is always float32 [B, H, T, width_v] and must not alias an input.
@@ -61,8 +70,11 @@ typedef enum {
   FEM_ERR_NULLPTR = 1,      /* a required pointer is NULL                      */
   FEM_ERR_SHAPE = 2,        /* B, H or T <= 0, or a size overflows             */
   FEM_ERR_UNSUPPORTED = 3,  /* width, chunk or dtype outside the supported set */
-  FEM_ERR_ALIGN = 4,        /* a tensor argument is not 16-byte aligned        */
-  FEM_ERR_HIP = 5           /* a HIP call or kernel launch failed              */
+  FEM_ERR_ALIGN = 4,        /* a tensor argument is not 16-byte aligned, or ws
+                               is not 256-byte aligned                         */
+  FEM_ERR_HIP = 5,          /* a HIP call or kernel launch failed              */
+  FEM_ERR_WORKSPACE = 6     /* ws is NULL or ws_bytes is below the workspace
+                               query's value                                   */
 } fem_status;
 
 /*
@@ -135,15 +147,20 @@ int fem_softmax_fwd_ex(const void* Q, const void* K, const void* V,
  *   dtype  : FEM_DTYPE_BF16
  *
  * fp32 arithmetic with a per-channel joint log-sum-exp (no shared shift).
- * The keys are split over workgroups whose partial results live in a
- * stream-ordered workspace of 8 * (d_v + 1) bytes per split and (b, h) (at
- * most 4 * compute units / (B * H) splits, each a multiple of 64 keys), taken
- * from the library's pool as in fem_linear_fwd.  Returns a fem_status.
+ * The keys are split over workgroups: S = ceil(L / (64 n)) splits of n =
+ * ceil(ceil(L / 64) / s0) key blocks of 64 each, s0 = min(ceil(1024 / (B H)),
+ * ceil(L / 64)).  Their partial results need a workspace of
+ *
+ *   fem_softmax_decode_workspace_bytes(B, H, L, d_qk, d_v) = 8 * B * H * S * (d_v + 1)
+ *
+ * bytes (0 for arguments outside the supported set).  Returns a fem_status.
  */
+size_t fem_softmax_decode_workspace_bytes(int B, int H, int L, int d_qk, int d_v);
+
 int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
                        const int* lens, const float* beta, float* out,
                        int B, int H, int L, int d_qk, int d_v, int dtype,
-                       hipStream_t stream);
+                       void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Training pair of the causal softmax-prior read (bf16 inputs, d = 32, 64 or
@@ -176,19 +193,28 @@ int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
  * channel still leave fp32's range (an output gradient near 2^100), the
  * element-wise pass redoes the whole call (~34x slower).  dbeta is
  * formed from the normalised posterior sums, so the forward's rounding of
- * out cancels from it.  A workspace of about 8 * B * H * T * d +
- * 20 * B * H * ceil(T / 64) * d bytes comes from the library's pool as in
- * fem_linear_fwd.  All pointers 16-byte aligned;
- * outputs must not alias inputs.  Returns a fem_status.
+ * out cancels from it.  The passes exchange intermediate results through a
+ * workspace of
+ *
+ *   fem_softmax_bwd_workspace_bytes(B, H, T, d) =
+ *       256 + round_up_256(4 * (B H T + 2 B H d + 5 B H n d + B H T d + B H Tp))
+ *           + 8 * B H Tp d,        n = ceil(T / 64), Tp = 64 n
+ *
+ * bytes (about 12 B H T d: at B8 H16 T4096 d128, 829 MB; 0 for arguments
+ * outside the supported set).  All pointers 16-byte aligned; outputs must not
+ * alias inputs.  Returns a fem_status.
  */
 int fem_softmax_fwd_train(const void* Q, const void* K, const void* V,
                           const float* beta, float* out, float* lse,
                           int B, int H, int T, int d, int dtype, hipStream_t stream);
 
+size_t fem_softmax_bwd_workspace_bytes(int B, int H, int T, int d);
+
 int fem_softmax_bwd(const void* Q, const void* K, const void* V,
                     const float* beta, const float* out, const float* lse,
                     const float* dout, float* dQ, float* dK, float* dV, float* dbeta,
-                    int B, int H, int T, int d, int dtype, hipStream_t stream);
+                    int B, int H, int T, int d, int dtype,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Two-level gated FEM read with the causal softmax prior (Sec. "Two-Level
@@ -235,18 +261,25 @@ int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V,
  *             beyond rounding.  Other values return FEM_ERR_UNSUPPORTED.
  *   dtype   : FEM_DTYPE_BF16
  *
- * The scan keeps per-segment states in a stream-ordered workspace of
- * 16.9 KiB per 512 tokens per (b, h), taken from and returned to a
- * library-owned memory pool of the current device on `stream` (the pool keeps
- * its memory until the process ends, so repeated calls of one size do not
- * reach the driver's allocator); an allocation failure returns FEM_ERR_HIP.
+ * The scan runs in segments of c = ceil(ceil(T / 64) / w) chunks, w =
+ * max(1, floor(512 / (B H))), S = ceil(ceil(T / 64) / c) segments per (b, h).
+ * With S > 1 the segments' own states and the states entering them need a
+ * workspace of
+ *
+ *   fem_linear_workspace_bytes(B, H, T, d_k, d_v, chunk) = 2 * 4 * B * H * S * 4224
+ *
+ * bytes (a state is the 64 x 64 matrix, the 64-entry normaliser and the 64
+ * channel shifts, 4224 floats); with S = 1 it is 0 and ws may be NULL.  0 is
+ * also returned for arguments outside the supported set.
  *
  * Returns a fem_status.
  */
+size_t fem_linear_workspace_bytes(int B, int H, int T, int d_k, int d_v, int chunk);
+
 int fem_linear_fwd(const void* Q, const void* K, const void* V,
                    const float* beta, float* out,
                    int B, int H, int T, int d_k, int d_v, int chunk,
-                   int dtype, hipStream_t stream);
+                   int dtype, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Causal GLA-prior FEM read as an O(T) chunked scan (Appendix "Gated Linear
@@ -269,13 +302,19 @@ int fem_linear_fwd(const void* Q, const void* K, const void* V,
  *   out     : [B, H, T, d_v] float32
  *   d_k, d_v: 64 (both);  chunk: 64;  dtype: FEM_DTYPE_BF16
  *
- * Workspace as fem_linear_fwd (plus 256 B per segment and (b, h)).  Returns a
- * fem_status.
+ * Workspace as fem_linear_fwd, each state carrying also its segment's total
+ * log-decay per key channel (4288 floats):
+ *
+ *   fem_gla_workspace_bytes(B, H, T, d_k, d_v, chunk) = 2 * 4 * B * H * S * 4288
+ *
+ * for S > 1, else 0.  Returns a fem_status.
  */
+size_t fem_gla_workspace_bytes(int B, int H, int T, int d_k, int d_v, int chunk);
+
 int fem_gla_fwd(const void* Q, const void* K, const void* V, const float* G,
                 const float* beta, float* out,
                 int B, int H, int T, int d_k, int d_v, int chunk,
-                int dtype, hipStream_t stream);
+                int dtype, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Static, NUL-terminated name of a status code (never NULL). */
 const char* fem_status_str(int status);

@@ -19,8 +19,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfem.so")
 FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 
 EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_fwd_train", "fem_softmax_bwd",
-           "fem_softmax_gated_fwd", "fem_softmax_decode", "fem_linear_fwd", "fem_gla_fwd",
-           "fem_status_str")
+           "fem_softmax_bwd_workspace_bytes", "fem_softmax_gated_fwd", "fem_softmax_decode",
+           "fem_softmax_decode_workspace_bytes", "fem_linear_fwd", "fem_linear_workspace_bytes",
+           "fem_gla_fwd", "fem_gla_workspace_bytes", "fem_status_str")
 
 FEM_FLAG_ENCODER = 1
 FEM_FLAG_OUT_BF16 = 2
@@ -41,23 +42,32 @@ def load() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2602_07160_amd.build`")
         lib = ctypes.CDLL(LIB_PATH)
-        vp, i, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p
+        vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t
         lib.fem_softmax_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_fwd.restype = i
         lib.fem_softmax_fwd_ex.argtypes = [vp, vp, vp, f, vp, i, i, i, i, i, i, i, vp]
         lib.fem_softmax_fwd_ex.restype = i
-        lib.fem_softmax_decode.argtypes = [vp, vp, vp, vp, f, f, i, i, i, i, i, i, vp]
+        lib.fem_softmax_decode.argtypes = [vp, vp, vp, vp, f, f, i, i, i, i, i, i, vp, sz, vp]
         lib.fem_softmax_decode.restype = i
+        lib.fem_softmax_decode_workspace_bytes.argtypes = [i, i, i, i, i]
+        lib.fem_softmax_decode_workspace_bytes.restype = sz
         lib.fem_softmax_gated_fwd.argtypes = [vp, vp, vp, f, f, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_gated_fwd.restype = i
-        lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp]
+        lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp, sz, vp]
         lib.fem_linear_fwd.restype = i
-        lib.fem_gla_fwd.argtypes = [vp, vp, vp, f, f, f, i, i, i, i, i, i, i, vp]
+        lib.fem_linear_workspace_bytes.argtypes = [i, i, i, i, i, i]
+        lib.fem_linear_workspace_bytes.restype = sz
+        lib.fem_gla_fwd.argtypes = [vp, vp, vp, f, f, f, i, i, i, i, i, i, i, vp, sz, vp]
         lib.fem_gla_fwd.restype = i
+        lib.fem_gla_workspace_bytes.argtypes = [i, i, i, i, i, i]
+        lib.fem_gla_workspace_bytes.restype = sz
         lib.fem_softmax_fwd_train.argtypes = [vp, vp, vp, f, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_fwd_train.restype = i
-        lib.fem_softmax_bwd.argtypes = [vp, vp, vp, f, f, f, f, f, f, f, f, i, i, i, i, i, vp]
+        lib.fem_softmax_bwd.argtypes = [vp, vp, vp, f, f, f, f, f, f, f, f, i, i, i, i, i, vp, sz,
+                                        vp]
         lib.fem_softmax_bwd.restype = i
+        lib.fem_softmax_bwd_workspace_bytes.argtypes = [i, i, i, i]
+        lib.fem_softmax_bwd_workspace_bytes.restype = sz
         lib.fem_status_str.argtypes = [i]
         lib.fem_status_str.restype = ctypes.c_char_p
         _lib = lib
@@ -81,6 +91,26 @@ def _dev_tensor(x: torch.Tensor, name: str, dtype=None) -> torch.Tensor:
     if dtype is not None and x.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, got {x.dtype}")
     return x
+
+
+def _workspace(nbytes: int, device, ws, stream):
+    """(tensor, pointer, size) of the workspace for a call that needs
+    ``nbytes``: the caller's uint8 GPU tensor ``ws`` if given, else a new one
+    from torch's allocator (its blocks are 512-byte aligned), allocated on the
+    stream the call runs on so that torch does not hand the memory out again
+    before the call's kernels have run.  (None, None, 0) when nothing is
+    needed."""
+    if ws is not None:
+        _dev_tensor(ws, "ws", torch.uint8)
+        return ws, ws.data_ptr(), ws.numel()
+    if nbytes == 0:
+        return None, None, 0
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    if not isinstance(s, torch.cuda.Stream):
+        s = torch.cuda.ExternalStream(int(s), device=device)
+    with torch.cuda.stream(s):
+        t = torch.empty(nbytes, device=device, dtype=torch.uint8)
+    return t, t.data_ptr(), nbytes
 
 
 def _stream_handle(device, stream) -> int:
@@ -150,10 +180,13 @@ def fem_softmax_fwd_ex(q, k, v, beta, out=None, causal: bool = True, out_dtype=t
     return out
 
 
-def fem_softmax_decode(q, k_cache, v_cache, beta, lens=None, out=None, stream=None) -> torch.Tensor:
+def fem_softmax_decode(q, k_cache, v_cache, beta, lens=None, out=None, ws=None,
+                       stream=None) -> torch.Tensor:
     """One decoding step: q [B, H, d_qk] reads the first lens[b] rows of the
     caches k_cache [B, H, L, d_qk], v_cache [B, H, L, d_v] (bf16).  lens: [B]
-    int32 GPU tensor or None (all L).  Returns [B, H, d_v] fp32."""
+    int32 GPU tensor or None (all L).  ws: optional uint8 GPU workspace of at
+    least fem_softmax_decode_workspace_bytes(...) bytes.  Returns [B, H, d_v]
+    fp32."""
     lib = load()
     _dev_tensor(q, "q", torch.bfloat16)
     _dev_tensor(k_cache, "k_cache", torch.bfloat16)
@@ -177,11 +210,13 @@ def fem_softmax_decode(q, k_cache, v_cache, beta, lens=None, out=None, stream=No
     _dev_tensor(out, "out", torch.float32)
     if tuple(out.shape) != (B, H, dv):
         raise ValueError("out must be [B, H, d_v]")
+    need = lib.fem_softmax_decode_workspace_bytes(B, H, L, dqk, dv)
     with torch.cuda.device(q.device):
+        wst, wsp, wsn = _workspace(need, q.device, ws, stream)
         rc = lib.fem_softmax_decode(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                     None if lens is None else lens.data_ptr(), beta.data_ptr(),
                                     out.data_ptr(), B, H, L, dqk, dv, FEM_DTYPE[q.dtype],
-                                    _stream_handle(q.device, stream))
+                                    wsp, wsn, _stream_handle(q.device, stream))
     _check(rc)
     return out
 
@@ -221,9 +256,12 @@ def fem_softmax_gated_fwd(q, k, v, beta_max, lam, gate=None, out=None, stream=No
     return out
 
 
-def fem_linear_fwd(q, k, v, beta, out=None, chunk: int = 64, stream=None) -> torch.Tensor:
+def fem_linear_fwd(q, k, v, beta, out=None, chunk: int = 64, ws=None,
+                   stream=None) -> torch.Tensor:
     """Causal linear-prior (phi = elu + 1) FEM read.  q, k: [B, H, T, d_k];
-    v: [B, H, T, d_v] bf16; beta: [H, d_v] fp32.  Returns [B, H, T, d_v] fp32."""
+    v: [B, H, T, d_v] bf16; beta: [H, d_v] fp32; ws: optional uint8 GPU
+    workspace of at least fem_linear_workspace_bytes(...) bytes.  Returns
+    [B, H, T, d_v] fp32."""
     lib = load()
     if q.dtype not in FEM_DTYPE:
         raise ValueError(f"unsupported dtype {q.dtype}")
@@ -242,15 +280,18 @@ def fem_linear_fwd(q, k, v, beta, out=None, chunk: int = 64, stream=None) -> tor
     _dev_tensor(out, "out", torch.float32)
     if tuple(out.shape) != (B, H, T, dv):
         raise ValueError("out must be [B, H, T, d_v]")
+    need = lib.fem_linear_workspace_bytes(B, H, T, dk, dv, int(chunk))
     with torch.cuda.device(q.device):
+        wst, wsp, wsn = _workspace(need, q.device, ws, stream)
         rc = lib.fem_linear_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
                                 out.data_ptr(), B, H, T, dk, dv, int(chunk),
-                                FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+                                FEM_DTYPE[q.dtype], wsp, wsn, _stream_handle(q.device, stream))
     _check(rc)
     return out
 
 
-def fem_gla_fwd(q, k, v, g, beta, out=None, chunk: int = 64, stream=None) -> torch.Tensor:
+def fem_gla_fwd(q, k, v, g, beta, out=None, chunk: int = 64, ws=None,
+                stream=None) -> torch.Tensor:
     """Causal GLA-prior FEM read.  q, k: [B, H, T, d_k] bf16; v: [B, H, T, d_v]
     bf16; g: [B, H, T, d_k] fp32 log-decays; beta: [H, d_v] fp32.  Returns
     [B, H, T, d_v] fp32."""
@@ -272,10 +313,12 @@ def fem_gla_fwd(q, k, v, g, beta, out=None, chunk: int = 64, stream=None) -> tor
     _dev_tensor(out, "out", torch.float32)
     if tuple(out.shape) != (B, H, T, dv):
         raise ValueError("out must be [B, H, T, d_v]")
+    need = lib.fem_gla_workspace_bytes(B, H, T, dk, dv, int(chunk))
     with torch.cuda.device(q.device):
+        wst, wsp, wsn = _workspace(need, q.device, ws, stream)
         rc = lib.fem_gla_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), g.data_ptr(),
                              beta.data_ptr(), out.data_ptr(), B, H, T, dk, dv, int(chunk),
-                             FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+                             FEM_DTYPE[q.dtype], wsp, wsn, _stream_handle(q.device, stream))
     _check(rc)
     return out
 
@@ -306,9 +349,11 @@ def fem_softmax_fwd_train(q, k, v, beta, out=None, lse=None, stream=None):
     return out, lse
 
 
-def fem_softmax_bwd(q, k, v, beta, out, lse, dout, stream=None):
+def fem_softmax_bwd(q, k, v, beta, out, lse, dout, ws=None, stream=None):
     """Gradients of sum(dout * out) w.r.t. q, k, v (fp32, shaped like them) and
-    beta ([H, d], summed over batch and time).  Returns (dq, dk, dv, dbeta)."""
+    beta ([H, d], summed over batch and time).  ws: optional uint8 GPU
+    workspace of at least fem_softmax_bwd_workspace_bytes(...) bytes.  Returns
+    (dq, dk, dv, dbeta)."""
     lib = load()
     for name, x in (("q", q), ("k", k), ("v", v)):
         _dev_tensor(x, name, torch.bfloat16)
@@ -327,10 +372,22 @@ def fem_softmax_bwd(q, k, v, beta, out, lse, dout, stream=None):
     dk = torch.empty_like(dq)
     dv = torch.empty_like(dq)
     db = torch.empty((H, d), device=q.device, dtype=torch.float32)
+    need = lib.fem_softmax_bwd_workspace_bytes(B, H, T, d)
     with torch.cuda.device(q.device):
+        wst, wsp, wsn = _workspace(need, q.device, ws, stream)
         rc = lib.fem_softmax_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
                                  out.data_ptr(), lse.data_ptr(), dout.data_ptr(), dq.data_ptr(),
                                  dk.data_ptr(), dv.data_ptr(), db.data_ptr(), B, H, T, d,
-                                 FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+                                 FEM_DTYPE[q.dtype], wsp, wsn, _stream_handle(q.device, stream))
     _check(rc)
     return dq, dk, dv, db
+
+
+def workspace_bytes(entry: str, *sizes) -> int:
+    """Exact workspace size (bytes) of the entry point ``entry`` ("linear",
+    "gla", "decode" or "bwd") for the given size arguments, as in fem.h."""
+    lib = load()
+    fn = {"linear": lib.fem_linear_workspace_bytes, "gla": lib.fem_gla_workspace_bytes,
+          "decode": lib.fem_softmax_decode_workspace_bytes,
+          "bwd": lib.fem_softmax_bwd_workspace_bytes}[entry]
+    return int(fn(*[int(x) for x in sizes]))

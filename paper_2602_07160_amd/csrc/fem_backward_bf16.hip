@@ -48,7 +48,6 @@
 
 #include <cstddef>
 #include <type_traits>
-#include <mutex>
 
 namespace fem {
 namespace {
@@ -1315,29 +1314,43 @@ __global__ __launch_bounds__(256) void dbeta_kernel(const float* __restrict__ ex
   }
 }
 
+// Workspace layout (fp32 unless noted): flag | lse renormalised by the q
+// pass [nbh T] | c, split [nbh D] | V max, V min, vdv, gf, exact partials
+// [nbh ntile D] | SA / P [nbh T D] | row constants [nbh Tp] | four bf16
+// operand arrays [nbh Tp D], Tp = 64 ntile: Y hi, Y lo, and W U hi, lo (the
+// q pass's, then the kv pass's W U').  Offsets in bytes from the base.
+struct BwdLayout {
+  size_t nl, nc, np, nz, nr, no, fbytes, total;
+  BwdLayout(int B, int H, int T, int D) {
+    const size_t nbh = (size_t)B * H;
+    const size_t ntile = ((size_t)T + kTile - 1) / kTile;
+    const size_t tp = ntile * kTile;
+    nl = nbh * T;
+    nc = nbh * D;
+    np = nbh * ntile * D;
+    nz = nbh * T * D;
+    nr = nbh * tp;
+    no = nbh * tp * D;
+    const size_t fl = nl + 2 * nc + 5 * np + nz + nr;
+    fbytes = (fl * sizeof(float) + 255) & ~(size_t)255;
+    total = 256 + fbytes + 4 * no * sizeof(bf16);
+  }
+};
+
 template <int D>
 hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* beta,
                       const float* out, const float* lse_fwd, const float* dout, float* dQ,
-                      float* dK, float* dV, float* dbeta, int B, int H, int T, hipStream_t stream) {
+                      float* dK, float* dV, float* dbeta, int B, int H, int T, void* wsv,
+                      hipStream_t stream) {
   const int nbh = B * H;
   const int ntile = (T + kTile - 1) / kTile;
   const bf16* q = reinterpret_cast<const bf16*>(Q);
   const bf16* k = reinterpret_cast<const bf16*>(K);
   const bf16* v = reinterpret_cast<const bf16*>(V);
-  // workspace (fp32 unless noted): flag | lse renormalised by the q pass
-  // [nbh T] | c, split [nbh D] | V max, V min, vdv, gf, exact partials
-  // [nbh ntile D] | SA / P [nbh T D] | row constants [nbh Tp] | four bf16
-  // operand arrays [nbh Tp D], Tp = 64 ntile: Y hi, Y lo, and W U hi, lo
-  // (the q pass's, then the kv pass's W U')
-  const size_t tp = (size_t)ntile * kTile;
-  const size_t nl = (size_t)nbh * T, nc = (size_t)nbh * D, np = (size_t)nbh * ntile * D;
-  const size_t nz = (size_t)nbh * T * D, nr = (size_t)nbh * tp, no = (size_t)nbh * tp * D;
-  const size_t fl = nl + 2 * nc + 5 * np + nz + nr;
-  const size_t fbytes = (fl * sizeof(float) + 255) & ~(size_t)255;
-  const size_t bytes = 256 + fbytes + 4 * no * sizeof(bf16);
-  char* ws = nullptr;
-  hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
-  if (e != hipSuccess) return e;
+  const BwdLayout lay(B, H, T, D);
+  const size_t nl = lay.nl, nc = lay.nc, np = lay.np, nz = lay.nz, no = lay.no;
+  const size_t fbytes = lay.fbytes;
+  char* ws = static_cast<char*>(wsv);
   int* flag = reinterpret_cast<int*>(ws);
   float* lse = reinterpret_cast<float*>(ws + 256);
   float* cg = lse + nl;
@@ -1353,6 +1366,7 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   bf16* yl = yh + no;
   bf16* wh = yl + no;
   bf16* wl = wh + no;
+  hipError_t e = hipSuccess;
   const dim3 grid((unsigned)(nbh * ntile)), blk(kThreads);
   hipLaunchKernelGGL(bwd_vstats_kernel<D>, grid, blk, 0, stream, v, vmx, vmn, flag, T, ntile);
   e = hipGetLastError();
@@ -1394,21 +1408,25 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
                        gfp, beta, flag, splitf, dbeta, B, H, ntile);
     e = hipGetLastError();
   }
-  const hipError_t f = workspace_free(ws, stream);
-  return e != hipSuccess ? e : f;
+  return e;
 }
 
 }  // namespace
 
+size_t softmax_bwd_ws_bytes(int B, int H, int T, int d) { return BwdLayout(B, H, T, d).total; }
+
 hipError_t launch_softmax_bwd_bf16(const void* Q, const void* K, const void* V,
                                    const float* beta, const float* out, const float* lse,
                                    const float* dout, float* dQ, float* dK, float* dV,
-                                   float* dbeta, int B, int H, int T, int d, hipStream_t stream) {
+                                   float* dbeta, int B, int H, int T, int d, void* ws,
+                                   hipStream_t stream) {
   switch (d) {
-    case 32: return launch_bwd<32>(Q, K, V, beta, out, lse, dout, dQ, dK, dV, dbeta, B, H, T, stream);
-    case 64: return launch_bwd<64>(Q, K, V, beta, out, lse, dout, dQ, dK, dV, dbeta, B, H, T, stream);
+    case 32:
+      return launch_bwd<32>(Q, K, V, beta, out, lse, dout, dQ, dK, dV, dbeta, B, H, T, ws, stream);
+    case 64:
+      return launch_bwd<64>(Q, K, V, beta, out, lse, dout, dQ, dK, dV, dbeta, B, H, T, ws, stream);
     case 128:
-      return launch_bwd<128>(Q, K, V, beta, out, lse, dout, dQ, dK, dV, dbeta, B, H, T, stream);
+      return launch_bwd<128>(Q, K, V, beta, out, lse, dout, dQ, dK, dV, dbeta, B, H, T, ws, stream);
     default: return hipErrorInvalidValue;
   }
 }

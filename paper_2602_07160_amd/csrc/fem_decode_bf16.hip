@@ -205,48 +205,64 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
   }
 }
 
-template <int DK, int DV>
-hipError_t launch_decode(const void* q, const void* Kc, const void* Vc, const int* lens,
-                         const float* beta, float* out, int B, int H, int L,
-                         hipStream_t stream) {
+// Split count of a step: enough (b, h, split) workgroups for about four per
+// compute unit of a 256-CU device, each split a whole number of key blocks.
+// A function of the sizes only, so that the workspace query needs no device.
+constexpr int kTargetWorkgroups = 1024;
+
+void decode_splits(int B, int H, int L, int* nsplit_out, int* bps_out) {
   const int nbh = B * H;
   const int blocks = (L + kBlk - 1) / kBlk;
-  const int cus = device_cus() > 0 ? device_cus() : 256;
-  int nsplit = (4 * cus + nbh - 1) / nbh;
+  int nsplit = (kTargetWorkgroups + nbh - 1) / nbh;
   nsplit = max(1, min(nsplit, blocks));
   const int bps = (blocks + nsplit - 1) / nsplit;
-  nsplit = (blocks + bps - 1) / bps;
+  *nsplit_out = (blocks + bps - 1) / bps;
+  *bps_out = bps;
+}
+
+template <int DK, int DV>
+hipError_t launch_decode(const void* q, const void* Kc, const void* Vc, const int* lens,
+                         const float* beta, float* out, int B, int H, int L, void* wsv,
+                         hipStream_t stream) {
+  const int nbh = B * H;
+  int nsplit, bps;
+  decode_splits(B, H, L, &nsplit, &bps);
   if (nsplit > 65535 || nbh > 65535) return hipErrorInvalidValue;
-  float2* ws = nullptr;
-  const size_t bytes = (size_t)nbh * nsplit * (DV + 1) * sizeof(float2);
-  hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
-  if (e != hipSuccess) return e;
+  float2* ws = static_cast<float2*>(wsv);  // partials [nbh][nsplit][DV + 1]
   hipLaunchKernelGGL((decode_partial_kernel<DK, DV>), dim3((unsigned)nsplit, (unsigned)nbh),
                      dim3(kThreads), 0, stream, reinterpret_cast<const bf16*>(q),
                      reinterpret_cast<const bf16*>(Kc), reinterpret_cast<const bf16*>(Vc), lens,
                      beta, ws, H, L, nsplit, bps);
-  e = hipGetLastError();
+  hipError_t e = hipGetLastError();
   if (e == hipSuccess) {
     hipLaunchKernelGGL((decode_merge_kernel<DV>), dim3((unsigned)nbh), dim3(kThreads), 0, stream,
                        ws, lens, beta, out, H, L, nsplit);
     e = hipGetLastError();
   }
-  const hipError_t f = workspace_free(ws, stream);
-  return e != hipSuccess ? e : f;
+  return e;
 }
 
 }  // namespace
 
+size_t decode_ws_bytes(int B, int H, int L, int dv) {
+  int nsplit, bps;
+  decode_splits(B, H, L, &nsplit, &bps);
+  return (size_t)B * H * nsplit * (dv + 1) * sizeof(float2);
+}
+
 hipError_t launch_decode_bf16(const void* q, const void* Kc, const void* Vc, const int* lens,
                               const float* beta, float* out, int B, int H, int L, int dk, int dv,
-                              hipStream_t stream) {
-  if (dk == 32 && dv == 32) return launch_decode<32, 32>(q, Kc, Vc, lens, beta, out, B, H, L, stream);
-  if (dk == 64 && dv == 64) return launch_decode<64, 64>(q, Kc, Vc, lens, beta, out, B, H, L, stream);
+                              void* ws, hipStream_t stream) {
+  if (dk == 32 && dv == 32)
+    return launch_decode<32, 32>(q, Kc, Vc, lens, beta, out, B, H, L, ws, stream);
+  if (dk == 64 && dv == 64)
+    return launch_decode<64, 64>(q, Kc, Vc, lens, beta, out, B, H, L, ws, stream);
   if (dk == 128 && dv == 128)
-    return launch_decode<128, 128>(q, Kc, Vc, lens, beta, out, B, H, L, stream);
-  if (dk == 64 && dv == 32) return launch_decode<64, 32>(q, Kc, Vc, lens, beta, out, B, H, L, stream);
+    return launch_decode<128, 128>(q, Kc, Vc, lens, beta, out, B, H, L, ws, stream);
+  if (dk == 64 && dv == 32)
+    return launch_decode<64, 32>(q, Kc, Vc, lens, beta, out, B, H, L, ws, stream);
   if (dk == 128 && dv == 64)
-    return launch_decode<128, 64>(q, Kc, Vc, lens, beta, out, B, H, L, stream);
+    return launch_decode<128, 64>(q, Kc, Vc, lens, beta, out, B, H, L, ws, stream);
   return hipErrorInvalidValue;
 }
 

@@ -49,14 +49,12 @@
 #include "fem_device.h"
 #include "fem_internal.h"
 
-#include <mutex>
 
 namespace fem {
 namespace {
 
 constexpr int DK = 64, DV = 64;  // supported widths
 constexpr int CH = 64;           // tokens per chunk
-constexpr int WG_PER_CU = 2;     // resident workgroups per CU (VGPR budget)
 constexpr int NTH = 256;         // 4 waves
 constexpr int ROW = 64 + 8;      // padded bf16 row (64 values + 16 B)
 constexpr int SROW = DK + 8;     // padded S^T row (bf16)
@@ -721,27 +719,44 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   }
 }
 
+// Segments of one call: the scan is sequential inside a segment, so the
+// fewest chunks per segment that still give about kScanSlots (b, h, segment)
+// workgroups (two per compute unit of a 256-CU device, all resident at
+// once).  A function of the sizes only, so the workspace query needs no
+// device.
+constexpr int kScanSlots = 512;
+
+struct ScanPlan {
+  int nseg, segc;
+  ScanPlan(int B, int H, int T) {
+    const int nbh = B * H;
+    const int nchunk = (T + CH - 1) / CH;
+    const int want = max(1, kScanSlots / nbh);
+    segc = (nchunk + want - 1) / want;
+    nseg = (nchunk + segc - 1) / segc;
+  }
+  // own segment states, then the entering (prefix) states; nothing when the
+  // whole sequence is one segment
+  size_t bytes(int B, int H, bool gla) const {
+    if (nseg <= 1) return 0;
+    const size_t sf = gla ? state_floats<kGla>() : state_floats<kElu>();
+    return 2 * (size_t)B * H * nseg * sf * sizeof(float);
+  }
+};
+
 template <int PRIOR>
 hipError_t launch_scan(const void* Q, const void* K, const void* V, const float* G,
-                       const float* beta, float* out, int B, int H, int T,
+                       const float* beta, float* out, int B, int H, int T, void* wsv,
                        hipStream_t stream) {
   constexpr int SF = state_floats<PRIOR>();
   const int nbh = B * H;
-  // Segments: the scan is sequential inside one, so the fewest chunks per
-  // segment that still let every workgroup be resident at once.
-  const int nchunk = (T + CH - 1) / CH;
-  const int slots = device_cus() * WG_PER_CU;
-  const int want = max(1, slots / nbh);
-  const int segc = (nchunk + want - 1) / want;
-  const int nseg = (nchunk + segc - 1) / segc;
-  float* ws = nullptr;
-  // own segment states, then the entering (prefix) states
-  const size_t bytes = 2 * (size_t)nbh * nseg * SF * sizeof(float);
-  hipError_t e = workspace_alloc(reinterpret_cast<void**>(&ws), bytes, stream);
-  if (e != hipSuccess) return e;
+  const ScanPlan plan(B, H, T);
+  const int nseg = plan.nseg, segc = plan.segc;
+  float* ws = static_cast<float*>(wsv);
   const bf16* q = reinterpret_cast<const bf16*>(Q);
   const bf16* k = reinterpret_cast<const bf16*>(K);
   const bf16* v = reinterpret_cast<const bf16*>(V);
+  hipError_t e = hipSuccess;
   if (nseg > 1) {
     hipLaunchKernelGGL((linear_kernel<PRIOR, false>), dim3((unsigned)(nbh * nseg)), dim3(NTH), 0,
                        stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
@@ -758,24 +773,28 @@ hipError_t launch_scan(const void* Q, const void* K, const void* V, const float*
                        stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
     e = hipGetLastError();
   }
-  const hipError_t f = workspace_free(ws, stream);
-  return e != hipSuccess ? e : f;
+  return e;
 }
 
 }  // namespace
 
+size_t scan_ws_bytes(int B, int H, int T, int chunk, bool gla) {
+  (void)chunk;
+  return ScanPlan(B, H, T).bytes(B, H, gla);
+}
+
 hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const float* beta,
                               float* out, int B, int H, int T, int dk, int dv, int chunk,
-                              hipStream_t stream) {
+                              void* ws, hipStream_t stream) {
   if (dk != DK || dv != DV || chunk != CH) return hipErrorNotSupported;
-  return launch_scan<kElu>(Q, K, V, nullptr, beta, out, B, H, T, stream);
+  return launch_scan<kElu>(Q, K, V, nullptr, beta, out, B, H, T, ws, stream);
 }
 
 hipError_t launch_gla_bf16(const void* Q, const void* K, const void* V, const float* G,
                            const float* beta, float* out, int B, int H, int T, int dk, int dv,
-                           int chunk, hipStream_t stream) {
+                           int chunk, void* ws, hipStream_t stream) {
   if (dk != DK || dv != DV || chunk != CH) return hipErrorNotSupported;
-  return launch_scan<kGla>(Q, K, V, G, beta, out, B, H, T, stream);
+  return launch_scan<kGla>(Q, K, V, G, beta, out, B, H, T, ws, stream);
 }
 
 }  // namespace fem

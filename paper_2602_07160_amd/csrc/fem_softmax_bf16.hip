@@ -67,7 +67,6 @@
 #include "fem_device.h"
 #include "fem_internal.h"
 
-#include <mutex>
 
 namespace fem {
 namespace {
@@ -580,7 +579,7 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
     const float* __restrict__ beta, const float* lam, const float* gate, float* out,
     float* __restrict__ lse, int H, int T, int nqb, int nbh) {
   constexpr int MODE = C::MODE;
-  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ __align__(16) unsigned char smem[C::LDS];
   const Smem<C> sm{smem};
 
   const int tid = threadIdx.x;
@@ -872,17 +871,10 @@ template <class C>
 hipError_t launch(const void* Q, const void* K, const void* V, const float* beta,
                   const float* lam, const float* gate, void* out, int B, int H, int T,
                   hipStream_t stream, float* lse = nullptr) {
-  static std::once_flag once;
-  static hipError_t attr_err = hipSuccess;
-  std::call_once(once, [] {
-    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&softmax_bf16_kernel<C>),
-                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
-  });
-  if (attr_err != hipSuccess) return attr_err;
   const int nqb = (T + C::BQ - 1) / C::BQ;
   const int nbh = B * H;
   dim3 grid((unsigned)(nqb * nbh)), block(C::NT);
-  hipLaunchKernelGGL((softmax_bf16_kernel<C>), grid, block, C::LDS, stream,
+  hipLaunchKernelGGL((softmax_bf16_kernel<C>), grid, block, 0, stream,
                      reinterpret_cast<const bf16*>(Q), reinterpret_cast<const bf16*>(K),
                      reinterpret_cast<const bf16*>(V), beta, lam, gate,
                      reinterpret_cast<float*>(out), lse, H, T, nqb, nbh);

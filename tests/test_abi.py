@@ -12,7 +12,7 @@ from paper_2602_07160_amd import binding
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "fem.h")
 
-OK, NULLPTR, SHAPE, UNSUPPORTED, ALIGN, HIPERR = range(6)
+OK, NULLPTR, SHAPE, UNSUPPORTED, ALIGN, HIPERR, WORKSPACE = range(7)
 BF16, F32 = 1, 0
 
 
@@ -35,10 +35,10 @@ def test_exports_match_header(lib):
 
 
 def test_status_strings(lib):
-    for s in range(6):
+    for s in range(7):
         assert binding.fem_status_str(s).startswith(
             ["FEM_OK", "FEM_ERR_NULLPTR", "FEM_ERR_SHAPE", "FEM_ERR_UNSUPPORTED",
-             "FEM_ERR_ALIGN", "FEM_ERR_HIP"][s])
+             "FEM_ERR_ALIGN", "FEM_ERR_HIP", "FEM_ERR_WORKSPACE"][s])
     assert "UNKNOWN" in binding.fem_status_str(99)
 
 
@@ -50,8 +50,9 @@ def sm(lib, q=A, k=A, v=A, beta=A, out=A, B=1, H=1, T=8, d=64, dt=BF16):
     return lib.fem_softmax_fwd(q, k, v, beta, out, B, H, T, d, dt, None)
 
 
-def ln(lib, q=A, k=A, v=A, beta=A, out=A, B=1, H=1, T=8, dk=64, dv=64, chunk=64, dt=BF16):
-    return lib.fem_linear_fwd(q, k, v, beta, out, B, H, T, dk, dv, chunk, dt, None)
+def ln(lib, q=A, k=A, v=A, beta=A, out=A, B=1, H=1, T=8, dk=64, dv=64, chunk=64, dt=BF16,
+       ws=None, wsb=0):
+    return lib.fem_linear_fwd(q, k, v, beta, out, B, H, T, dk, dv, chunk, dt, ws, wsb, None)
 
 
 def test_softmax_validation(lib):
@@ -114,8 +115,9 @@ def test_ex_validation(lib):
     assert ex(lib, dqk=128, dv=64, k=A + 8) == ALIGN
 
 
-def dec(lib, q=A, k=A, v=A, lens=A, beta=A, out=A, B=1, H=1, L=8, dqk=64, dv=64, dt=BF16):
-    return lib.fem_softmax_decode(q, k, v, lens, beta, out, B, H, L, dqk, dv, dt, None)
+def dec(lib, q=A, k=A, v=A, lens=A, beta=A, out=A, B=1, H=1, L=8, dqk=64, dv=64, dt=BF16,
+        ws=None, wsb=0):
+    return lib.fem_softmax_decode(q, k, v, lens, beta, out, B, H, L, dqk, dv, dt, ws, wsb, None)
 
 
 def test_decode_validation(lib):
@@ -128,8 +130,9 @@ def test_decode_validation(lib):
     assert dec(lib, k=A + 4) == ALIGN
 
 
-def gla(lib, q=A, k=A, v=A, g=A, beta=A, out=A, B=1, H=1, T=8, dk=64, dv=64, chunk=64, dt=BF16):
-    return lib.fem_gla_fwd(q, k, v, g, beta, out, B, H, T, dk, dv, chunk, dt, None)
+def gla(lib, q=A, k=A, v=A, g=A, beta=A, out=A, B=1, H=1, T=8, dk=64, dv=64, chunk=64, dt=BF16,
+        ws=None, wsb=0):
+    return lib.fem_gla_fwd(q, k, v, g, beta, out, B, H, T, dk, dv, chunk, dt, ws, wsb, None)
 
 
 def test_gla_validation(lib):
@@ -150,9 +153,94 @@ def test_train_and_backward_validation(lib):
     assert tr(o=A + 4) == ALIGN
     names = ("q", "k", "v", "b", "o", "l", "g", "dq", "dk", "dv", "db")
     bw = lambda **kw: lib.fem_softmax_bwd(*[kw.get(n, A) for n in names], kw.get("B", 1), 1, 8,
-                                          kw.get("d", 64), kw.get("dt", BF16), None)
+                                          kw.get("d", 64), kw.get("dt", BF16), kw.get("ws"),
+                                          kw.get("wsb", 0), None)
     assert bw(db=None) == NULLPTR
     assert bw(g=None) == NULLPTR
     assert bw(B=0) == SHAPE
     assert bw(d=16) == UNSUPPORTED
     assert bw(dk=A + 8) == ALIGN
+    # every size needs a workspace here: none, a short one, a misaligned one
+    need = lib.fem_softmax_bwd_workspace_bytes(1, 1, 8, 64)
+    assert need > 0
+    assert bw() == WORKSPACE
+    assert bw(ws=A, wsb=need - 1) == WORKSPACE
+    assert bw(ws=A + 16, wsb=need) == ALIGN
+
+
+# ---- workspace queries: the exact sizes documented in fem.h ----------------
+
+def cdiv(a, b):
+    return -(-a // b)
+
+
+def want_decode(B, H, L, dqk, dv):
+    blocks = cdiv(L, 64)
+    s0 = max(1, min(cdiv(1024, B * H), blocks))
+    n = cdiv(blocks, s0)
+    return 8 * B * H * cdiv(blocks, n) * (dv + 1)
+
+
+def want_scan(B, H, T, gla):
+    nchunk = cdiv(T, 64)
+    w = max(1, 512 // (B * H))
+    c = cdiv(nchunk, w)
+    S = cdiv(nchunk, c)
+    return 0 if S == 1 else 2 * 4 * B * H * S * (4288 if gla else 4224)
+
+
+def want_bwd(B, H, T, d):
+    nbh, n = B * H, cdiv(T, 64)
+    tp = 64 * n
+    fl = nbh * T + 2 * nbh * d + 5 * nbh * n * d + nbh * T * d + nbh * tp
+    return 256 + cdiv(4 * fl, 256) * 256 + 8 * nbh * tp * d
+
+
+SIZES = [(1, 1, 1), (1, 1, 8), (1, 1, 63), (1, 1, 64), (1, 1, 65), (2, 3, 700), (4, 16, 8192),
+         (8, 16, 4096), (1, 8, 16384), (1, 1, 100000), (64, 64, 128), (3, 5, 1000)]
+
+
+def test_workspace_queries(lib):
+    for B, H, T in SIZES:
+        for dqk, dv in ((32, 32), (64, 64), (128, 128), (64, 32), (128, 64)):
+            assert lib.fem_softmax_decode_workspace_bytes(B, H, T, dqk, dv) == \
+                want_decode(B, H, T, dqk, dv), (B, H, T, dqk, dv)
+        assert lib.fem_linear_workspace_bytes(B, H, T, 64, 64, 64) == want_scan(B, H, T, False)
+        assert lib.fem_gla_workspace_bytes(B, H, T, 64, 64, 64) == want_scan(B, H, T, True)
+        for d in (32, 64, 128):
+            assert lib.fem_softmax_bwd_workspace_bytes(B, H, T, d) == want_bwd(B, H, T, d)
+    # the headline and linear workloads
+    assert lib.fem_softmax_bwd_workspace_bytes(8, 16, 4096, 128) == want_bwd(8, 16, 4096, 128)
+    assert want_bwd(8, 16, 4096, 128) > 800e6
+    assert lib.fem_linear_workspace_bytes(4, 16, 8192, 64, 64, 64) == 2 * 4 * 64 * 8 * 4224
+    # arguments outside the supported set give 0
+    assert lib.fem_linear_workspace_bytes(4, 16, 8192, 32, 64, 64) == 0
+    assert lib.fem_linear_workspace_bytes(0, 16, 8192, 64, 64, 64) == 0
+    assert lib.fem_softmax_decode_workspace_bytes(1, 1, 8, 32, 64) == 0
+    assert lib.fem_softmax_bwd_workspace_bytes(1, 1, 8, 48) == 0
+    assert binding.workspace_bytes("linear", 4, 16, 8192, 64, 64, 64) == want_scan(4, 16, 8192, False)
+
+
+def test_workspace_errors(lib):
+    need = lib.fem_linear_workspace_bytes(4, 16, 8192, 64, 64, 64)
+    big = dict(B=4, H=16, T=8192)
+    assert ln(lib, **big) == WORKSPACE
+    assert ln(lib, **big, ws=A, wsb=need - 1) == WORKSPACE
+    assert ln(lib, **big, ws=A + 128, wsb=need) == ALIGN
+    assert gla(lib, **big) == WORKSPACE
+    needd = lib.fem_softmax_decode_workspace_bytes(8, 16, 4096, 128, 128)
+    assert needd > 0
+    assert dec(lib, B=8, H=16, L=4096, dqk=128, dv=128) == WORKSPACE
+    assert dec(lib, B=8, H=16, L=4096, dqk=128, dv=128, ws=A, wsb=needd - 8) == WORKSPACE
+    # the argument checks come first
+    assert ln(lib, **big, k=None) == NULLPTR
+    assert ln(lib, **big, chunk=48) == UNSUPPORTED
+
+
+def test_no_pool_in_library():
+    """The library allocates nothing: no allocation or pool call in its sources."""
+    csrc = os.path.join(os.path.dirname(HEADER), "..", "paper_2602_07160_amd", "csrc")
+    for name in os.listdir(csrc):
+        src = open(os.path.join(csrc, name)).read()
+        for call in ("hipMalloc", "hipFree", "hipMemPool", "hipMallocAsync", "hipHostMalloc"):
+            assert call not in src, (name, call)

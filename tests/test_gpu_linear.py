@@ -116,3 +116,25 @@ def test_linear_rejects_unsupported(fem):
     q32 = torch.zeros(1, 1, 8, 32, dtype=torch.bfloat16, device=dev)
     with pytest.raises(fem.FemError):
         fem.fem_linear_fwd(q32, q32, q32, torch.ones(1, 32, device=dev))
+
+
+def test_linear_caller_workspace(fem):
+    """A caller-provided workspace gives the same bits as one the binding
+    allocates; a short one is rejected before anything is launched."""
+    say("linear caller workspace: B2 H4 T3000 (several segments)")
+    dev = torch.device("cuda:0")
+    q, k, v, b = inputs.draw(4401, 2, 4, 3000, 64, dtype="bf16")
+    q, k, v, b = q.to(dev), k.to(dev), v.to(dev), b.to(dev)
+    need = fem.workspace_bytes("linear", 2, 4, 3000, 64, 64, 64)
+    assert need > 0
+    ws = torch.full((need + 512,), 0xAB, dtype=torch.uint8, device=dev)  # dirty on purpose
+    a = fem.fem_linear_fwd(q, k, v, b, ws=ws)
+    c = fem.fem_linear_fwd(q, k, v, b)
+    torch.cuda.synchronize()
+    assert torch.equal(a, c)
+    out = torch.full((2, 4, 3000, 64), 7.0, device=dev)
+    with pytest.raises(fem.FemError) as e:
+        fem.fem_linear_fwd(q, k, v, b, out=out, ws=ws[:need - 1])
+    assert e.value.status == 6
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())
