@@ -163,6 +163,27 @@ int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
                        void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * fem_softmax_decode for callers that cannot allocate device memory at all:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, result and kernels as fem_softmax_decode,
+ * without ws / ws_bytes: the partial results live in a fixed array of 8 MiB
+ * in the library's device code, one per device, kept until the process
+ * ends.  The call allocates nothing; its first call on a device looks the
+ * array's address up (hipGetSymbolAddress) with that device current.
+ *
+ * Limit: sizes whose fem_softmax_decode_workspace_bytes(...) exceeds
+ * 8 MiB (8388608 bytes) return FEM_ERR_WORKSPACE; e.g. d_v = 128 allows
+ * B * H up to 8128 at any L.  Every call on one device shares that device's
+ * array: calls that overlap in time on one device (different streams, or
+ * different host threads) race and give undefined results.  Returns a
+ * fem_status.
+ */
+int fem_softmax_decode_noalloc(const void* q, const void* Kc, const void* Vc,
+                               const int* lens, const float* beta, float* out,
+                               int B, int H, int L, int d_qk, int d_v, int dtype,
+                               hipStream_t stream);
+
+/*
  * Training pair of the causal softmax-prior read (bf16 inputs, d = 32, 64 or
  * 128).
  *

@@ -20,7 +20,7 @@ FEM_DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 
 EXPORTS = ("fem_softmax_fwd", "fem_softmax_fwd_ex", "fem_softmax_fwd_train", "fem_softmax_bwd",
            "fem_softmax_bwd_workspace_bytes", "fem_softmax_gated_fwd", "fem_softmax_decode",
-           "fem_softmax_decode_workspace_bytes", "fem_linear_fwd", "fem_linear_workspace_bytes",
+           "fem_softmax_decode_workspace_bytes", "fem_softmax_decode_noalloc", "fem_linear_fwd", "fem_linear_workspace_bytes",
            "fem_gla_fwd", "fem_gla_workspace_bytes", "fem_status_str")
 
 FEM_FLAG_ENCODER = 1
@@ -51,6 +51,8 @@ def load() -> ctypes.CDLL:
         lib.fem_softmax_decode.restype = i
         lib.fem_softmax_decode_workspace_bytes.argtypes = [i, i, i, i, i]
         lib.fem_softmax_decode_workspace_bytes.restype = sz
+        lib.fem_softmax_decode_noalloc.argtypes = [vp, vp, vp, vp, f, f, i, i, i, i, i, i, vp]
+        lib.fem_softmax_decode_noalloc.restype = i
         lib.fem_softmax_gated_fwd.argtypes = [vp, vp, vp, f, f, f, f, i, i, i, i, i, vp]
         lib.fem_softmax_gated_fwd.restype = i
         lib.fem_linear_fwd.argtypes = [vp, vp, vp, f, f, i, i, i, i, i, i, i, vp, sz, vp]
@@ -180,14 +182,7 @@ def fem_softmax_fwd_ex(q, k, v, beta, out=None, causal: bool = True, out_dtype=t
     return out
 
 
-def fem_softmax_decode(q, k_cache, v_cache, beta, lens=None, out=None, ws=None,
-                       stream=None) -> torch.Tensor:
-    """One decoding step: q [B, H, d_qk] reads the first lens[b] rows of the
-    caches k_cache [B, H, L, d_qk], v_cache [B, H, L, d_v] (bf16).  lens: [B]
-    int32 GPU tensor or None (all L).  ws: optional uint8 GPU workspace of at
-    least fem_softmax_decode_workspace_bytes(...) bytes.  Returns [B, H, d_v]
-    fp32."""
-    lib = load()
+def _decode_args(q, k_cache, v_cache, beta, lens, out):
     _dev_tensor(q, "q", torch.bfloat16)
     _dev_tensor(k_cache, "k_cache", torch.bfloat16)
     _dev_tensor(v_cache, "v_cache", torch.bfloat16)
@@ -210,6 +205,35 @@ def fem_softmax_decode(q, k_cache, v_cache, beta, lens=None, out=None, ws=None,
     _dev_tensor(out, "out", torch.float32)
     if tuple(out.shape) != (B, H, dv):
         raise ValueError("out must be [B, H, d_v]")
+    return B, H, L, dqk, dv, out
+
+
+def fem_softmax_decode_noalloc(q, k_cache, v_cache, beta, lens=None, out=None,
+                               stream=None) -> torch.Tensor:
+    """fem_softmax_decode without a workspace: the library keeps the partial
+    results in a fixed 8 MiB array per device (for callers that cannot
+    allocate; overlapping calls on one device race).  Same arguments and
+    result as fem_softmax_decode."""
+    lib = load()
+    B, H, L, dqk, dv, out = _decode_args(q, k_cache, v_cache, beta, lens, out)
+    with torch.cuda.device(q.device):
+        rc = lib.fem_softmax_decode_noalloc(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                            None if lens is None else lens.data_ptr(),
+                                            beta.data_ptr(), out.data_ptr(), B, H, L, dqk, dv,
+                                            FEM_DTYPE[q.dtype], _stream_handle(q.device, stream))
+    _check(rc)
+    return out
+
+
+def fem_softmax_decode(q, k_cache, v_cache, beta, lens=None, out=None, ws=None,
+                       stream=None) -> torch.Tensor:
+    """One decoding step: q [B, H, d_qk] reads the first lens[b] rows of the
+    caches k_cache [B, H, L, d_qk], v_cache [B, H, L, d_v] (bf16).  lens: [B]
+    int32 GPU tensor or None (all L).  ws: optional uint8 GPU workspace of at
+    least fem_softmax_decode_workspace_bytes(...) bytes.  Returns [B, H, d_v]
+    fp32."""
+    lib = load()
+    B, H, L, dqk, dv, out = _decode_args(q, k_cache, v_cache, beta, lens, out)
     need = lib.fem_softmax_decode_workspace_bytes(B, H, L, dqk, dv)
     with torch.cuda.device(q.device):
         wst, wsp, wsn = _workspace(need, q.device, ws, stream)

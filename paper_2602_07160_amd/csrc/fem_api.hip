@@ -108,6 +108,20 @@ extern "C" int fem_softmax_decode(const void* q, const void* Kc, const void* Vc,
       fem::launch_decode_bf16(q, Kc, Vc, lens, beta, out, B, H, L, d_qk, d_v, ws, stream));
 }
 
+extern "C" int fem_softmax_decode_noalloc(const void* q, const void* Kc, const void* Vc,
+                                          const int* lens, const float* beta, float* out, int B,
+                                          int H, int L, int d_qk, int d_v, int dtype,
+                                          hipStream_t stream) {
+  if (!q || !Kc || !Vc || !beta || !out) return FEM_ERR_NULLPTR;
+  if (!decode_sizes_ok(B, H, L, d_qk, d_v)) return FEM_ERR_SHAPE;
+  if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
+  if (!decode_pair_ok(d_qk, d_v)) return FEM_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(Kc) || !aligned16(Vc)) return FEM_ERR_ALIGN;
+  if (fem::decode_ws_bytes(B, H, L, d_v) > fem::kNoallocScratchBytes) return FEM_ERR_WORKSPACE;
+  return from_hip(fem::launch_decode_noalloc_bf16(q, Kc, Vc, lens, beta, out, B, H, L, d_qk,
+                                                  d_v, stream));
+}
+
 extern "C" int fem_softmax_fwd_train(const void* Q, const void* K, const void* V,
                                      const float* beta, float* out, float* lse, int B, int H,
                                      int T, int d, int dtype, hipStream_t stream) {

@@ -28,6 +28,7 @@
 #include "fem_device.h"
 #include "fem_internal.h"
 
+#include <atomic>
 #include <math.h>
 
 namespace fem {
@@ -243,6 +244,46 @@ hipError_t launch_decode(const void* q, const void* Kc, const void* Vc, const in
 }
 
 }  // namespace
+
+// Scratch of the entry point that allocates nothing (decode_noalloc): one
+// array per device, held until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it is a stand-in, not the device
+// address): the device address comes from hipGetSymbolAddress, once per
+// device, and is kept below.
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+
+// Device address of `scratch` on the current device (resolved on the first
+// call on that device).
+hipError_t scratch_address(void** p) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* a = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!a) {
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!a) return hipErrorInvalidSymbol;
+    g_scratch_addr[dev].store(a, std::memory_order_release);
+  }
+  *p = a;
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_decode_noalloc_bf16(const void* q, const void* Kc, const void* Vc,
+                                      const int* lens, const float* beta, float* out, int B,
+                                      int H, int L, int dk, int dv, hipStream_t stream) {
+  if (decode_ws_bytes(B, H, L, dv) > kNoallocScratchBytes) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = scratch_address(&ws);
+  if (e != hipSuccess) return e;
+  return launch_decode_bf16(q, Kc, Vc, lens, beta, out, B, H, L, dk, dv, ws, stream);
+}
 
 size_t decode_ws_bytes(int B, int H, int L, int dv) {
   int nsplit, bps;

@@ -45,6 +45,14 @@ hipError_t launch_decode_bf16(const void* q, const void* Kc, const void* Vc, con
                               const float* beta, float* out, int B, int H, int L, int dk, int dv,
                               void* ws, hipStream_t stream);
 
+// The same step with its partials in a fixed per-device array of
+// kNoallocScratchBytes (no allocation, no workspace argument).  Sizes whose
+// decode_ws_bytes exceed it return hipErrorInvalidValue.
+constexpr size_t kNoallocScratchBytes = (size_t)8 << 20;
+hipError_t launch_decode_noalloc_bf16(const void* q, const void* Kc, const void* Vc,
+                                      const int* lens, const float* beta, float* out, int B,
+                                      int H, int L, int dk, int dv, hipStream_t stream);
+
 // Exact fp32 vector-unit softmax-prior read, 1 <= d <= 256.
 hipError_t launch_softmax_f32(const float* Q, const float* K, const float* V,
                               const float* beta, float* out,

@@ -244,3 +244,18 @@ def test_no_pool_in_library():
         src = open(os.path.join(csrc, name)).read()
         for call in ("hipMalloc", "hipFree", "hipMemPool", "hipMallocAsync", "hipHostMalloc"):
             assert call not in src, (name, call)
+
+
+def test_decode_noalloc_validation(lib):
+    na = lambda **kw: lib.fem_softmax_decode_noalloc(
+        kw.get("q", A), A, A, A, A, kw.get("out", A), kw.get("B", 1), kw.get("H", 1),
+        kw.get("L", 8), kw.get("dqk", 64), kw.get("dv", 64), kw.get("dt", BF16), None)
+    assert na(q=None) == NULLPTR
+    assert na(L=0) == SHAPE
+    assert na(dqk=32, dv=64) == UNSUPPORTED
+    assert na(dt=F32) == UNSUPPORTED
+    assert na(q=A + 2) == ALIGN
+    # partials beyond the fixed 8 MiB array are refused before any launch
+    assert want_decode(64, 128, 64, 128, 128) > 8 << 20
+    assert na(B=64, H=128, L=64, dqk=128, dv=128) == WORKSPACE
+    assert want_decode(63, 129, 64, 128, 128) <= 8 << 20
