@@ -84,6 +84,20 @@ __device__ __forceinline__ void dma16(const void* src, void* dst) {
       : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
       : "memory");
 }
+// The same load with a wave-uniform 64-bit base in SGPRs and a 32-bit lane
+// offset: one VGPR per load instead of a 64-bit address pair.
+__device__ __forceinline__ void dma16s(const void* base, unsigned off, void* dst) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
+      : "memory");
+}
 __device__ __forceinline__ void dma4(const void* src, void* dst) {
   unsigned saved;
   asm volatile(

@@ -51,21 +51,27 @@
 // Schedule.  A wave keeps issuing independent vector instructions while its
 // own MFMAs run (about four per 32x32x16 MFMA come for free), so each
 // iteration k (one barrier) is two interleaved phases per wave:
-//   phase 1: QK^T(k) on the matrix pipe  ||  tilt of the wave's channels of
-//            tile k on the vector pipe;
-//   phase 2: PV(k-1) (hi, lo and the row-sum product)  ||  softmax of tile k
-//            (the scores phase 1 just produced).
-// The instruction order of each phase is pinned with scheduling barriers.  Row
-// and column rescales of the accumulator are rare; they are deferred to just
-// before the next PV so that neither phase needs a branch.  softmax(k)
-// overwrites the P registers behind PV(k-1) as it issues.  K(k+1) and
-// V(k+1) stream straight into the free LDS buffers (global_load_lds_dwordx4)
-// during iteration k; K, V and E are double buffered.  Workgroups run longest
-// causal extent first; workgroup i of a causal level covers head i, so a
-// head's workgroups share an XCD.
+//   phase 1: QK^T(k), the row sums and k-step 0 of PV(k-1) on the matrix
+//            pipe  ||  tilt of the wave's channels of tile k and the direct
+//            loads of tile k+1;
+//   phase 2: PV(k-1) k-steps 1..3 (hi and lo)  ||  softmax of tile k (the
+//            scores phase 1 just produced).
+// The instruction order of each phase is pinned with scheduling barriers, and
+// each chain of vector work (exponent, 2^, rounding) is spread over
+// consecutive slots so that no instruction waits on its own slot.  Row and
+// column rescales of the accumulator are rare; they are deferred to the start
+// of the next iteration, before any MFMA reads the accumulator.  P is double
+// buffered (softmax(k) writes one buffer while PV(k-1) reads the other); the
+// loop is unrolled by two so that the buffer index is a compile-time
+// constant.  K(k+1) and V(k+1) stream straight into the free LDS buffers
+// (global_load_lds_dwordx4) during iteration k; K, V and E are double
+// buffered.  Workgroups run longest causal extent first; workgroup i of a
+// causal level covers head i, so a head's workgroups share an XCD.
 
 #include "fem_device.h"
 #include "fem_internal.h"
+
+#include <type_traits>
 
 
 namespace fem {
@@ -120,11 +126,7 @@ struct Cfg {
   static constexpr int OFF_F = OFF_EL + 2 * EB;   // floats
   static constexpr int NF = DV /*bl*/ + DV /*inv*/ + 2 * DV /*c*/ + 2 * DV /*g*/ + 64 /*sink*/;
   static constexpr int OFF_R = OFF_F + NF * 4;    // column-update flags [2][NW]
-  // tile-load lane offsets [NW][64][TW]: K tile, then V tile unless SAME
-  static constexpr int OFF_T = OFF_R + 2 * NW * 4;
-  static constexpr int TWK = (BPWK + 3) / 4 * 4;
-  static constexpr int TW = TWK + (SAME ? 0 : (BPWV + 3) / 4 * 4);
-  static constexpr size_t LDS = OFF_T + NW * 64 * TW * 4;
+  static constexpr size_t LDS = OFF_R + 2 * NW * 4;
   static_assert(CPW * NW == DV && G * CPW == 64 && RPL * G == 16, "tilt mapping");
   static_assert(DK % 32 == 0 && DV % 32 == 0, "widths");
   static_assert(NW % 4 == 0, "flags are read as int4");
@@ -200,11 +202,6 @@ struct Smem {
   // Write-only slots for lanes whose store would otherwise need a branch.
   __device__ float* sink() const { return bl() + 6 * DV; }
   __device__ int* upd(int b) const { return reinterpret_cast<int*>(base + C::OFF_R) + b * C::NW; }
-  // this lane's offsets of a whole K tile; those of a V tile follow unless SAME
-  __device__ unsigned* ltab(int w, int l) const {
-    return reinterpret_cast<unsigned*>(base + C::OFF_T) + (w * 64 + l) * C::TW;
-  }
-  __device__ unsigned* ltabv(int w, int l) const { return ltab(w, l) + (C::SAME ? 0 : C::TWK); }
 };
 
 // Bits of two floats' upper halves packed into one dword (bf16 truncation).
@@ -301,8 +298,13 @@ struct Tilt {
     *(lane == 0 ? sm.upd(tt & 1) + wave : reinterpret_cast<int*>(sink)) = rose;
   }
 
-  __device__ __forceinline__ void value(int u, int b) {
-    e[u][b] = MODE == kMean ? v[u][b] : exp2_hw(fmaf(v[u][b], bl, sh));
+  // E of key 4(g + G u) + b in two stages, placed one slot apart: the exponent,
+  // then 2^exponent.
+  __device__ __forceinline__ void value_arg(int u, int b) {
+    e[u][b] = MODE == kMean ? v[u][b] : fmaf(v[u][b], bl, sh);
+  }
+  __device__ __forceinline__ void value_exp(int u, int b) {
+    if (MODE != kMean) e[u][b] = exp2_hw(e[u][b]);
   }
 
   __device__ __forceinline__ void store(int u) {
@@ -378,13 +380,24 @@ struct Softmax {
     apend = (mnew == m) ? 1.f : exp2_hw(m - mnew);
     m = mnew;
   }
-  __device__ __forceinline__ static void probs(const f32x16 (&sc)[2], bf16x8& p, int ks, int u,
-                                               float m, float scale2) {
-    const int kb = ks >> 1, s0 = (ks & 1) * 8;
-    const bf16x2 p2 = to_bf16x2(exp2_hw(fmaf(sc[kb][s0 + u], scale2, -m)),
-                                exp2_hw(fmaf(sc[kb][s0 + u + 1], scale2, -m)));
-    p[u] = p2[0];
-    p[u + 1] = p2[1];
+  // The probabilities of pair q (k-step q / 4, entries 2 (q % 4), +1) in three
+  // stages, placed one slot apart so that no stage waits on the one before:
+  // the exponents, 2^exponent, and the rounding into the MFMA B operand.
+  __device__ __forceinline__ static void prob_arg(const f32x16 (&sc)[2], f32x2& x, int q, float m,
+                                                  float scale2) {
+    const int ks = q >> 2, u = 2 * (q & 3), kb = ks >> 1, s0 = (ks & 1) * 8;
+    x[0] = fmaf(sc[kb][s0 + u], scale2, -m);
+    x[1] = fmaf(sc[kb][s0 + u + 1], scale2, -m);
+  }
+  __device__ __forceinline__ static void prob_exp(f32x2& x) {
+    x[0] = exp2_hw(x[0]);
+    x[1] = exp2_hw(x[1]);
+  }
+  __device__ __forceinline__ static void prob_round(const f32x2& x, bf16x8 (&p)[4], int q) {
+    const int ks = q >> 2, u = 2 * (q & 3);
+    const bf16x2 p2 = to_bf16x2(x[0], x[1]);
+    p[ks][u] = p2[0];
+    p[ks][u + 1] = p2[1];
   }
 };
 
@@ -393,9 +406,8 @@ struct Softmax {
 // 64*blk + l, i.e. row slot/SPR, chunk slot%SPR (the pad chunk re-reads chunk
 // 0).  Rows at or past T are clamped to T-1: their keys are masked anyway.
 // The address is a uniform tile base plus a 32-bit lane offset, so the loads
-// use scalar-base addressing.  The lane offsets of a whole tile (no clamping)
-// are computed once into an LDS table (tile_offsets) and read back per tile,
-// rather than held in registers across the loop.
+// use scalar-base addressing.  The lane offsets are a few integer operations,
+// recomputed per tile inside the MFMA slots of phase 1.
 template <int W, int NW>
 __device__ __forceinline__ unsigned tile_offset(int u, int k0, int T, int wave, int lane) {
   constexpr int SPR = (W + 8) / 8;  // 16-byte slots per padded row
@@ -404,32 +416,26 @@ __device__ __forceinline__ unsigned tile_offset(int u, int k0, int T, int wave, 
   return (unsigned)(row * W + (chunk < W / 8 ? chunk * 8 : 0)) * 2u;
 }
 
-template <int BPW>
-__device__ __forceinline__ void tile_offsets(const unsigned* t, unsigned* off) {
-#pragma unroll
-  for (int u = 0; u < BPW; ++u) off[u] = t[u];
-}
-
-template <int W, int NW, int BPW>
-__device__ __forceinline__ void load_tile(const bf16* __restrict__ src, unsigned char* dst, int k0,
-                                          int wave, const unsigned* off) {
+// Block u of this wave's share of a tile: the direct load, if the tile has it.
+template <int W, int NW>
+__device__ __forceinline__ void load_block(const bf16* __restrict__ src, unsigned char* dst,
+                                           int k0, int wave, int u, unsigned off) {
   constexpr int BLOCKS = 64 * ((W + 8) / 8) / 64;
-  const char* base = reinterpret_cast<const char*>(src + (size_t)k0 * W);
-#pragma unroll
-  for (int u = 0; u < BPW; ++u) {
-    const int blk = wave + NW * u;
-    if (BLOCKS % NW == 0 || blk < BLOCKS)
-      dma16(base + off[u], dst + blk * 1024);
-  }
+  const int blk = wave + NW * u;
+  if (BLOCKS % NW == 0 || blk < BLOCKS)
+    dma16s(src + (size_t)k0 * W, off, dst + blk * 1024);
 }
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Phase 1 of an iteration, interleaved by hand with the tilt of tile k (QKT):
-// on the matrix pipe, the row-sum products and k-step 0 of PV(k-1) (PVA),
-// then S^T = K Q^T of tile k into s (QKT).  Slot st issues MFMA st, the LDS
-// read of the operand fragment RING steps ahead and a fixed slice of the
-// tilt; a scheduling barrier after every slot keeps this order.
+// on the matrix pipe, S^T = K Q^T of tile k into s (QKT), then the row-sum
+// products and k-step 0 of PV(k-1) (PVA).  Slot st issues MFMA st, the LDS
+// read of the operand fragment RING steps ahead, one stage of the tilt and
+// whatever side(st) adds (the next tile's direct loads); a scheduling
+// barrier after every slot keeps this order.  The tilt's stages sit one
+// slot apart (exponent, 2^, rounding and store), so no vector instruction
+// waits on a result from its own slot.
 //
 // Row sums: a 16x16x32 product of a constant 0/1 selector (lsel) with the
 // same P^T fragments.  Lane l supplies selector row l%16 over k-block l/16;
@@ -437,34 +443,38 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // m = 4r for the k-blocks with b%2 == r%2 sums query (l%16) + 16*(r%2) into
 // output row 4r, which the 16x16 output layout places in register 0 of lane
 // 16r + l%16.  Hence lacc[0] of every lane is the row sum of its query l%32.
-template <class C, bool PVA, bool QKT>
+template <class C, bool PVA, bool QKT, class Side>
 __device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, int wave, int lane,
                                        int kofs, int eofs, const bf16x8 (&qf)[C::NKS],
                                        f32x16 (&s)[2], f32x16 (&acc)[C::NCB], f32x4& lacc,
-                                       const bf16x8 (&pp)[4], const bf16x8& lsel) {
+                                       const bf16x8 (&pp)[4], const bf16x8& lsel, Side&& side) {
   constexpr int MODE = C::MODE;
+  constexpr int NQ = QKT ? 2 * C::NKS : 0;    // QK MFMAs
   constexpr int NL = PVA ? 4 : 0;             // row-sum MFMAs
   constexpr int NLO = MODE == kMean ? 0 : C::NCB;  // lo blocks
   constexpr int NE = PVA ? C::NCB + NLO : 0;  // PV k-step 0: hi blocks, then lo blocks
-  constexpr int NQ = QKT ? 2 * C::NKS : 0;    // QK MFMAs
-  constexpr int NF = NE + NQ;                 // LDS operand fragments
-  constexpr int NS = NL + NF;
+  constexpr int NF = NQ + NE;                 // LDS operand fragments, in issue order
+  constexpr int NS = NQ + NL + NE;
   constexpr int RING = 4;
   constexpr int NV = QKT ? C::RPL * 4 : 0;    // tilt values of the lane
-  constexpr int C0 = PVA ? 2 : 0;             // slot of the column max
-  constexpr int NSLOT = NS > C0 + 2 + NV ? NS : C0 + 2 + NV;
-  auto vslot = [&](int x) { return C0 + 2 + (x * (NSLOT - C0 - 2)) / (NV > 0 ? NV : 1); };
+  // Tilt stages: column max at CM (late enough for the V reads issued at the
+  // start of the phase to have landed), shift at CM + 1, then value x's
+  // exponent at V0 + x, its 2^ one slot later, and run u's store one slot
+  // after its last 2^.
+  constexpr int CM = 4;
+  constexpr int V0 = CM + 2;
+  constexpr int NVS = NV > 0 ? V0 + NV + 2 : 0;
+  constexpr int NSLOT = NS > NVS ? NS : NVS;
   if (QKT) tl.read(sm, k, wave, lane);
   const unsigned char* kt = sm.base + pin(C::OFF_K + (k & 1) * C::KB + kofs);
   const unsigned char* eb = sm.base + (PVA ? pin(C::OFF_EH + ((k - 1) & 1) * C::EB + eofs) : 0u);
   auto frag = [&](int f) -> bf16x8 {
-    if (f < NE) {
-      const int lo = f >= C::NCB ? 1 : 0, cb = lo ? f - C::NCB : f;
-      return *reinterpret_cast<const bf16x8*>(eb + lo * (C::OFF_EL - C::OFF_EH) +
-                                              cb * 32 * C::EROW * 2);
-    }
-    const int st = f - NE;
-    return *reinterpret_cast<const bf16x8*>(kt + (st & 1) * 32 * C::KROW * 2 + (st >> 1) * 32);
+    if (f < NQ)
+      return *reinterpret_cast<const bf16x8*>(kt + (f & 1) * 32 * C::KROW * 2 + (f >> 1) * 32);
+    const int e = f - NQ;
+    const int lo = e >= C::NCB ? 1 : 0, cb = lo ? e - C::NCB : e;
+    return *reinterpret_cast<const bf16x8*>(eb + lo * (C::OFF_EL - C::OFF_EH) +
+                                            cb * 32 * C::EROW * 2);
   };
   bf16x8 ring[RING];
 #pragma unroll
@@ -478,55 +488,51 @@ __device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, in
   float vmax = 0.f;
 #pragma unroll
   for (int st = 0; st < NSLOT; ++st) {
-    if (st < NL) {
-      lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lsel, pp[st], lacc, 0, 0, 0);
-    } else if (st < NS) {
-      const int f = st - NL;
+    if (st < NQ || (st >= NQ + NL && st < NS)) {
+      const int f = st < NQ ? st : st - NL;
       const bf16x8 a = ring[f % RING];
       if (f + RING < NF) ring[f % RING] = frag(f + RING);
-      if (f < NE) {
-        const int cb = f >= C::NCB ? f - C::NCB : f;
-        acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pp[0], acc[cb], 0, 0, 0);
+      if (f < NQ) {
+        s[f & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[f >> 1], s[f & 1], 0, 0, 0);
       } else {
-        const int q = f - NE;
-        s[q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[q >> 1], s[q & 1], 0, 0, 0);
+        const int e = f - NQ, cb = e >= C::NCB ? e - C::NCB : e;
+        acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pp[0], acc[cb], 0, 0, 0);
       }
+    } else if (st >= NQ && st < NQ + NL) {
+      lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lsel, pp[st - NQ], lacc, 0, 0, 0);
     }
+    side(st);
     if (QKT) {
-      if (MODE != kMean && st == C0) vmax = tl.colmax();
-      if (MODE != kMean && st == C0 + 1) tl.shift(sm, k, wave, lane, vmax);
-#pragma unroll
-      for (int x = 0; x < NV; ++x) {
-        if (vslot(x) == st) {
-          tl.value(x >> 2, x & 3);
-          if ((x & 3) == 3) tl.store(x >> 2);
-        }
-      }
+      if (MODE != kMean && st == CM) vmax = tl.colmax();
+      if (MODE != kMean && st == CM + 1) tl.shift(sm, k, wave, lane, vmax);
+      const int xa = st - V0, xe = xa - 1, xs = xa - 5;  // values at each stage
+      if (xa >= 0 && xa < NV) tl.value_arg(xa >> 2, xa & 3);
+      if (xe >= 0 && xe < NV) tl.value_exp(xe >> 2, xe & 3);
+      if (xs >= 0 && (xs & 3) == 0 && (xs >> 2) < C::RPL) tl.store(xs >> 2);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// Phase 2 of an iteration: k-steps 1..3 of PV(k-1) (PVB), interleaved by hand
-// with the softmax of this tile (SM; MASK on the wave's diagonal tile and the
-// tiles after it).  One P buffer serves both products: an MFMA reads its
-// operands when it issues, so the softmax writes the new P of k-step ks only
-// in slots after the last MFMA that reads ks (k-step 0 was read in phase 1).
+// Phase 2 of an iteration: k-steps 1..3 of PV(k-1) (PVB), reading P(k-1)
+// from pp, interleaved by hand with the softmax of this tile (SM; MASK on the
+// wave's diagonal tile and the tiles after it), which writes P(k) into the
+// other buffer pn.  The softmax's stages sit one slot apart as in phase 1.
 template <class C, bool PVB, bool SM, bool MASK>
 __device__ __forceinline__ void phase2(const Smem<C>& sm, f32x16 (&acc)[C::NCB],
-                                       bf16x8 (&pp)[4], f32x16 (&sc)[2], float& m, float& apend,
-                                       int j, int eofs, int k0, int tq, int hl, float scale2) {
+                                       const bf16x8 (&pp)[4], bf16x8 (&pn)[4], f32x16 (&sc)[2],
+                                       float& m, float& apend, int j, int eofs, int k0, int tq,
+                                       int hl, float scale2) {
   constexpr int MODE = C::MODE;
   constexpr int NPK = MODE == kMean ? C::NCB : 2 * C::NCB;  // fragments per k-step
   constexpr int NF = PVB ? 3 * NPK : 0;               // k-steps 1..3
   constexpr int RING = 4;
-  constexpr int NSLOT = NF > 8 ? NF : 8;
-  // first slot free of reads of P k-step ks, then spread the 4 pairs
-  auto pslot = [&](int ks, int u) {
-    const int first = PVB ? NPK * ks : 0;
-    const int sl = first + (u / 2) * (NPK >= 4 ? NPK / 4 : 1);
-    return sl < 4 ? 4 + sl : sl;
-  };
+  // Softmax stages: the max tree in slots 0..2, the row-max update in 3, then
+  // pair q's exponents at P0 + q, its 2^ one slot later and its rounding into
+  // the next P buffer one slot after that.
+  constexpr int P0 = 4;
+  constexpr int NSS = SM ? P0 + 16 + 2 : 0;
+  constexpr int NSLOT = NF > NSS ? NF : NSS;
   const unsigned char* eb = sm.base + (PVB ? pin(C::OFF_EH + (j & 1) * C::EB + eofs) : 0u);
   auto frag = [&](int f) -> bf16x8 {
     const int ks = 1 + f / NPK, rem = f % NPK;
@@ -539,6 +545,7 @@ __device__ __forceinline__ void phase2(const Smem<C>& sm, f32x16 (&acc)[C::NCB],
   for (int f = 0; f < RING; ++f)
     if (f < NF) ring[f] = frag(f);
   Softmax smx;
+  f32x2 px[16];
   if (SM) smx.mask<MASK>(sc, k0, tq, hl);
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -554,22 +561,12 @@ __device__ __forceinline__ void phase2(const Smem<C>& sm, f32x16 (&acc)[C::NCB],
       if (st == 1) smx.max1(sc, 1);
       if (st == 2) smx.max2();
       if (st == 3) smx.update(m, apend, scale2);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-        for (int u = 0; u < 8; u += 2)
-          if (pslot(ks, u) == st) Softmax::probs(sc, pp[ks], ks, u, m, scale2);
-      }
+      const int qa = st - P0, qe = qa - 1, qr = qa - 2;  // pairs at each stage
+      if (qa >= 0 && qa < 16) Softmax::prob_arg(sc, px[qa], qa, m, scale2);
+      if (qe >= 0 && qe < 16) Softmax::prob_exp(px[qe]);
+      if (qr >= 0 && qr < 16) Softmax::prob_round(px[qr], pn, qr);
     }
     __builtin_amdgcn_sched_barrier(0);
-  }
-  if (SM) {
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-      for (int u = 0; u < 8; u += 2)
-        if (pslot(ks, u) >= NSLOT) Softmax::probs(sc, pp[ks], ks, u, m, scale2);
-    }
   }
 }
 
@@ -622,23 +619,12 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
                     : C::CAUSAL ? min((wq0 + 31) / C::BK, ntiles - 1)
                                 : ntiles - 1;
 
-  {
-    unsigned offk[C::BPWK], offv[C::BPWV];
 #pragma unroll
-    for (int u = 0; u < C::BPWK; ++u) {
-      offk[u] = tile_offset<C::DK, C::NW>(u, 0, T, wave, lane);
-      sm.ltab(wave, lane)[u] = tile_offset<C::DK, C::NW>(u, 0, 1 << 30, wave, lane);
-    }
-    if (!C::SAME) {
+  for (int u = 0; u < C::BPWK; ++u)
+    load_block<C::DK, C::NW>(Kh, sm.k(0), 0, wave, u, tile_offset<C::DK, C::NW>(u, 0, T, wave, lane));
 #pragma unroll
-      for (int u = 0; u < C::BPWV; ++u) {
-        offv[u] = tile_offset<C::DV, C::NW>(u, 0, T, wave, lane);
-        sm.ltabv(wave, lane)[u] = tile_offset<C::DV, C::NW>(u, 0, 1 << 30, wave, lane);
-      }
-    }
-    load_tile<C::DK, C::NW, C::BPWK>(Kh, sm.k(0), 0, wave, offk);
-    load_tile<C::DV, C::NW, C::BPWV>(Vh, sm.v(0), 0, wave, C::SAME ? offk : offv);
-  }
+  for (int u = 0; u < C::BPWV; ++u)
+    load_block<C::DV, C::NW>(Vh, sm.v(0), 0, wave, u, tile_offset<C::DV, C::NW>(u, 0, T, wave, lane));
   bf16x8 qf[C::NKS];
 #pragma unroll
   for (int ks = 0; ks < C::NKS; ++ks) {
@@ -654,7 +640,9 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
 #pragma unroll
   for (int cb = 0; cb < C::NCB; ++cb) acc[cb] = f32x16{};
   f32x16 sacc[2] = {f32x16{}, f32x16{}};  // scores of the current tile
-  bf16x8 pp[4] = {};                      // probabilities: softmax(k) -> PV(k)
+  // probabilities, double-buffered: softmax(k) writes tile k's into buffer
+  // k & 1 while PV(k-1) reads buffer (k-1) & 1
+  bf16x8 pbuf[2][4] = {};
   float m = -INFINITY;  // running row max (log2 units), shared by the lane pair
   float apend = 1.f;    // row rescale owed to the accumulator before the next PV
   f32x4 lacc = {};      // lacc[0]: row sum of the rounded P (see phase2)
@@ -669,27 +657,36 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
   const int kofs = n * C::KROW * 2 + hl * 16;  // lane part of K fragment addresses
   const int eofs = n * C::EROW * 2 + hl * 16;  // lane part of E fragment addresses
 
-  // The lane offsets of the next tile's loads: the table, or clamped rows for
-  // the last tile.
-  auto next_offsets = [&](int k, unsigned* offk, unsigned* offv) {
+  // Direct loads of tile k+1 into the free K and V buffers; the lane offsets
+  // are a few integer operations each.
+  auto load_next = [&](int k) {
     const int kn = (k + 1) * C::BK;
-    if (kn + C::BK <= T) {
-      tile_offsets<C::BPWK>(sm.ltab(wave, lane), offk);
-      if (!C::SAME) tile_offsets<C::BPWV>(sm.ltabv(wave, lane), offv);
-    } else {  // last tile: rows at or past T read row T-1
 #pragma unroll
-      for (int u = 0; u < C::BPWK; ++u) offk[u] = tile_offset<C::DK, C::NW>(u, kn, T, wave, lane);
-      if (!C::SAME) {
+    for (int u = 0; u < C::BPWK; ++u)
+      load_block<C::DK, C::NW>(Kh, sm.k((k + 1) & 1), kn, wave, u,
+                               tile_offset<C::DK, C::NW>(u, kn, T, wave, lane));
 #pragma unroll
-        for (int u = 0; u < C::BPWV; ++u)
-          offv[u] = tile_offset<C::DV, C::NW>(u, kn, T, wave, lane);
-      }
-    }
+    for (int u = 0; u < C::BPWV; ++u)
+      load_block<C::DV, C::NW>(Vh, sm.v((k + 1) & 1), kn, wave, u,
+                               tile_offset<C::DV, C::NW>(u, kn, T, wave, lane));
   };
-  auto load_next = [&](int k, const unsigned* offk, const unsigned* offv) {
+  // The same loads spread over the MFMA slots of phase 1, one per slot from
+  // slot LD0 on (K blocks, then V blocks), so that the waves of a workgroup
+  // do not all wait on the memory pipeline at once.
+  constexpr int LD0 = 2;
+  auto loads_in_slots = [&](int k) {
+    const bool more = k + 1 < ntiles;
     const int kn = (k + 1) * C::BK;
-    load_tile<C::DK, C::NW, C::BPWK>(Kh, sm.k((k + 1) & 1), kn, wave, offk);
-    load_tile<C::DV, C::NW, C::BPWV>(Vh, sm.v((k + 1) & 1), kn, wave, C::SAME ? offk : offv);
+    return [=](int st) __attribute__((always_inline)) {
+      if (!more) return;
+      const int u = st - LD0, w = u - C::BPWK;
+      if (u >= 0 && u < C::BPWK)
+        load_block<C::DK, C::NW>(Kh, sm.k((k + 1) & 1), kn, wave, u,
+                                 tile_offset<C::DK, C::NW>(u, kn, T, wave, lane));
+      if (w >= 0 && w < C::BPWV)
+        load_block<C::DV, C::NW>(Vh, sm.v((k + 1) & 1), kn, wave, w,
+                                 tile_offset<C::DV, C::NW>(w, kn, T, wave, lane));
+    };
   };
   // Deferred rescales owed before PV(j): the row factor of softmax(j) and the
   // column factors of tilt(j) (flag word from upd(j)).
@@ -705,6 +702,9 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
           if (col) gg *= *reinterpret_cast<const f32x4*>(gcol + cb * 32 + g * 8 + hl * 4);
 #pragma unroll
           for (int e = 0; e < 4; ++e) acc[cb][g * 4 + e] *= gg[e];
+          // one group of factors at a time: this runs where the scores and
+          // the tilt's values are live
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
       lacc[0] *= apend;
@@ -718,10 +718,12 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
     for (int w = 1; w < C::NW / 4; ++w) any4 |= uf[w];
     return any4;
   };
-#define FEM_PHASE1(PVA, QKT) \
-  phase1<C, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, pp, lsel)
-#define FEM_PHASE2(PVB, SM, MK) \
-  phase2<C, PVB, SM, MK>(sm, acc, pp, sacc, m, apend, k - 1, eofs, k * C::BK, tm, hl, scale2)
+#define FEM_PHASE1(PVA, QKT, PPREV, SIDE) \
+  phase1<C, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, PPREV, lsel, SIDE)
+  const auto none = [](auto...) __attribute__((always_inline)) {};
+#define FEM_PHASE2(PVB, SM, MK, PPREV, PNEXT)                                                    \
+  phase2<C, PVB, SM, MK>(sm, acc, PPREV, PNEXT, sacc, m, apend, k - 1, eofs, k * C::BK, tm, hl, \
+                         scale2)
 
   // Every wave runs the same steps on every tile: past its diagonal tile the
   // softmax masks every key, so P = 0 and PV adds nothing, while the
@@ -731,41 +733,49 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
   // 1..3 || softmax(k); one barrier.
   {
     const int k = 0;
-    if (k + 1 < ntiles) {
-      unsigned offk[C::BPWK], offv[C::BPWV];
-      next_offsets(k, offk, offv);
-      load_next(k, offk, offv);
-    }
+    if (k + 1 < ntiles) load_next(k);
     Tilt<C> tl;
-    FEM_PHASE1(false, true);
-    if (wlast <= 0) FEM_PHASE2(false, true, true);
-    else FEM_PHASE2(false, true, false);
+    FEM_PHASE1(false, true, pbuf[1], none);
+    if (wlast <= 0) FEM_PHASE2(false, true, true, pbuf[1], pbuf[0]);
+    else FEM_PHASE2(false, true, false, pbuf[1], pbuf[0]);
     wait_vmem();
     __syncthreads();
   }
-  for (int k = 1; k < ntiles; ++k) {
-    // LDS reads of the flag words and the load offsets go out together
-    const i32x4 any4 = flags_of(k - 1);
-    if (k + 1 < ntiles) {
-      unsigned offk[C::BPWK], offv[C::BPWV];
-      next_offsets(k, offk, offv);
-      load_next(k, offk, offv);
-    }
-    if (k > 1) rescale(k - 1, any4);
+  // iteration k; PAR = k & 1 is a compile-time constant so that the P
+  // buffers stay in registers
+  auto body = [&](const int k, auto par) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(par)::value;
+    // the flag words' LDS reads go out first; their latency hides behind
+    // the load issue
+    if (k > 1) rescale(k - 1, flags_of(k - 1));
     Tilt<C> tl;
-    FEM_PHASE1(true, true);
-    if (k >= wlast) FEM_PHASE2(true, true, true);
-    else FEM_PHASE2(true, true, false);
+    // A wave in phase 1 issues ahead of the other wave of its SIMD in phase
+    // 2: the QK products then run while the other wave does its softmax on
+    // the vector unit, and the two waves reach the barrier closer together.
+    __builtin_amdgcn_s_setprio(1);
+    FEM_PHASE1(true, true, pbuf[PAR ^ 1], loads_in_slots(k));
+    __builtin_amdgcn_s_setprio(0);
+    if (k >= wlast) FEM_PHASE2(true, true, true, pbuf[PAR ^ 1], pbuf[PAR]);
+    else FEM_PHASE2(true, true, false, pbuf[PAR ^ 1], pbuf[PAR]);
     wait_vmem();
     __syncthreads();
+  };
+  int kk = 1;
+  for (; kk + 1 < ntiles; kk += 2) {
+    body(kk, std::integral_constant<int, 1>());
+    body(kk + 1, std::integral_constant<int, 0>());
   }
-  {
+  if (kk < ntiles) body(kk, std::integral_constant<int, 1>());
+  auto tail = [&](auto par) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(par)::value;  // parity of the last tile
     const int k = ntiles;
     if (k > 1) rescale(k - 1, flags_of(k - 1));
     Tilt<C> tl;
-    FEM_PHASE1(true, false);
-    FEM_PHASE2(true, false, false);
-  }
+    FEM_PHASE1(true, false, pbuf[PAR], none);
+    FEM_PHASE2(true, false, false, pbuf[PAR], pbuf[PAR]);
+  };
+  if ((ntiles - 1) & 1) tail(std::integral_constant<int, 1>());
+  else tail(std::integral_constant<int, 0>());
 #undef FEM_PHASE1
 #undef FEM_PHASE2
 
