@@ -9,20 +9,26 @@ synthetic data resident in HBM before the timed region.  Prints ONE JSON line.
 
 Throughput is algorithmic: FLOP = 2*B*H*T*(T+1)*d per call (Q K^T and P E
 multiply-adds over the causal triangle, diagonal included; exponentials not
-counted).  The linear-prior read (fem_linear_fwd, B=4, H=16, T=8192,
-d_k=d_v=64, chunk 64) is timed too and reported under "linear", and the
-two-level gated read (fem_softmax_gated_fwd) on the headline shape under
-"gated" (FLOP = 3*B*H*T*(T+1)*d: Q K^T, P E and P V), and one decoding step
-(fem_softmax_decode) against a full B=8, H=16, L=4096, d=128 KV cache under
-"decode" (bytes = the caches read once + q + out), and the GLA-prior read
-(fem_gla_fwd) on the linear workload's shape with seeded log-decays under
-"gla" (bytes = q, k, v, the fp32 decays and out, once each), and the
-backward pass (fem_softmax_bwd) on the headline shape under "backward": its
-matrix-core passes run 32*d FLOP per (t, i <= t) pair (Q K^T in the q and kv
-passes, the posterior products dP in both passes
-and the normaliser sums SA in the q pass with bf16 hi/lo operands, three
-products each, and dQ, dK, dV^T (hi/lo)), so its roofline is the bf16
-matrix peak.
+counted).  Before the W warm-up steps the headline step runs untimed for
+--settle-ms of wall time (the GPU clock ramps up over the first ~25 ms of
+sustained load); then exactly K steps are timed with HIP events on the
+stream the kernels run on, and the line reports their mean (ms_per_step)
+and median.
+
+Also timed, under their own keys (none of them is the headline value):
+  config2, config4  the softmax read on the B4 H8 T1024 d64 and the
+                    long-context B1 H8 T16384 d64 workloads
+  linear            fem_linear_fwd, B4 H16 T8192 d_k=d_v=64, chunk 64 (HBM roofline:
+                    q, k, v read once, fp32 out written once)
+  gla               fem_gla_fwd on the same shape with seeded log-decays
+  gated             fem_softmax_gated_fwd on the headline shape (6*d FLOP per pair)
+  decode            one fem_softmax_decode step against a full B8 H16 L4096 d128 cache
+  backward          fem_softmax_bwd on the headline shape: its algorithmic work
+                    is 10*d FLOP per (t, i <= t) pair (Q K^T recomputed, the
+                    posterior weights sum_j W (R - 1), dV, dQ and dK), its
+                    issued matrix-core work 32*d (hi/lo operand splits, both
+                    passes' Q K^T) is reported beside it
+The oracle (float64 numpy) is timed on the host as cpu_baseline.
 """
 
 from __future__ import annotations
@@ -31,6 +37,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -39,7 +46,6 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak (published)
-# x 2.4 GHz / 4
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -60,27 +66,49 @@ def measured_traffic(kernel: str):
     return ent["fetch_bytes"] + ent["write_bytes"]
 
 
-def time_calls(fn, steps: int, warmup: int):
+def time_calls(fn, steps: int, warmup: int, settle_ms: float = 0.0):
+    """Run ``fn`` untimed for settle_ms of wall time, then ``warmup`` untimed
+    calls, then time exactly ``steps`` calls with events on the current
+    stream.  Returns (mean ms per call over the bracket, median ms per call)."""
     import torch
+    if settle_ms > 0:
+        t_end = time.perf_counter() + settle_ms / 1e3
+        while time.perf_counter() < t_end:
+            fn()
+            torch.cuda.synchronize()
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for _ in range(steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record(stream)
+    for i in range(steps):
         fn()
-    t1.record(stream)
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
-    return t0.elapsed_time(t1) / steps  # ms per call
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return ev[0].elapsed_time(ev[steps]) / steps, statistics.median(per)
+
+
+def blas_info():
+    try:
+        from threadpoolctl import threadpool_info
+        info = [x for x in threadpool_info() if x.get("user_api") == "blas"]
+        if info:
+            x = info[0]
+            return f"{x.get('internal_api')} {x.get('version')}", int(x.get("num_threads", 1))
+    except Exception:
+        pass
+    return "unknown", 0
 
 
 def cpu_baseline(q, k, v, beta, budget_s: float):
-    """Time the float64 oracle on whole heads of the same workload until
-    ``budget_s`` seconds have been spent; report algorithmic TFLOP/s."""
+    """Time the float64 oracle on whole heads of the headline workload until
+    ``budget_s`` seconds have been spent (BLAS threads = every usable core),
+    and one config-2 head with a single BLAS thread; algorithmic TFLOP/s."""
     import numpy as np
     import oracle
+    from paper_2602_07160_amd import inputs
     B, H, T, d = q.shape
     heads = 0
     t_start = time.perf_counter()
@@ -91,30 +119,66 @@ def cpu_baseline(q, k, v, beta, budget_s: float):
         heads += 1
     el = time.perf_counter() - t_start
     flop = 2.0 * heads * T * (T + 1) * d
+    blas, threads = blas_info()
+    # one thread, whole heads of config 2 (B4 H8 T1024 d64), about two seconds
+    q2, k2, v2, b2 = inputs.make_inputs(2)
+    T2, d2 = q2.shape[2], q2.shape[3]
+    single = None
     try:
-        from threadpoolctl import threadpool_info
-        threads = max(int(x.get("num_threads", 1)) for x in threadpool_info()) if threadpool_info() else 1
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1, user_api="blas"):
+            n2, t2 = 0, time.perf_counter()
+            while time.perf_counter() - t2 < 2.0 and n2 < q2.shape[0] * q2.shape[1]:
+                bb, hh = divmod(n2, q2.shape[1])
+                oracle.fem_softmax(q2[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                   k2[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                   v2[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                   b2[hh:hh + 1].double().numpy())
+                n2 += 1
+            e2 = time.perf_counter() - t2
+        single = {"value": 2.0 * n2 * T2 * (T2 + 1) * d2 / e2 / 1e12, "unit": "TFLOP/s",
+                  "cores": 1, "sample": f"{n2} whole heads of B4 H8 T1024 d64, {e2:.2f} s"}
+    except Exception as e:  # threadpoolctl missing: say so, no figure
+        single = {"error": str(e)}
     return {
         "value": flop / el / 1e12,
         "unit": "TFLOP/s",
         "tokens_per_s": heads * T / el,
-        "cores": threads,
+        "cores": len(os.sched_getaffinity(0)),
+        "blas": blas,
+        "blas_threads": threads,
         "kind": "oracle",
         "sample": f"{heads} whole (b,h) head(s) of the B8 H16 T4096 d128 workload, float64 numpy, {el:.1f} s",
+        "single_thread_config2": single,
     }
+
+
+def softmax_entry(binding, inputs, dev, no, steps, warmup, settle_ms):
+    """Timing of fem_softmax_fwd on workload ``no`` (2 or 4)."""
+    import torch
+    w = inputs.WORKLOADS[no]
+    q, k, v, beta = (x.to(dev) for x in inputs.make_inputs(no))
+    out = torch.empty(q.shape, device=dev, dtype=torch.float32)
+    ms, med = time_calls(lambda: binding.fem_softmax_fwd(q, k, v, beta, out=out), steps, warmup,
+                         settle_ms)
+    flop = 2.0 * w.B * w.H * w.T * (w.T + 1) * w.d
+    return {"workload": w.name, "ms": round(ms, 4), "ms_median": round(med, 4),
+            "tokens_per_s": round(w.B * w.T / (ms * 1e-3), 1), "flop_per_call": flop,
+            "achieved_TFLOPs": round(flop / (ms * 1e-3) / 1e12, 2),
+            "peak_TFLOPs": PEAK_BF16_TFLOPS,
+            "frac": round(flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    # ~0.1 s of untimed calls: the first ~25 ms of sustained load run at a
-    # lower clock (same kernel: 1.04 ms per call then, 0.91 ms after)
-    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle-ms", type=float, default=250.0,
+                    help="untimed calls for this much wall time before the warm-up steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-extra", action="store_true", help="time the headline workload only")
     ap.add_argument("--no-linear", action="store_true")
     ap.add_argument("--no-gated", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
@@ -129,6 +193,8 @@ def main():
         print("bench.py measures one GPU only: the FEM read is benchmarked on a single MI355X "
               "(multi-GPU sharding is a design note, not a measured path)", file=sys.stderr)
         sys.exit(2)
+    if args.no_extra:
+        args.no_linear = args.no_gated = args.no_decode = args.no_gla = args.no_backward = True
 
     import torch
     from paper_2602_07160_amd import binding, inputs
@@ -147,7 +213,7 @@ def main():
     qd, kd, vd, bd = (x.to(dev) for x in (q, k, v, beta))
     out = torch.empty(q.shape, device=dev, dtype=torch.float32)
     fn = lambda: binding.fem_softmax_fwd(qd, kd, vd, bd, out=out)
-    ms = time_calls(fn, args.steps, args.warmup)
+    ms, med = time_calls(fn, args.steps, args.warmup, args.settle_ms)
     B, H, T, d = w.B, w.H, w.T, w.d
     flop = 2.0 * B * H * T * (T + 1) * d
     tflops = flop / (ms * 1e-3) / 1e12
@@ -162,7 +228,9 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_ms": args.settle_ms,
         "ms_per_step": round(ms, 4),
+        "ms_median": round(med, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -176,56 +244,65 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic("softmax_bf16_kernel<128,8,kFem>"),
-            "kernel": "softmax_bf16_kernel<128,8,kFem>",
+            "traffic": measured_traffic("softmax_bf16_kernel<128,128,8,kFem>"),
+            "kernel": "softmax_bf16_kernel<128,128,8,kFem>",
         },
     }
+    if not args.no_extra:
+        for no in (2, 4):
+            result[f"config{no}"] = softmax_entry(binding, inputs, dev, no, args.steps,
+                                                  args.warmup, 0.0)
     if not args.no_gated:
         lam, g = inputs.draw_gates(inputs.BASE_SEED + 103, B, H, T, d)
         lamd, gd = lam.to(dev), g.to(dev)
         fng = lambda: binding.fem_softmax_gated_fwd(qd, kd, vd, bd, lamd, gd, out=out)
-        msg = time_calls(fng, args.steps, args.warmup)
+        msg, medg = time_calls(fng, args.steps, args.warmup)
         flop_g = 3.0 * B * H * T * (T + 1) * d
         result["gated"] = {
-            "workload": w.name + "_gated", "ms": round(msg, 4),
+            "workload": w.name + "_gated", "ms": round(msg, 4), "ms_median": round(medg, 4),
             "tokens_per_s": round(B * T / (msg * 1e-3), 1),
             "flop_per_call": flop_g,
             "achieved_TFLOPs": round(flop_g / (msg * 1e-3) / 1e12, 2),
             "peak_TFLOPs": PEAK_BF16_TFLOPS,
             "frac": round(flop_g / (msg * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-            "kernels": ["softmax_bf16_kernel<128,8,kMean>", "softmax_bf16_kernel<128,8,kGated>"],
         }
         del lamd, gd
     if not args.no_backward:
         outt, lse = binding.fem_softmax_fwd_train(qd, kd, vd, bd)
         gout = torch.randn(outt.shape, device=dev, dtype=torch.float32,
                            generator=torch.Generator(device=dev).manual_seed(7))
-        fnb = lambda: binding.fem_softmax_bwd(qd, kd, vd, bd, outt, lse, gout)
-        msb = time_calls(fnb, args.backward_steps, 1)
-        flop_b = 32 * d * B * H * T * (T + 1) // 2
+        wsb = torch.empty(binding.workspace_bytes("bwd", B, H, T, d), device=dev,
+                          dtype=torch.uint8)
+        fnb = lambda: binding.fem_softmax_bwd(qd, kd, vd, bd, outt, lse, gout, ws=wsb)
+        msb, medb = time_calls(fnb, args.backward_steps, 1)
+        pairs = B * H * T * (T + 1) // 2
+        flop_b = 10 * d * pairs
         result["backward"] = {
-            "workload": w.name + "_bwd", "ms": round(msb, 3), "steps": args.backward_steps,
-            "flop_per_call": flop_b,
+            "workload": w.name + "_bwd", "ms": round(msb, 3), "ms_median": round(medb, 3),
+            "steps": args.backward_steps,
+            "flop_per_call": flop_b, "issued_flop_per_call": 32 * d * pairs,
             "achieved_TFLOPs": round(flop_b / (msb * 1e-3) / 1e12, 2),
             "peak_TFLOPs": PEAK_BF16_TFLOPS,
             "frac": round(flop_b / (msb * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-            "kernels": ["bwd_q_fast_kernel<128>", "bwd_kv_fast_kernel<128>", "bwd_vstats_kernel<128>", "bwd_prepk_kernel<128>", "bwd_prepq_kernel<128>"],
+            "issued_frac": round(32 * d * pairs / (msb * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         }
-        del outt, lse, gout
+        del outt, lse, gout, wsb
     if not args.no_decode:
         q1 = qd[:, :, -1].contiguous()
         outd = torch.empty((B, H, d), device=dev, dtype=torch.float32)
-        fnd = lambda: binding.fem_softmax_decode(q1, kd, vd, bd, out=outd)
-        msd = time_calls(fnd, args.steps, args.warmup)
+        wsd = torch.empty(binding.workspace_bytes("decode", B, H, T, d, d), device=dev,
+                          dtype=torch.uint8)
+        fnd = lambda: binding.fem_softmax_decode(q1, kd, vd, bd, out=outd, ws=wsd)
+        msd, medd = time_calls(fnd, args.steps, args.warmup)
         io = 2 * B * H * T * d * 2 + q1.numel() * 2 + outd.numel() * 4
         result["decode"] = {
             "workload": f"fem_softmax_decode_bf16_B{B}_H{H}_L{T}_d{d}", "ms": round(msd, 4),
-            "algorithmic_bytes": io,
+            "ms_median": round(medd, 4), "algorithmic_bytes": io,
             "achieved_GBs": round(io / (msd * 1e-3) / 1e9, 1),
             "peak_GBs": PEAK_HBM_GBS,
             "frac": round(io / (msd * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         }
-        del q1, outd
+        del q1, outd, wsd
     del qd, kd, vd, out
     torch.cuda.empty_cache()
 
@@ -234,34 +311,38 @@ def main():
         ql, kl, vl, bl = inputs.make_inputs(5)
         qld, kld, vld, bld = (x.to(dev) for x in (ql, kl, vl, bl))
         outl = torch.empty(vl.shape, device=dev, dtype=torch.float32)
-        try:
-            fnl = lambda: binding.fem_linear_fwd(qld, kld, vld, bld, out=outl, chunk=wl.chunk)
-            msl = time_calls(fnl, args.steps, args.warmup)
-            io = 3 * ql.numel() * 2 + outl.numel() * 4
-            result["linear"] = {
-                "workload": wl.name, "chunk": wl.chunk, "ms": round(msl, 4),
-                "tokens_per_s": round(wl.B * wl.T / (msl * 1e-3), 1),
-                "algorithmic_bytes": io,
-                "achieved_GBs": round(io / (msl * 1e-3) / 1e9, 1),
-                "peak_GBs": PEAK_HBM_GBS,
-                "frac": round(io / (msl * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            }
-        except binding.FemError as e:
-            result["linear"] = {"error": str(e)}
+        wsl = torch.empty(max(1, binding.workspace_bytes("linear", wl.B, wl.H, wl.T, wl.d, wl.dv,
+                                                         wl.chunk)), device=dev, dtype=torch.uint8)
+        fnl = lambda: binding.fem_linear_fwd(qld, kld, vld, bld, out=outl, chunk=wl.chunk, ws=wsl)
+        msl, medl = time_calls(fnl, args.steps, args.warmup)
+        io = 3 * ql.numel() * 2 + outl.numel() * 4
+        result["linear"] = {
+            "workload": wl.name, "chunk": wl.chunk, "ms": round(msl, 4), "ms_median": round(medl, 4),
+            "tokens_per_s": round(wl.B * wl.T / (msl * 1e-3), 1),
+            "algorithmic_bytes": io,
+            "achieved_GBs": round(io / (msl * 1e-3) / 1e9, 1),
+            "peak_GBs": PEAK_HBM_GBS,
+            "frac": round(io / (msl * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        }
         if not args.no_gla:
             gld = inputs.draw_gla_decay(inputs.BASE_SEED + 105, wl.B, wl.H, wl.T, wl.d).to(dev)
-            fng = lambda: binding.fem_gla_fwd(qld, kld, vld, gld, bld, out=outl, chunk=wl.chunk)
-            msg = time_calls(fng, args.steps, args.warmup)
+            wsg = torch.empty(max(1, binding.workspace_bytes("gla", wl.B, wl.H, wl.T, wl.d, wl.dv,
+                                                             wl.chunk)), device=dev,
+                              dtype=torch.uint8)
+            fng = lambda: binding.fem_gla_fwd(qld, kld, vld, gld, bld, out=outl, chunk=wl.chunk,
+                                              ws=wsg)
+            msg, medg = time_calls(fng, args.steps, args.warmup)
             iog = 3 * ql.numel() * 2 + gld.numel() * 4 + outl.numel() * 4
             result["gla"] = {
                 "workload": wl.name.replace("linear", "gla"), "chunk": wl.chunk,
-                "ms": round(msg, 4), "tokens_per_s": round(wl.B * wl.T / (msg * 1e-3), 1),
+                "ms": round(msg, 4), "ms_median": round(medg, 4),
+                "tokens_per_s": round(wl.B * wl.T / (msg * 1e-3), 1),
                 "algorithmic_bytes": iog,
                 "achieved_GBs": round(iog / (msg * 1e-3) / 1e9, 1),
                 "peak_GBs": PEAK_HBM_GBS,
                 "frac": round(iog / (msg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             }
-            del gld
+            del gld, wsg
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(q, k, v, beta, args.cpu_budget)
