@@ -277,13 +277,17 @@ int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V,
  *   beta    : [H, d_v] float32, > 0
  *   out     : [B, H, T, d_v] float32
  *   d_k, d_v: 64 (both)
- *   chunk   : length of the intra-chunk (quadratic) block of the scan; 64.
- *             It only schedules the work: the result does not depend on it
- *             beyond rounding.  Other values return FEM_ERR_UNSUPPORTED.
+ *   chunk   : length of the intra-chunk (quadratic) block of the scan: 16, 32,
+ *             64 or 128.  A query sees the keys of its own chunk through the
+ *             masked product phi(Q_c) phi(K_c)^T and every earlier key
+ *             through the carried state.  The chunk only schedules the work:
+ *             the result does not depend on it beyond rounding.  Other
+ *             values return FEM_ERR_UNSUPPORTED.
  *   dtype   : FEM_DTYPE_BF16
  *
- * The scan runs in segments of c = ceil(ceil(T / 64) / w) chunks, w =
- * max(1, floor(512 / (B H))), S = ceil(ceil(T / 64) / c) segments per (b, h).
+ * The scan runs over tiles of L = max(chunk, 32) tokens (chunk 16: two
+ * chunks per tile) in segments of c = ceil(n / w) tiles, n = ceil(T / L),
+ * w = max(1, floor(512 / (B H))), S = ceil(n / c) segments per (b, h).
  * With S > 1 the segments' own states and the states entering them need a
  * workspace of
  *
@@ -321,10 +325,11 @@ int fem_linear_fwd(const void* Q, const void* K, const void* V,
  *             inside float range
  *   beta    : [H, d_v] float32, > 0
  *   out     : [B, H, T, d_v] float32
- *   d_k, d_v: 64 (both);  chunk: 64;  dtype: FEM_DTYPE_BF16
+ *   d_k, d_v: 64 (both);  chunk: 64 (the decay factors of a chunk stay
+ *             inside float range for 64 tokens);  dtype: FEM_DTYPE_BF16
  *
- * Workspace as fem_linear_fwd, each state carrying also its segment's total
- * log-decay per key channel (4288 floats):
+ * Workspace as fem_linear_fwd at chunk 64, each state carrying also its
+ * segment's total log-decay per key channel (4288 floats):
  *
  *   fem_gla_workspace_bytes(B, H, T, d_k, d_v, chunk) = 2 * 4 * B * H * S * 4288
  *

@@ -38,9 +38,10 @@ bool decode_sizes_ok(int B, int H, int L, int d_qk, int d_v) {
   return sizes_ok(B, H, L, d_qk) && sizes_ok(B, H, L, d_v) && (unsigned long long)B * H <= 65535ull;
 }
 
-bool scan_args_ok(int B, int H, int T, int d_k, int d_v, int chunk) {
-  return sizes_ok(B, H, T, d_k) && sizes_ok(B, H, T, d_v) && d_k == 64 && d_v == 64 &&
-         chunk == 64;
+// The linear scan takes chunks of 16, 32, 64 or 128 tokens; the GLA scan 64.
+bool scan_args_ok(int B, int H, int T, int d_k, int d_v, int chunk, bool gla) {
+  const bool chunk_ok = gla ? chunk == 64 : (chunk == 16 || chunk == 32 || chunk == 64 || chunk == 128);
+  return sizes_ok(B, H, T, d_k) && sizes_ok(B, H, T, d_v) && d_k == 64 && d_v == 64 && chunk_ok;
 }
 
 bool bwd_args_ok(int B, int H, int T, int d) {
@@ -173,12 +174,12 @@ extern "C" int fem_softmax_gated_fwd(const void* Q, const void* K, const void* V
 }
 
 extern "C" size_t fem_linear_workspace_bytes(int B, int H, int T, int d_k, int d_v, int chunk) {
-  if (!scan_args_ok(B, H, T, d_k, d_v, chunk)) return 0;
+  if (!scan_args_ok(B, H, T, d_k, d_v, chunk, false)) return 0;
   return fem::scan_ws_bytes(B, H, T, chunk, false);
 }
 
 extern "C" size_t fem_gla_workspace_bytes(int B, int H, int T, int d_k, int d_v, int chunk) {
-  if (!scan_args_ok(B, H, T, d_k, d_v, chunk)) return 0;
+  if (!scan_args_ok(B, H, T, d_k, d_v, chunk, true)) return 0;
   return fem::scan_ws_bytes(B, H, T, chunk, true);
 }
 
@@ -188,7 +189,7 @@ extern "C" int fem_linear_fwd(const void* Q, const void* K, const void* V, const
   if (!Q || !K || !V || !beta || !out) return FEM_ERR_NULLPTR;
   if (!sizes_ok(B, H, T, d_k) || !sizes_ok(B, H, T, d_v)) return FEM_ERR_SHAPE;
   if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
-  if (!scan_args_ok(B, H, T, d_k, d_v, chunk)) return FEM_ERR_UNSUPPORTED;
+  if (!scan_args_ok(B, H, T, d_k, d_v, chunk, false)) return FEM_ERR_UNSUPPORTED;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return FEM_ERR_ALIGN;
   const int w = check_ws(ws, ws_bytes, fem::scan_ws_bytes(B, H, T, chunk, false));
   if (w != FEM_OK) return w;
@@ -204,7 +205,7 @@ extern "C" int fem_gla_fwd(const void* Q, const void* K, const void* V, const fl
   if (!Q || !K || !V || !G || !beta || !out) return FEM_ERR_NULLPTR;
   if (!sizes_ok(B, H, T, d_k) || !sizes_ok(B, H, T, d_v)) return FEM_ERR_SHAPE;
   if (dtype != FEM_DTYPE_BF16) return FEM_ERR_UNSUPPORTED;
-  if (!scan_args_ok(B, H, T, d_k, d_v, chunk)) return FEM_ERR_UNSUPPORTED;
+  if (!scan_args_ok(B, H, T, d_k, d_v, chunk, true)) return FEM_ERR_UNSUPPORTED;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(G) || !aligned16(out))
     return FEM_ERR_ALIGN;
   const int w = check_ws(ws, ws_bytes, fem::scan_ws_bytes(B, H, T, chunk, true));

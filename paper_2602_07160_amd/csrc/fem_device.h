@@ -120,7 +120,7 @@ __device__ __forceinline__ void dma4(const void* src, void* dst) {
 __host__ __device__ constexpr int epos32(int r) {
   return (r & 16) + (((r >> 2) & 1) << 3) + (((r >> 3) & 1) << 2) + (r & 3);
 }
-__host__ __device__ constexpr int ppos(int x) { return (x & 32) + epos32(x & 31); }
+__host__ __device__ constexpr int ppos(int x) { return (x & ~31) + epos32(x & 31); }
 
 // A streamed [64][D] bf16 tile sits in LDS unpadded, 16-byte chunk c of row r
 // at chunk position c ^ swz(r).  swz makes both read patterns bank-conflict

@@ -54,7 +54,7 @@ namespace fem {
 namespace {
 
 constexpr int DK = 64, DV = 64;  // supported widths
-constexpr int CH = 64;           // tokens per chunk
+constexpr int GCH = 64;          // tokens per chunk of the GLA prior
 constexpr int NTH = 256;         // 4 waves
 constexpr int ROW = 64 + 8;      // padded bf16 row (64 values + 16 B)
 constexpr int SROW = DK + 8;     // padded S^T row (bf16)
@@ -99,36 +99,39 @@ constexpr float kUnderflow = 0x1p-64f;
 
 typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 
+// One tile of CH tokens; NSUB sub-chunks of CH / NSUB tokens per tile.  The
+// state enters the outputs of sub-chunk s as it stood at the start of s.
+template <int CH, int NSUB>
 struct LinSmem {
-  bf16 fq[CH * ROW];    // phi(Q) [token][d_k]
-  bf16 fk[CH * DK];     // phi(K) [key][d_k], swizzled; phi(K)^T comes from transposing reads
-  bf16 vs[CH * DV];     // V [key][d_v], swizzled; V^T comes from transposing reads
-  bf16 sh[DV * SROW];   // S^T hi [d_v][d_k]
-  bf16 sl[DV * SROW];   // S^T lo
-  float c[DV];          // running shift (published for the epilogue)
-  float bl[DV];         // beta log2 e
+  bf16 fq[CH * ROW];          // phi(Q) [token][d_k]
+  bf16 fk[CH * DK];           // phi(K) [key][d_k], swizzled; phi(K)^T comes from transposing reads
+  bf16 vs[CH * DV];           // V [key][d_v], swizzled; V^T comes from transposing reads
+  bf16 sh[NSUB][DV * SROW];   // S^T hi [d_v][d_k] at the start of each sub-chunk
+  bf16 sl[NSUB][DV * SROW];   // S^T lo
+  float c[DV];                // running shift (published for the epilogue)
+  float bl[DV];               // beta log2 e
   float inv[DV];
-  float z[DK];          // sum of phi(k) over earlier chunks
-  float zc[4 * DK];     // partial sums of phi(k) over this chunk (four row quarters)
+  float z[DK];                // sum of phi(k) over earlier tiles
+  float zc[4 * DK];           // partial sums of phi(k) over this tile (four row quarters)
 };
 
 // GLA: chunk-local running log-decay B[token][d_k] (fp32), its quarter
 // totals, and e^{R} z for the inter-chunk normaliser.
 struct GlaSmem {
-  float b[CH * DK];
+  float b[GCH * DK];
   float bq[4 * DK];
   float zr[DK];
-  bf16 fk2[CH * DK];  // k~ e^{B_last - B} [key][d_k], swizzled (the state update's operand)
+  bf16 fk2[GCH * DK];  // k~ e^{B_last - B} [key][d_k], swizzled (the state update's operand)
 };
-template <int PRIOR>
-struct ScanSmem : LinSmem {
+template <int PRIOR, int CH, int NSUB>
+struct ScanSmem : LinSmem<CH, NSUB> {
   __device__ float* gb() { return nullptr; }
   __device__ float* gbq() { return nullptr; }
   __device__ float* gzr() { return nullptr; }
-  __device__ bf16* fku() { return fk; }  // the state update's key features
+  __device__ bf16* fku() { return this->fk; }  // the state update's key features
 };
 template <>
-struct ScanSmem<kGla> : LinSmem {
+struct ScanSmem<kGla, GCH, 1> : LinSmem<GCH, 1> {
   GlaSmem gla;
   __device__ float* gb() { return gla.b; }
   __device__ float* gbq() { return gla.bq; }
@@ -238,10 +241,11 @@ __device__ float exact_read_linear(const bf16* __restrict__ Qh, const bf16* __re
   return (num.wave_total() - den.wave_total()) / bl;
 }
 
-// Raw Q, K, V of one chunk held in registers: thread tid covers the 16-byte
+// Raw Q, K, V of one tile held in registers: thread tid covers the 16-byte
 // slots e = tid + NTH*i (row e >> 3, columns (e & 7)*8 ..).
-constexpr int SLOTS = CH * 8 / NTH;
+template <int CH>
 struct ChunkRegs {
+  static constexpr int SLOTS = CH * 8 / NTH;
   bf16x8 q[SLOTS], k[SLOTS], v[SLOTS];
   f32x4 g[SLOTS][2];  // GLA log-decays of the slot's 8 channels
 };
@@ -262,9 +266,10 @@ __device__ __forceinline__ f32x4 load16f(__amdgpu_buffer_rsrc_t r, unsigned off)
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
 }
 
-template <int PRIOR, bool OUT>
-__device__ __forceinline__ void fetch_chunk(ChunkRegs& cr, const bf16* Qh, const bf16* Kh,
+template <int PRIOR, bool OUT, int CH>
+__device__ __forceinline__ void fetch_chunk(ChunkRegs<CH>& cr, const bf16* Qh, const bf16* Kh,
                                             const bf16* Vh, const float* Gh, int t0, int T) {
+  constexpr int SLOTS = ChunkRegs<CH>::SLOTS;
   const int tid = threadIdx.x;
   const unsigned rows = (unsigned)min(CH, T - t0);
   const __amdgpu_buffer_rsrc_t rk = rsrc(Kh + (size_t)t0 * DK, rows * DK * 2u);
@@ -288,28 +293,42 @@ __device__ __forceinline__ void fetch_chunk(ChunkRegs& cr, const bf16* Qh, const
   }
 }
 
-// One chunk of the scan.  Stages tokens [t0, t0 + CH) from cr (rows past T
-// are zero and masked), starts fetching the next chunk into cr, forms the
+// One tile of the scan.  Stages tokens [t0, t0 + CH) from cr (rows past T
+// are zero and masked), starts fetching the next tile into cr, forms the
 // tilt, rescales the state, produces outputs (OUT) and updates S.
 // Wave w owns channel block dvb = w >> 1 and sub = w & 1: S^T block
-// (dvb, d_k block sub) and output block (dvb, query block sub).
+// (dvb, d_k block sub) and the outputs of channel block dvb for the query
+// blocks qb = sub, sub + 2, ... of the tile.
 //
-// The tilt E^T (32 channels x 64 keys of the wave's block) is formed in
+// The chunk of the scan is CH / NSUB tokens: a query sees the keys of its
+// own chunk through the masked intra-chunk product A and every earlier key
+// through the state.  With NSUB = 2 (16-token chunks in a 32-token tile) the
+// state also advances by the first chunk's keys before the second chunk's
+// outputs, which read it as a second snapshot.
+//
+// The tilt E^T (32 channels x CH keys of the wave's block) is formed in
 // registers as the MFMA A operand: lane (n, hl) holds channel dvb*32 + n and
 // the keys at MFMA positions ks*16 + hl*8 .. +8 of each k-step ks, read from
 // V^T staged in the same key order.  The two waves of a channel block form
 // the same E; each lane keeps the running shift cj of its channel.
-template <int PRIOR, bool OUT>
-__device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, float& cj, float blj,
-                                           float& ldc, ChunkRegs& cr, const bf16* Qh,
-                                           const bf16* Kh, const bf16* Vh, const float* Gh,
-                                           float* Oh, int t0, int tnext, int T) {
+template <int PRIOR, bool OUT, int CH, int NSUB>
+__device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16& st, float& cj,
+                                           float blj, float& ldc, ChunkRegs<CH>& cr,
+                                           const bf16* Qh, const bf16* Kh, const bf16* Vh,
+                                           const float* Gh, float* Oh, int t0, int tnext, int T) {
+  constexpr int SLOTS = ChunkRegs<CH>::SLOTS;
+  constexpr int NKS = CH / 16;    // 16-key k-steps of the tile
+  constexpr int NQB = CH / 32;    // 32-row query blocks of the tile
+  constexpr int SUB = CH / NSUB;  // tokens per chunk
+  static_assert(CH == 32 || CH == 64 || CH == 128, "tile length");
+  static_assert(NSUB == 1 || (CH == 32 && NSUB == 2), "two 16-token chunks per 32-token tile");
+  static_assert(PRIOR != kGla || (CH == GCH && NSUB == 1), "GLA: 64-token chunks");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, hl = lane >> 5;
   const int dvb = wave >> 1, sub = wave & 1;
   const int ch = dvb * 32 + n;
 
-  if (PRIOR == kGla) {
+  if constexpr (PRIOR == kGla) {
     // ---- chunk-local running log-decay B down each key channel: clipped g
     // into LDS, prefix of each quarter of 16 rows, then the lower quarters'
     // totals added (rows past T hold g = 0 from the fetch)
@@ -358,7 +377,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     // rows past T: phi of the zeros fetched there, times 0 (no branch)
     const float okf = t0 + r < T ? 1.f : 0.f;
     bf16x8 pk, pq;
-    if (PRIOR == kGla) {
+    if constexpr (PRIOR == kGla) {
       float kx[8], qx[8];
       bf16x8 pu;
 #pragma unroll
@@ -392,23 +411,23 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.vs) + swz_off<DV>(r, c8 >> 3)) = cr.v[i];
     if (OUT) *reinterpret_cast<bf16x8*>(sm.fq + r * ROW + c8) = pq;
   }
-  // the next chunk's loads run while this one is processed
-  if (tnext < T) fetch_chunk<PRIOR, OUT>(cr, Qh, Kh, Vh, Gh, tnext, T);
+  // the next tile's loads run while this one is processed
+  if (tnext < T) fetch_chunk<PRIOR, OUT, CH>(cr, Qh, Kh, Vh, Gh, tnext, T);
   lds_barrier();
 
   // ---- tilt of the wave's channel block, in registers
-  bf16x8 eh[4], el[4];
+  bf16x8 eh[NKS], el[NKS];
   float gj;
   bool rose;
   {
-    bf16x8 vr[4];
+    bf16x8 vr[NKS];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) vr[ks] = frag_tr<DV>(sm.vs, dvb * 32, ks * 16);
-    // keys at or past T (last chunk only) stay out of the max and give E = 0
+    for (int ks = 0; ks < NKS; ++ks) vr[ks] = frag_tr<DV>(sm.vs, dvb * 32, ks * 16);
+    // keys at or past T (last tile only) stay out of the max and give E = 0
     const bool full = t0 + CH <= T;
     float vmax = -INFINITY;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
       for (int u = 0; u < 8; ++u)
         if (full || t0 + e_pos(ks * 16 + hl * 8 + u) < T) vmax = fmaxf(vmax, (float)vr[ks][u]);
@@ -421,7 +440,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
     rose = __any(cnew != cj);
     cj = cnew;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
       for (int u = 0; u < 8; u += 2) {
         float ev[2];
@@ -440,7 +459,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
       }
     }
   }
-  // chunk sum of phi(k): thread (column tid & 63, quarter tid >> 6) sums 16
+  // tile sum of phi(k): thread (column tid & 63, quarter tid >> 6) sums CH/4
   // rows; the four partial sums meet in LDS
   {
     const int dkc = tid & 63, q4 = tid >> 6;
@@ -459,139 +478,174 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR>& sm, f32x16& st, floa
 #pragma unroll
     for (int i = 0; i < 16; ++i) st[i] *= __shfl(gj, (i >> 2) * 8 + hl * 4 + (i & 3));
   }
-  if (OUT) {
-    const float eR =
-        PRIOR == kGla ? exp2_hw(sm.gb()[(CH / 2 - 1) * DK + sub * 32 + n] * kLog2e) : 1.f;
+  // S^T(dvb, dkb = sub) += E^T phi(K) over the keys of k-steps [k0, k1)
+  auto update = [&](int k0, int k1) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
-      const int col = sub * 32 + n;
-      const float sv = st[i] * eR;
-      const bf16 hi = (bf16)sv;
-      sm.sh[row * SROW + col] = hi;
-      sm.sl[row * SROW + col] = (bf16)(sv - (float)hi);
-    }
-    if (sub == 0 && hl == 0) sm.c[ch] = cj;
-    lds_barrier();
-
-    // ---- outputs of query block qb = sub, channel block dvb
-    const int qb = sub;
-    const int tq = t0 + qb * 32 + n;
-    // A^T blocks (keys kb x queries qb), kb <= qb; masked (key > query),
-    // rounded to bf16, normaliser from the rounded values
-    bf16x8 pf[4] = {};
-    float den = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      if (kb > qb) continue;
-      f32x16 at = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < DK / 16; ++ks) {
-        const bf16x8 a = frag_rows<DK>(sm.fk, kb * 32 + n, 2 * ks + hl);
-        const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + (qb * 32 + n) * ROW + ks * 16 + hl * 8);
-        at = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, at, 0, 0, 0);
-      }
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int ks = kb * 2 + half, s0 = half * 8;
-#pragma unroll
-        for (int u = 0; u < 8; u += 2) {
-          const int i0 = s0 + u, i1 = s0 + u + 1;
-          const int key0 = kb * 32 + (i0 >> 2) * 8 + hl * 4 + (i0 & 3);
-          const int key1 = kb * 32 + (i1 >> 2) * 8 + hl * 4 + (i1 & 3);
-          const float a0 = (key0 <= qb * 32 + n) ? at[i0] : 0.f;
-          const float a1 = (key1 <= qb * 32 + n) ? at[i1] : 0.f;
-          const bf16x2 p2 = to_bf16x2(a0, a1);
-          pf[ks][u] = p2[0];
-          pf[ks][u + 1] = p2[1];
-          den = add_bf16x2(p2, den);
-        }
-      }
-    }
-    // numerator: E^T A^T (intra) + S^T phi(Q)^T (inter); the inter-chunk
-    // normaliser phi(q)^T z (this lane's half of d_k) reuses the phi(Q)
-    // fragments, with four partial sums
-    f32x16 num = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      if ((ks >> 1) > qb) continue;
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eh[ks], pf[ks], num, 0, 0, 0);
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el[ks], pf[ks], num, 0, 0, 0);
-    }
-    const int soff = (dvb * 32 + n) * SROW + hl * 8;
-    float dz[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < DK / 16; ++ks) {
-      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.sh + soff + ks * 16);
-      const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.sl + soff + ks * 16);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + (qb * 32 + n) * ROW + ks * 16 + hl * 8);
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
-      num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, num, 0, 0, 0);
-      const float* zz = PRIOR == kGla ? sm.gzr() : sm.z;
-      const f32x4 z0 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8);
-      const f32x4 z1 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8 + 4);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        dz[u] = fmaf((float)b[u], z0[u], dz[u]);
-        dz[u] = fmaf((float)b[u + 4], z1[u], dz[u]);
-      }
-    }
-    den += (dz[0] + dz[1]) + (dz[2] + dz[3]);
-    den += other_half(den);
-    // epilogue
-    int ed;
-    const float fd = log2_hw(frexpf(den, &ed));
-    uint32_t flags = 0;
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const int ch0 = dvb * 32 + g4 * 8 + hl * 4;
-      const f32x4 cc = *reinterpret_cast<const f32x4*>(sm.c + ch0);
-      const f32x4 iv = *reinterpret_cast<const f32x4*>(sm.inv + ch0);
-      f32x4 o;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float a = num[g4 * 4 + e];
-        int ea;
-        const float fa = log2_hw(frexpf(a, &ea));
-        o[e] = ((float)(ea - ed - (int)kBias) + (fa - fd) + cc[e]) * iv[e];
-        if (!(a >= kUnderflow) && tq < T) flags |= 1u << (g4 * 4 + e);
-      }
-      if (tq < T) *reinterpret_cast<f32x4*>(Oh + (size_t)tq * DV + ch0) = o;
-    }
-    while (true) {
-      const uint64_t who = __ballot(flags != 0);
-      if (who == 0) break;
-      const int src = __builtin_ctzll(who);
-      const uint32_t fl = __builtin_amdgcn_readlane(flags, src);
-      const int e = __builtin_ctz(fl);
-      const int t = __builtin_amdgcn_readlane(tq, src);
-      const int ch2 = dvb * 32 + (e >> 2) * 8 + (src >> 5) * 4 + (e & 3);
-      const float o = PRIOR == kGla ? exact_read_gla(Qh, Kh, Vh, Gh, t, ch2, sm.bl[ch2])
-                                    : exact_read_linear(Qh, Kh, Vh, t, ch2, sm.bl[ch2]);
-      if (lane == src) {
-        flags &= ~(1u << e);
-        Oh[(size_t)t * DV + ch2] = o;
-      }
-    }
-  }
-
-  // ---- state update S^T(dvb, dkb = sub) += E^T phi(K)   (keys of this chunk);
-  // GLA: the state first decays by e^{B_last} along its key channel (column)
-  {
-    if (PRIOR == kGla) {
-      const float dcy = exp2_hw(sm.gb()[(CH - 1) * DK + sub * 32 + n] * kLog2e);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) st[i] *= dcy;
-    }
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks) {
+      if (ks < k0 || ks >= k1) continue;
       const bf16x8 b = frag_tr<DK>(sm.fku(), sub * 32, ks * 16);
       st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eh[ks], b, st, 0, 0, 0);
       st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el[ks], b, st, 0, 0, 0);
     }
+  };
+  // the state update of the first chunk's keys comes before the second
+  // chunk's snapshot (NSUB = 2); the rest after the outputs
+  constexpr int KS_EARLY = NSUB == 2 ? NKS / 2 : 0;
+  if (OUT) {
+    const float eR =
+        PRIOR == kGla ? exp2_hw(sm.gb()[(CH / 2 - 1) * DK + sub * 32 + n] * kLog2e) : 1.f;
+    auto snapshot = [&](int sn) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
+        const int col = sub * 32 + n;
+        const float sv = st[i] * eR;
+        const bf16 hi = (bf16)sv;
+        sm.sh[sn][row * SROW + col] = hi;
+        sm.sl[sn][row * SROW + col] = (bf16)(sv - (float)hi);
+      }
+    };
+    snapshot(0);
+    if (NSUB == 2) {
+      update(0, KS_EARLY);
+      snapshot(1);
+    }
+    if (sub == 0 && hl == 0) sm.c[ch] = cj;
+    lds_barrier();
+
+    // ---- outputs of channel block dvb for the query blocks of this wave
+#pragma unroll
+    for (int qb = sub; qb < NQB; qb += 2) {
+      const int qrow = qb * 32 + n;  // query row within the tile
+      const int tq = t0 + qrow;
+      const int qs = qrow / SUB;     // its chunk within the tile
+      // A^T blocks (keys kb x queries qb), kb <= qb; masked to keys of the
+      // query's own chunk at or before it, rounded to bf16, normaliser from
+      // the rounded values
+      bf16x8 pf[NKS];
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) pf[ks] = bf16x8{};
+      float den = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < NQB; ++kb) {
+        if (kb > qb) continue;
+        f32x16 at = f32x16{};
+#pragma unroll
+        for (int ks = 0; ks < DK / 16; ++ks) {
+          const bf16x8 a = frag_rows<DK>(sm.fk, kb * 32 + n, 2 * ks + hl);
+          const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + qrow * ROW + ks * 16 + hl * 8);
+          at = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, at, 0, 0, 0);
+        }
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int ks = kb * 2 + half, s0 = half * 8;
+#pragma unroll
+          for (int u = 0; u < 8; u += 2) {
+            const int i0 = s0 + u, i1 = s0 + u + 1;
+            const int key0 = kb * 32 + (i0 >> 2) * 8 + hl * 4 + (i0 & 3);
+            const int key1 = kb * 32 + (i1 >> 2) * 8 + hl * 4 + (i1 & 3);
+            const bool in0 = key0 <= qrow && (NSUB == 1 || key0 / SUB == qs);
+            const bool in1 = key1 <= qrow && (NSUB == 1 || key1 / SUB == qs);
+            const bf16x2 p2 = to_bf16x2(in0 ? at[i0] : 0.f, in1 ? at[i1] : 0.f);
+            pf[ks][u] = p2[0];
+            pf[ks][u + 1] = p2[1];
+            den = add_bf16x2(p2, den);
+          }
+        }
+      }
+      // numerator: E^T A^T (intra) + S^T phi(Q)^T (inter, the state at the
+      // start of the query's chunk); the inter-chunk normaliser phi(q)^T z
+      // (this lane's half of d_k) reuses the phi(Q) fragments, with four
+      // partial sums
+      f32x16 num = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        if ((ks >> 1) > qb) continue;
+        num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eh[ks], pf[ks], num, 0, 0, 0);
+        num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el[ks], pf[ks], num, 0, 0, 0);
+      }
+      const int soff = (dvb * 32 + n) * SROW + hl * 8;
+      float dz[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int sn = 0; sn < NSUB; ++sn) {
+        // NSUB = 2: snapshot sn feeds only the query columns of chunk sn
+        const bool mine = NSUB == 1 || qs == sn;
+#pragma unroll
+        for (int ks = 0; ks < DK / 16; ++ks) {
+          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.sh[sn] + soff + ks * 16);
+          const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.sl[sn] + soff + ks * 16);
+          bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + qrow * ROW + ks * 16 + hl * 8);
+          if (!mine) b = bf16x8{};
+          num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
+          num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, num, 0, 0, 0);
+          const float* zz = PRIOR == kGla ? sm.gzr() : sm.z;
+          f32x4 z0 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8);
+          f32x4 z1 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8 + 4);
+          if (NSUB == 2 && sn == 1) {  // plus the first chunk's phi(k) (quarters 0, 1)
+            z0 += *reinterpret_cast<const f32x4*>(sm.zc + ks * 16 + hl * 8) +
+                  *reinterpret_cast<const f32x4*>(sm.zc + DK + ks * 16 + hl * 8);
+            z1 += *reinterpret_cast<const f32x4*>(sm.zc + ks * 16 + hl * 8 + 4) +
+                  *reinterpret_cast<const f32x4*>(sm.zc + DK + ks * 16 + hl * 8 + 4);
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            dz[u] = fmaf((float)b[u], z0[u], dz[u]);
+            dz[u] = fmaf((float)b[u + 4], z1[u], dz[u]);
+          }
+        }
+      }
+      den += (dz[0] + dz[1]) + (dz[2] + dz[3]);
+      den += other_half(den);
+      // epilogue
+      int ed;
+      const float fd = log2_hw(frexpf(den, &ed));
+      uint32_t flags = 0;
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int ch0 = dvb * 32 + g4 * 8 + hl * 4;
+        const f32x4 cc = *reinterpret_cast<const f32x4*>(sm.c + ch0);
+        const f32x4 iv = *reinterpret_cast<const f32x4*>(sm.inv + ch0);
+        f32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float a = num[g4 * 4 + e];
+          int ea;
+          const float fa = log2_hw(frexpf(a, &ea));
+          o[e] = ((float)(ea - ed - (int)kBias) + (fa - fd) + cc[e]) * iv[e];
+          if (!(a >= kUnderflow) && tq < T) flags |= 1u << (g4 * 4 + e);
+        }
+        if (tq < T) *reinterpret_cast<f32x4*>(Oh + (size_t)tq * DV + ch0) = o;
+      }
+      while (true) {
+        const uint64_t who = __ballot(flags != 0);
+        if (who == 0) break;
+        const int src = __builtin_ctzll(who);
+        const uint32_t fl = __builtin_amdgcn_readlane(flags, src);
+        const int e = __builtin_ctz(fl);
+        const int t = __builtin_amdgcn_readlane(tq, src);
+        const int ch2 = dvb * 32 + (e >> 2) * 8 + (src >> 5) * 4 + (e & 3);
+        const float o = PRIOR == kGla ? exact_read_gla(Qh, Kh, Vh, Gh, t, ch2, sm.bl[ch2])
+                                      : exact_read_linear(Qh, Kh, Vh, t, ch2, sm.bl[ch2]);
+        if (lane == src) {
+          flags &= ~(1u << e);
+          Oh[(size_t)t * DV + ch2] = o;
+        }
+      }
+    }
   }
-  // every read of this chunk's LDS tiles and of z is done before the next
-  // chunk stages and before z moves on
+
+  // ---- state update S^T(dvb, dkb = sub) += E^T phi(K)   (keys of this tile);
+  // GLA: the state first decays by e^{B_last} along its key channel (column)
+  {
+    if constexpr (PRIOR == kGla) {
+      const float dcy = exp2_hw(sm.gb()[(CH - 1) * DK + sub * 32 + n] * kLog2e);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) st[i] *= dcy;
+    }
+    update(OUT ? KS_EARLY : 0, NKS);
+  }
+  // every read of this tile's LDS tiles and of z is done before the next
+  // tile stages and before z moves on
   // (B_last is read before the barrier: the next chunk overwrites B after it)
   const float blast = (PRIOR == kGla && tid < DK) ? sm.gb()[(CH - 1) * DK + tid] : 0.f;
   lds_barrier();
@@ -644,7 +698,7 @@ __global__ __launch_bounds__(NTH) void prefix_kernel(const float* __restrict__ o
   }
 }
 
-template <int PRIOR, bool OUT>
+template <int PRIOR, bool OUT, int CH, int NSUB>
 __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
                                                      const bf16* __restrict__ K,
                                                      const bf16* __restrict__ V,
@@ -654,7 +708,7 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
                                                      float* __restrict__ ws, int H, int T,
                                                      int nseg, int segc) {
   constexpr int SF = state_floats<PRIOR>();
-  __shared__ __align__(16) ScanSmem<PRIOR> sm;
+  __shared__ __align__(16) ScanSmem<PRIOR, CH, NSUB> sm;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hl = lane >> 5;
   const int seg = blockIdx.x % nseg;
@@ -683,8 +737,8 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
 
   const int tbeg = seg * segc * CH;
   const int tend = min(tbeg + segc * CH, T);
-  ChunkRegs cr;
-  fetch_chunk<PRIOR, OUT>(cr, Qh, Kh, Vh, Gh, tbeg, T);
+  ChunkRegs<CH> cr;
+  fetch_chunk<PRIOR, OUT, CH>(cr, Qh, Kh, Vh, Gh, tbeg, T);
 
   if (OUT && seg > 0) {
     // entering state, left by the prefix kernel in the second half of ws
@@ -701,8 +755,8 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   }
 
   for (int t0 = tbeg; t0 < tend; t0 += CH)
-    scan_chunk<PRIOR, OUT>(sm, st, cj, blj, ldc, cr, Qh, Kh, Vh, Gh, Oh, t0,
-                           t0 + CH < tend ? t0 + CH : T, T);
+    scan_chunk<PRIOR, OUT, CH, NSUB>(sm, st, cj, blj, ldc, cr, Qh, Kh, Vh, Gh, Oh, t0,
+                                     t0 + CH < tend ? t0 + CH : T, T);
 
   if (!OUT) {
     float* S = wsh + (size_t)seg * SF;
@@ -720,20 +774,22 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
 }
 
 // Segments of one call: the scan is sequential inside a segment, so the
-// fewest chunks per segment that still give about kScanSlots (b, h, segment)
+// fewest tiles per segment that still give about kScanSlots (b, h, segment)
 // workgroups (two per compute unit of a 256-CU device, all resident at
 // once).  A function of the sizes only, so the workspace query needs no
-// device.
+// device.  Tiles are max(chunk, 32) tokens.
 constexpr int kScanSlots = 512;
+
+int tile_of_chunk(int chunk) { return chunk < 32 ? 32 : chunk; }
 
 struct ScanPlan {
   int nseg, segc;
-  ScanPlan(int B, int H, int T) {
+  ScanPlan(int B, int H, int T, int tile) {
     const int nbh = B * H;
-    const int nchunk = (T + CH - 1) / CH;
+    const int ntile = (T + tile - 1) / tile;
     const int want = max(1, kScanSlots / nbh);
-    segc = (nchunk + want - 1) / want;
-    nseg = (nchunk + segc - 1) / segc;
+    segc = (ntile + want - 1) / want;
+    nseg = (ntile + segc - 1) / segc;
   }
   // own segment states, then the entering (prefix) states; nothing when the
   // whole sequence is one segment
@@ -744,13 +800,13 @@ struct ScanPlan {
   }
 };
 
-template <int PRIOR>
+template <int PRIOR, int CH, int NSUB>
 hipError_t launch_scan(const void* Q, const void* K, const void* V, const float* G,
                        const float* beta, float* out, int B, int H, int T, void* wsv,
                        hipStream_t stream) {
   constexpr int SF = state_floats<PRIOR>();
   const int nbh = B * H;
-  const ScanPlan plan(B, H, T);
+  const ScanPlan plan(B, H, T, CH);
   const int nseg = plan.nseg, segc = plan.segc;
   float* ws = static_cast<float*>(wsv);
   const bf16* q = reinterpret_cast<const bf16*>(Q);
@@ -758,8 +814,8 @@ hipError_t launch_scan(const void* Q, const void* K, const void* V, const float*
   const bf16* v = reinterpret_cast<const bf16*>(V);
   hipError_t e = hipSuccess;
   if (nseg > 1) {
-    hipLaunchKernelGGL((linear_kernel<PRIOR, false>), dim3((unsigned)(nbh * nseg)), dim3(NTH), 0,
-                       stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
+    hipLaunchKernelGGL((linear_kernel<PRIOR, false, CH, NSUB>), dim3((unsigned)(nbh * nseg)),
+                       dim3(NTH), 0, stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
     e = hipGetLastError();
     if (e == hipSuccess) {
       hipLaunchKernelGGL(prefix_kernel<PRIOR>,
@@ -769,8 +825,8 @@ hipError_t launch_scan(const void* Q, const void* K, const void* V, const float*
     }
   }
   if (e == hipSuccess) {
-    hipLaunchKernelGGL((linear_kernel<PRIOR, true>), dim3((unsigned)(nbh * nseg)), dim3(NTH), 0,
-                       stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
+    hipLaunchKernelGGL((linear_kernel<PRIOR, true, CH, NSUB>), dim3((unsigned)(nbh * nseg)),
+                       dim3(NTH), 0, stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
     e = hipGetLastError();
   }
   return e;
@@ -779,22 +835,27 @@ hipError_t launch_scan(const void* Q, const void* K, const void* V, const float*
 }  // namespace
 
 size_t scan_ws_bytes(int B, int H, int T, int chunk, bool gla) {
-  (void)chunk;
-  return ScanPlan(B, H, T).bytes(B, H, gla);
+  return ScanPlan(B, H, T, tile_of_chunk(chunk)).bytes(B, H, gla);
 }
 
 hipError_t launch_linear_bf16(const void* Q, const void* K, const void* V, const float* beta,
                               float* out, int B, int H, int T, int dk, int dv, int chunk,
                               void* ws, hipStream_t stream) {
-  if (dk != DK || dv != DV || chunk != CH) return hipErrorNotSupported;
-  return launch_scan<kElu>(Q, K, V, nullptr, beta, out, B, H, T, ws, stream);
+  if (dk != DK || dv != DV) return hipErrorNotSupported;
+  switch (chunk) {
+    case 16: return launch_scan<kElu, 32, 2>(Q, K, V, nullptr, beta, out, B, H, T, ws, stream);
+    case 32: return launch_scan<kElu, 32, 1>(Q, K, V, nullptr, beta, out, B, H, T, ws, stream);
+    case 64: return launch_scan<kElu, 64, 1>(Q, K, V, nullptr, beta, out, B, H, T, ws, stream);
+    case 128: return launch_scan<kElu, 128, 1>(Q, K, V, nullptr, beta, out, B, H, T, ws, stream);
+    default: return hipErrorNotSupported;
+  }
 }
 
 hipError_t launch_gla_bf16(const void* Q, const void* K, const void* V, const float* G,
                            const float* beta, float* out, int B, int H, int T, int dk, int dv,
                            int chunk, void* ws, hipStream_t stream) {
-  if (dk != DK || dv != DV || chunk != CH) return hipErrorNotSupported;
-  return launch_scan<kGla>(Q, K, V, G, beta, out, B, H, T, ws, stream);
+  if (dk != DK || dv != DV || chunk != GCH) return hipErrorNotSupported;
+  return launch_scan<kGla, GCH, 1>(Q, K, V, G, beta, out, B, H, T, ws, stream);
 }
 
 }  // namespace fem

@@ -77,8 +77,12 @@ def test_linear_validation(lib):
     assert ln(lib, T=0) == SHAPE
     assert ln(lib, dk=32) == UNSUPPORTED
     assert ln(lib, dv=128) == UNSUPPORTED
-    assert ln(lib, chunk=48) == UNSUPPORTED
-    assert ln(lib, chunk=32) == UNSUPPORTED
+    for c in (0, 8, 48, 96, 256):
+        assert ln(lib, chunk=c) == UNSUPPORTED, c
+    # chunks 16, 32, 64 and 128 pass the chunk check (another argument fails)
+    for c in (16, 32, 64, 128):
+        assert ln(lib, chunk=c, dk=32) == UNSUPPORTED
+        assert ln(lib, chunk=c, v=A + 2) == ALIGN
     assert ln(lib, dt=F32) == UNSUPPORTED
     assert ln(lib, v=A + 2) == ALIGN
 
@@ -181,11 +185,11 @@ def want_decode(B, H, L, dqk, dv):
     return 8 * B * H * cdiv(blocks, n) * (dv + 1)
 
 
-def want_scan(B, H, T, gla):
-    nchunk = cdiv(T, 64)
+def want_scan(B, H, T, gla, chunk=64):
+    ntile = cdiv(T, max(chunk, 32))
     w = max(1, 512 // (B * H))
-    c = cdiv(nchunk, w)
-    S = cdiv(nchunk, c)
+    c = cdiv(ntile, w)
+    S = cdiv(ntile, c)
     return 0 if S == 1 else 2 * 4 * B * H * S * (4288 if gla else 4224)
 
 
@@ -205,7 +209,9 @@ def test_workspace_queries(lib):
         for dqk, dv in ((32, 32), (64, 64), (128, 128), (64, 32), (128, 64)):
             assert lib.fem_softmax_decode_workspace_bytes(B, H, T, dqk, dv) == \
                 want_decode(B, H, T, dqk, dv), (B, H, T, dqk, dv)
-        assert lib.fem_linear_workspace_bytes(B, H, T, 64, 64, 64) == want_scan(B, H, T, False)
+        for c in (16, 32, 64, 128):
+            assert lib.fem_linear_workspace_bytes(B, H, T, 64, 64, c) == \
+                want_scan(B, H, T, False, c), (B, H, T, c)
         assert lib.fem_gla_workspace_bytes(B, H, T, 64, 64, 64) == want_scan(B, H, T, True)
         for d in (32, 64, 128):
             assert lib.fem_softmax_bwd_workspace_bytes(B, H, T, d) == want_bwd(B, H, T, d)
@@ -215,6 +221,8 @@ def test_workspace_queries(lib):
     assert lib.fem_linear_workspace_bytes(4, 16, 8192, 64, 64, 64) == 2 * 4 * 64 * 8 * 4224
     # arguments outside the supported set give 0
     assert lib.fem_linear_workspace_bytes(4, 16, 8192, 32, 64, 64) == 0
+    assert lib.fem_linear_workspace_bytes(4, 16, 8192, 64, 64, 48) == 0
+    assert lib.fem_gla_workspace_bytes(4, 16, 8192, 64, 64, 32) == 0
     assert lib.fem_linear_workspace_bytes(0, 16, 8192, 64, 64, 64) == 0
     assert lib.fem_softmax_decode_workspace_bytes(1, 1, 8, 32, 64) == 0
     assert lib.fem_softmax_bwd_workspace_bytes(1, 1, 8, 48) == 0

@@ -110,12 +110,60 @@ def test_linear_rejects_unsupported(fem):
     dev = torch.device("cuda:0")
     q = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16, device=dev)
     b = torch.ones(1, 64, device=dev)
-    with pytest.raises(fem.FemError) as e:
-        fem.fem_linear_fwd(q, q, q, b, chunk=32)
-    assert e.value.status == 3
+    for c in (8, 48, 256):
+        with pytest.raises(fem.FemError) as e:
+            fem.fem_linear_fwd(q, q, q, b, chunk=c)
+        assert e.value.status == 3
     q32 = torch.zeros(1, 1, 8, 32, dtype=torch.bfloat16, device=dev)
     with pytest.raises(fem.FemError):
         fem.fem_linear_fwd(q32, q32, q32, torch.ones(1, 32, device=dev))
+
+
+CHUNKS = (16, 32, 64, 128)
+
+
+@pytest.mark.parametrize("chunk", CHUNKS)
+@pytest.mark.parametrize("T", [1, 15, 16, 17, 31, 33, 64, 127, 129, 300, 1000])
+def test_linear_chunks_small(fem, chunk, T):
+    seed = 5100 + T + chunk
+    say(f"linear chunk {chunk}: B2 H3 T{T} d64, seed {seed}")
+    q, k, v, b = inputs.draw(seed, 2, 3, T, 64, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
+    check(run(fem, q, k, v, b, chunk=chunk), ref(q, k, v, b), TOL, f"linear chunk {chunk} T{T}")
+
+
+def test_linear_chunk_invariance(fem):
+    """The chunk only schedules the scan (the result is chunk-independent in
+    exact arithmetic): every chunk length matches the oracle, and the four
+    schedules agree with each other to the same budget, on a case with many
+    segments, a ragged tail and both small and large beta."""
+    say("linear chunk invariance: B2 H4 T3001 d64, chunks 16/32/64/128, seed 5201")
+    q, k, v, b = inputs.draw(5201, 2, 4, 3001, 64, dtype="bf16", beta_lo=0.05, beta_hi=8.0)
+    want = ref(q, k, v, b)
+    got = {c: run(fem, q, k, v, b, chunk=c) for c in CHUNKS}
+    for c in CHUNKS:
+        check(got[c], want, TOL, f"chunk {c} vs oracle")
+    for c in CHUNKS[1:]:
+        d = np.abs(got[c] - got[CHUNKS[0]]).max()
+        say(f"chunk {c} vs chunk {CHUNKS[0]}: max abs diff {d:.3e}")
+        assert d <= TOL
+    # the schedules differ: chunk 16 routes half of each tile's keys through
+    # the state, chunk 128 through the masked product
+    assert not np.array_equal(got[16], got[128])
+
+
+@pytest.mark.parametrize("chunk", (16, 32, 128))
+def test_workload5_other_chunks_sampled(fem, chunk):
+    say(f"workload 5 at chunk {chunk}: B4 H16 T8192 d64, sampled rows")
+    q, k, v, b = inputs.make_inputs(5)
+    got = run(fem, q, k, v, b, chunk=chunk)
+    rows = np.array([0, 1, 15, 16, 17, 31, 32, 127, 128, 4095, 4096, 8191])
+    for bb, hh in [(0, 0), (3, 15)]:
+        want = oracle.fem_linear(q[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                 k[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                 v[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                 b[hh:hh + 1].double().numpy(), rows=rows)
+        check(got[bb:bb + 1, hh:hh + 1][:, :, rows], want, TOL,
+              f"workload 5 chunk {chunk} (b={bb}, h={hh})")
 
 
 def test_linear_caller_workspace(fem):
