@@ -39,20 +39,23 @@ def check(got, want, tol, what):
     assert err <= tol, f"{what}: max abs err {err} > {tol}"
 
 
-def test_workload5_full_size_sampled(fem):
-    say("workload 5: linear bf16 B4 H16 T8192 d64 chunk 64, seed 47, sampled rows")
+def test_workload5_full_size_every_row(fem):
+    say("workload 5: linear bf16 B4 H16 T8192 d64 chunk 64, seed 47, every head and row")
     q, k, v, b = inputs.make_inputs(5)
     got = run(fem, q, k, v, b)
-    rng = np.random.default_rng(5)
-    rows = sorted(set([0, 1, 63, 64, 511, 512, 513, 4095, 8190, 8191]) |
-                  set(int(x) for x in rng.integers(0, 8192, 14)))
-    rows = np.array(rows)
-    for bb, hh in [(0, 0), (1, 9), (3, 15)]:
-        want = oracle.fem_linear(q[bb:bb + 1, hh:hh + 1].double().numpy(),
-                                 k[bb:bb + 1, hh:hh + 1].double().numpy(),
-                                 v[bb:bb + 1, hh:hh + 1].double().numpy(),
-                                 b[hh:hh + 1].double().numpy(), rows=rows)[0, 0]
-        check(got[bb, hh, rows], want, TOL, f"w5 b{bb} h{hh}")
+    worst = 0.0
+    for bb in range(4):
+        for hh in range(16):
+            want = oracle.fem_linear(q[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                     k[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                     v[bb:bb + 1, hh:hh + 1].double().numpy(),
+                                     b[hh:hh + 1].double().numpy())[0, 0]
+            assert np.isfinite(got[bb, hh]).all()
+            err = float(np.abs(got[bb, hh] - want).max())
+            worst = max(worst, err)
+            assert err <= TOL, f"workload 5 b{bb} h{hh}: {err} > {TOL}"
+        say(f"workload 5: batch {bb} done, worst max abs err so far {worst:.3e}")
+    say(f"workload 5: all 64 heads, every row: max abs err {worst:.3e} (tol {TOL})")
 
 
 def test_workload5_reduced_full(fem):
