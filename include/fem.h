@@ -319,10 +319,13 @@ int fem_linear_fwd(const void* Q, const void* K, const void* V,
  *
  *   Q, K    : [B, H, T, d_k] bfloat16
  *   V       : [B, H, T, d_v] bfloat16
- *   G       : [B, H, T, d_k] float32 log-decays; clipped to [-2, 0] (a decay
- *             factor of at least e^-2 per step), so g <= 0 as the paper
- *             requires and every factor of the 64-token chunk form stays
- *             inside float range
+ *   G       : [B, H, T, d_k] float32 log-decays, each in [-2, 0]
+ *             (precondition, not checked: it would need a device read).
+ *             g <= 0 is the paper's decay; the floor, a decay factor of at
+ *             least e^-2 per step, keeps every factor of the 64-token chunk
+ *             form inside float range.  Values outside the domain are
+ *             clamped into it, so the result is then not the read of the
+ *             given decays
  *   beta    : [H, d_v] float32, > 0
  *   out     : [B, H, T, d_v] float32
  *   d_k, d_v: 64 (both);  chunk: 64 (the decay factors of a chunk stay

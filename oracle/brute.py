@@ -89,9 +89,9 @@ def brute_fem_linear(q, k, v, beta, dps=50):
     return brute_read(brute_linear_prior(q, k, dps), v, beta, dps)
 
 
-def brute_gla_prior(q, k, g, eps, base, gmin, dps=50):
+def brute_gla_prior(q, k, g, eps, base, dps=50):
     """GLA prior rows term by term: features ReLU(RoPE(x)) + eps, decay
-    exp(sum_{tau=i+1}^{t} clip(g_tau)) per key channel (Appendix "Gated Linear
+    exp(sum_{tau=i+1}^{t} g_tau) per key channel (Appendix "Gated Linear
     Attention (GLA) Prior", eq. gla-score-appendix)."""
     with mpmath.workdps(dps):
         T = len(q)
@@ -107,8 +107,7 @@ def brute_gla_prior(q, k, g, eps, base, gmin, dps=50):
                 out[2 * m + 1] = a * s + b * c
             return [max(u, 0) + mpmath.mpf(eps) for u in out]
 
-        gg = [[min(max(mpmath.mpf(g[t][c]), mpmath.mpf(gmin)), 0) for c in range(d)]
-              for t in range(T)]
+        gg = [[mpmath.mpf(g[t][c]) for c in range(d)] for t in range(T)]
         rows = []
         for t in range(T):
             fq = feat(q[t], t)
@@ -125,5 +124,5 @@ def brute_gla_prior(q, k, g, eps, base, gmin, dps=50):
         return rows
 
 
-def brute_fem_gla(q, k, v, g, beta, eps, base, gmin, dps=50):
-    return brute_read(brute_gla_prior(q, k, g, eps, base, gmin, dps), v, beta, dps)
+def brute_fem_gla(q, k, v, g, beta, eps, base, dps=50):
+    return brute_read(brute_gla_prior(q, k, g, eps, base, dps), v, beta, dps)

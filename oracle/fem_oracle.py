@@ -355,7 +355,6 @@ def fem_softmax_ltl(q, k, v, beta_max, lam, gate=None, rows=None,
 # ---------------------------------------------------------------------------
 GLA_EPS = 1e-6          # the small positive constant of the feature map
 GLA_ROPE_BASE = 10000.0  # RoPE frequency base
-GLA_G_MIN = -2.0        # log-decays are clipped to [GLA_G_MIN, 0]
 
 
 def rope(x: np.ndarray, pos: np.ndarray, base: float = GLA_ROPE_BASE) -> np.ndarray:
@@ -376,22 +375,19 @@ def gla_features(x: np.ndarray, pos: np.ndarray) -> np.ndarray:
     return np.maximum(rope(x, pos), 0.0) + GLA_EPS
 
 
-def gla_log_decay(g: np.ndarray) -> np.ndarray:
-    """The learned log-decays g <= 0, clipped to [GLA_G_MIN, 0] (the envelope
-    is clipped in practice)."""
-    return np.clip(g, GLA_G_MIN, 0.0)
-
-
 def gla_prior_rows(q: np.ndarray, k: np.ndarray, g: np.ndarray, rows: np.ndarray) -> np.ndarray:
     """Causal GLA prior p_t(i) = s_t(i) / Z_t (eq. gla-score-appendix) with a
     per-key-channel decay: s_t(i) = sum_c q~_{t,c} k~_{i,c} exp(sum_{tau=i+1}^{t}
     g_{tau,c}) for i <= t, i.e. <D_t q~_t, D_i^{-1} k~_i> with the envelope D
-    acting element-wise.  q, k, g: [T, d_k]; returns [len(rows), max(rows)+1].
+    acting element-wise.  The log-decays g are used as given (the paper's
+    decays have g <= 0; it clips the envelope in practice without saying
+    where, so the definition itself carries no clip).  q, k, g: [T, d_k];
+    returns [len(rows), max(rows)+1].
     """
     n = int(rows.max()) + 1
     fq = gla_features(q[rows], rows)
     fk = gla_features(k[:n], np.arange(n))
-    G = np.cumsum(gla_log_decay(g[:n]), axis=0)  # G_t = sum_{tau <= t} g_tau
+    G = np.cumsum(g[:n], axis=0)  # G_t = sum_{tau <= t} g_tau, the decays as given
     s = np.zeros((len(rows), n))
     step = max(1, (1 << 21) // (n * k.shape[1]))
     for a in range(0, len(rows), step):
@@ -441,7 +437,7 @@ def fem_gla_recurrent(q, k, v, g, beta) -> np.ndarray:
             e = np.exp(x - c[None, :])
             fq = gla_features(q[b, h], pos)
             fk = gla_features(k[b, h], pos)
-            a = np.exp(gla_log_decay(g[b, h]))
+            a = np.exp(g[b, h])
             S = np.zeros((dk, dv))
             z = np.zeros(dk)
             for t in range(T):

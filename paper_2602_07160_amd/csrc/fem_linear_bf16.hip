@@ -31,7 +31,7 @@
 // GLA prior (Appendix "Gated Linear Attention (GLA) Prior"): the same scan
 // with features q~ = ReLU(RoPE(q)) + eps, k~ likewise, and a decay envelope
 // per key channel c: p_t(i) propto sum_c q~_tc k~_ic exp(G_tc - G_ic), G the
-// running sum of the log-decays g (clipped to [-2, 0]).  Inside a chunk, with
+// running sum of the log-decays g, which must lie in [-2, 0].  Inside a chunk, with
 // B the chunk-local running sum and R = B at its middle row:
 //   intra:  A_ti = sum_c (q~_tc e^{B_tc - R_c}) (k~_ic e^{R_c - B_ic})
 //   inter:  num_t += sum_c (q~_tc e^{B_tc - R_c}) (e^{R_c} S_c)
@@ -65,7 +65,12 @@ template <int PRIOR>
 constexpr int state_floats() { return PRIOR == kGla ? STATE + DK : STATE; }
 
 constexpr float kGlaEps = 1e-6f;   // the feature map's positive constant
-constexpr float kGlaGMin = -2.f;   // log-decays are clipped to [kGlaGMin, 0]
+// The log-decays' domain is [kGlaGMin, 0] (a precondition of the entry
+// point: the paper's decays have g <= 0, and the floor keeps every factor of
+// the 64-token chunk form within e^+-64).  Values outside it are clamped into
+// it, which only keeps the arithmetic finite: the read is then not the
+// paper's for those inputs.
+constexpr float kGlaGMin = -2.f;
 
 // RoPE frequencies in revolutions per position, f_m = 10000^(-2m/DK) / (2 pi),
 // as float hi + lo pairs of the double value (m = 0 .. DK/2 - 1), so that the

@@ -51,16 +51,22 @@ def test_gla_shapes(fem, T):
     check(run(fem, q, k, v, g, b), ref(q, k, v, g, b), f"gla T{T}")
 
 
-@pytest.mark.parametrize("regime", ["none", "strong", "clipped"])
+@pytest.mark.parametrize("regime", ["none", "strong", "floor"])
 def test_gla_decay_regimes(fem, regime):
+    """Decays across the kernel's domain g in [-2, 0]: none, strong, and
+    uniform over the whole domain with a quarter of the entries exactly at
+    its floor -2 (the oracle applies the decays as given)."""
     say(f"gla decay regime {regime}: B1 H2 T900 d64, seed 12000")
     q, k, v, b = inputs.draw(12000, 1, 2, 900, 64, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
     if regime == "none":
         g = torch.zeros(1, 2, 900, 64)
     elif regime == "strong":
-        g = inputs.draw_gla_decay(12001, 1, 2, 900, 64, scale=1.0)
-    else:  # values outside [-2, 0] are clipped by the kernel and the oracle alike
-        g = 3.0 * torch.randn(1, 2, 900, 64, generator=torch.Generator().manual_seed(12002))
+        g = inputs.draw_gla_decay(12001, 1, 2, 900, 64, scale=1.0 / 3.0).clamp_(min=-2.0)
+    else:
+        gen = torch.Generator().manual_seed(12002)
+        g = -2.0 * torch.rand(1, 2, 900, 64, generator=gen)
+        g[torch.rand(1, 2, 900, 64, generator=gen) < 0.25] = -2.0
+    assert float(g.min()) >= -2.0 and float(g.max()) <= 0.0
     check(run(fem, q, k, v, g, b), ref(q, k, v, g, b), f"gla {regime}")
 
 
