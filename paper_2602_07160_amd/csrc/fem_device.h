@@ -85,8 +85,15 @@ __device__ __forceinline__ void dma16(const void* src, void* dst) {
       : "memory");
 }
 // The same load with a wave-uniform 64-bit base in SGPRs and a 32-bit lane
-// offset: one VGPR per load instead of a 64-bit address pair.
-__device__ __forceinline__ void dma16s(const void* base, unsigned off, void* dst) {
+// offset: one VGPR per load instead of a 64-bit address pair.  The base is
+// the same in every lane; it is read from the first lane so that it sits in
+// SGPRs wherever the compiler cannot prove it uniform.
+__device__ __forceinline__ void dma16s(const void* base_any, unsigned off, void* dst) {
+  // (the builtin returns int: each half is widened as unsigned, never sign-extended)
+  const uint64_t b = reinterpret_cast<uint64_t>(base_any);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((unsigned)(b >> 32));
+  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((unsigned)b);
+  const uint64_t base = ((uint64_t)hi << 32) | (uint64_t)lo;
   unsigned saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"

@@ -81,6 +81,10 @@ constexpr float kBias = 64.f;        // E = 2^(x - c + kBias) <= 2^(kBias + kCol
 constexpr float kColLag = 16.f;      // column shift raised only past this lag
 constexpr float kRowLag = 8.f;       // row max raised only past this lag (P <= 2^8)
 constexpr float kUnderflow = 0x1p-64f;
+// Channels with beta at or above this take E rounded to bf16 (relative error
+// at most 2^-8, which moves F by at most 2^-8 / beta <= 2^-7) and no lo
+// product; smaller beta amplifies that rounding, so those keep hi + lo.
+constexpr float kLoBeta = 0.5f;
 
 // What a launch computes (see the header comment).
 constexpr int kFem = 0;    // F at beta
@@ -124,7 +128,8 @@ struct Cfg {
   static constexpr int OFF_EH = OFF_V + 2 * VB;   // 2 buffers
   static constexpr int OFF_EL = OFF_EH + 2 * EB;  // 2 buffers
   static constexpr int OFF_F = OFF_EL + 2 * EB;   // floats
-  static constexpr int NF = DV /*bl*/ + DV /*inv*/ + 2 * DV /*c*/ + 2 * DV /*g*/ + 64 /*sink*/;
+  static constexpr int NF =
+      DV /*bl*/ + DV /*inv*/ + 2 * DV /*c*/ + 2 * DV /*g*/ + 64 /*sink*/ + DV /*channel order*/;
   static constexpr int OFF_R = OFF_F + NF * 4;    // column-update flags [2][NW]
   static constexpr size_t LDS = OFF_R + 2 * NW * 4;
   static_assert(CPW * NW == DV && G * CPW == 64 && RPL * G == 16, "tilt mapping");
@@ -201,6 +206,8 @@ struct Smem {
   __device__ float* g(int b) const { return bl() + 4 * DV + b * DV; }
   // Write-only slots for lanes whose store would otherwise need a branch.
   __device__ float* sink() const { return bl() + 6 * DV; }
+  // Input channel held by accumulator column j (channel split, see kLoBeta).
+  __device__ int* chan() const { return reinterpret_cast<int*>(bl() + 6 * DV + 64); }
   __device__ int* upd(int b) const { return reinterpret_cast<int*>(base + C::OFF_R) + b * C::NW; }
 };
 
@@ -226,15 +233,17 @@ __device__ __forceinline__ float max_xor(float x, int o) {
 
 // Tilt of tile tt for this wave's CPW channels, as separately placeable steps
 // (the phases interleave them with MFMAs):
-//   read    : this lane's V values (channel jj, 4-key runs g + G*u), beta and
-//             the previous column shift, all from LDS;
+//   read    : this lane's V values (accumulator column jj, which holds input
+//             channel vcol; 4-key runs g + G*u), beta and the previous column
+//             shift, all from LDS;
 //   colmax  : column max over the tile (a tree in-lane, then across the G
 //             lanes of a channel);
 //   shift   : lazily raised running shift c_j; stores c, the rescale factor
 //             g = 2^(c_old - c_new) and the wave's "some c rose" flag;
 //   value(u, b), store(u) : E = 2^(x - c + bias) of key 4(g + G u) + b split
-//             into bf16 hi (truncated) and lo (the rounded remainder), and the
-//             store of run u into the E^T buffers.
+//             into bf16 hi (truncated) and lo (the rounded remainder), or for
+//             a column without lo product E rounded to bf16, and the store of
+//             run u into the E^T buffers.
 // Keys at or past T (last tile only) hold copies of row T-1 (see load_tile):
 // they leave the column max unchanged and give finite E, which meet P = 0
 // (the causal mask), so the tilt treats every tile as full.
@@ -248,11 +257,11 @@ struct Tilt {
   float bl, cold, cnew, sh;
   unsigned char* eh;
 
-  __device__ __forceinline__ void read(const Smem<C>& sm, int tt, int wave, int lane) {
+  __device__ __forceinline__ void read(const Smem<C>& sm, int tt, int wave, int lane, int vcol) {
     const int jj = lane % C::CPW, g = lane / C::CPW;
     const int j = wave * C::CPW + jj;
     const unsigned char* sv =
-        sm.base + pin(C::OFF_V + (tt & 1) * C::VB + j * 2 + 4 * g * C::VROW * 2);
+        sm.base + pin(C::OFF_V + (tt & 1) * C::VB + vcol * 2 + 4 * g * C::VROW * 2);
 #pragma unroll
     for (int u = 0; u < C::RPL; ++u) {
 #pragma unroll
@@ -307,11 +316,18 @@ struct Tilt {
     if (MODE != kMean) e[u][b] = exp2_hw(e[u][b]);
   }
 
-  __device__ __forceinline__ void store(int u) {
+  // with_lo: this wave's columns take the lo product (wave-uniform)
+  __device__ __forceinline__ void store(int u, bool with_lo) {
     static_assert(e_pos_splits(C::G), "tilt write positions");
     if (MODE == kMean) {  // bf16 values: the truncation is exact
       const u32x2 v2 = {pack_hi16(e[u][0], e[u][1]), pack_hi16(e[u][2], e[u][3])};
       *reinterpret_cast<u32x2*>(eh + e_pos(4 * C::G * u) * 2) = v2;
+      return;
+    }
+    if (!with_lo) {
+      const bf16x2 h01 = to_bf16x2(e[u][0], e[u][1]), h23 = to_bf16x2(e[u][2], e[u][3]);
+      const u32x2 h2 = {__builtin_bit_cast(unsigned, h01), __builtin_bit_cast(unsigned, h23)};
+      *reinterpret_cast<u32x2*>(eh + e_pos(4 * C::G * u) * 2) = h2;
       return;
     }
     float lo[4];
@@ -430,7 +446,8 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 
 // Phase 1 of an iteration, interleaved by hand with the tilt of tile k (QKT):
 // on the matrix pipe, S^T = K Q^T of tile k into s (QKT), then the row-sum
-// products and k-step 0 of PV(k-1) (PVA).  Slot st issues MFMA st, the LDS
+// products and k-step 0 of PV(k-1) (PVA; the lo product for the first NLO
+// column blocks only).  Slot st issues MFMA st, the LDS
 // read of the operand fragment RING steps ahead, one stage of the tilt and
 // whatever side(st) adds (the next tile's direct loads); a scheduling
 // barrier after every slot keeps this order.  The tilt's stages sit one
@@ -443,15 +460,15 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // m = 4r for the k-blocks with b%2 == r%2 sums query (l%16) + 16*(r%2) into
 // output row 4r, which the 16x16 output layout places in register 0 of lane
 // 16r + l%16.  Hence lacc[0] of every lane is the row sum of its query l%32.
-template <class C, bool PVA, bool QKT, class Side>
+template <class C, int NLO, bool PVA, bool QKT, class Side>
 __device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, int wave, int lane,
-                                       int kofs, int eofs, const bf16x8 (&qf)[C::NKS],
+                                       int kofs, int eofs, int vcol, const bf16x8 (&qf)[C::NKS],
                                        f32x16 (&s)[2], f32x16 (&acc)[C::NCB], f32x4& lacc,
                                        const bf16x8 (&pp)[4], const bf16x8& lsel, Side&& side) {
   constexpr int MODE = C::MODE;
+  static_assert(NLO >= 0 && NLO <= C::NCB && (MODE != kMean || NLO == 0), "lo blocks");
   constexpr int NQ = QKT ? 2 * C::NKS : 0;    // QK MFMAs
   constexpr int NL = PVA ? 4 : 0;             // row-sum MFMAs
-  constexpr int NLO = MODE == kMean ? 0 : C::NCB;  // lo blocks
   constexpr int NE = PVA ? C::NCB + NLO : 0;  // PV k-step 0: hi blocks, then lo blocks
   constexpr int NF = NQ + NE;                 // LDS operand fragments, in issue order
   constexpr int NS = NQ + NL + NE;
@@ -465,7 +482,8 @@ __device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, in
   constexpr int V0 = CM + 2;
   constexpr int NVS = NV > 0 ? V0 + NV + 2 : 0;
   constexpr int NSLOT = NS > NVS ? NS : NVS;
-  if (QKT) tl.read(sm, k, wave, lane);
+  if (QKT) tl.read(sm, k, wave, lane, vcol);
+  const bool lo = wave * C::CPW < 32 * NLO;  // this wave's columns take the lo product
   const unsigned char* kt = sm.base + pin(C::OFF_K + (k & 1) * C::KB + kofs);
   const unsigned char* eb = sm.base + (PVA ? pin(C::OFF_EH + ((k - 1) & 1) * C::EB + eofs) : 0u);
   auto frag = [&](int f) -> bf16x8 {
@@ -508,23 +526,24 @@ __device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, in
       const int xa = st - V0, xe = xa - 1, xs = xa - 5;  // values at each stage
       if (xa >= 0 && xa < NV) tl.value_arg(xa >> 2, xa & 3);
       if (xe >= 0 && xe < NV) tl.value_exp(xe >> 2, xe & 3);
-      if (xs >= 0 && (xs & 3) == 0 && (xs >> 2) < C::RPL) tl.store(xs >> 2);
+      if (xs >= 0 && (xs & 3) == 0 && (xs >> 2) < C::RPL) tl.store(xs >> 2, lo);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// Phase 2 of an iteration: k-steps 1..3 of PV(k-1) (PVB), reading P(k-1)
+// Phase 2 of an iteration: k-steps 1..3 of PV(k-1) (PVB; hi blocks, then the
+// NLO lo blocks of each k-step), reading P(k-1)
 // from pp, interleaved by hand with the softmax of this tile (SM; MASK on the
 // wave's diagonal tile and the tiles after it), which writes P(k) into the
 // other buffer pn.  The softmax's stages sit one slot apart as in phase 1.
-template <class C, bool PVB, bool SM, bool MASK>
+template <class C, int NLO, bool PVB, bool SM, bool MASK>
 __device__ __forceinline__ void phase2(const Smem<C>& sm, f32x16 (&acc)[C::NCB],
                                        const bf16x8 (&pp)[4], bf16x8 (&pn)[4], f32x16 (&sc)[2],
                                        float& m, float& apend, int j, int eofs, int k0, int tq,
                                        int hl, float scale2) {
-  constexpr int MODE = C::MODE;
-  constexpr int NPK = MODE == kMean ? C::NCB : 2 * C::NCB;  // fragments per k-step
+  static_assert(NLO >= 0 && NLO <= C::NCB && (C::MODE != kMean || NLO == 0), "lo blocks");
+  constexpr int NPK = C::NCB + NLO;                   // fragments per k-step
   constexpr int NF = PVB ? 3 * NPK : 0;               // k-steps 1..3
   constexpr int RING = 4;
   // Softmax stages: the max tree in slots 0..2, the row-max update in 3, then
@@ -570,13 +589,36 @@ __device__ __forceinline__ void phase2(const Smem<C>& sm, f32x16 (&acc)[C::NCB],
   }
 }
 
+// Number of channels of one head whose beta needs the lo product (the same
+// value in every lane).
 template <class C>
-__global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
+__device__ __forceinline__ int lo_channels(const float* hbeta, int lane) {
+  int n = 0;
+#pragma unroll
+  for (int c0 = 0; c0 < C::DV; c0 += 64) {
+    const int j = c0 + lane;
+    n += __popcll(__ballot(j < C::DV && !(hbeta[j] >= kLoBeta)));
+  }
+  return n;
+}
+
+// Number of set bits of m below this lane.
+__device__ __forceinline__ int bits_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+
+// The read of one workgroup (a block of BQ query rows of one head) whose
+// first NLO accumulator column blocks take the lo product.  With 0 < NLO <
+// NCB the columns hold the head's channels reordered: the nlo channels with
+// beta below kLoBeta first, then the others, each group in input order.
+template <class C, int NLO>
+__device__ __forceinline__ void read_body(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ beta, const float* lam, const float* gate, float* out,
-    float* __restrict__ lse, int H, int T, int nqb, int nbh) {
+    float* __restrict__ lse, int H, int T, int nqb, int nbh, unsigned char* smem, int nneed) {
   constexpr int MODE = C::MODE;
-  __shared__ __align__(16) unsigned char smem[C::LDS];
+  constexpr bool SPLIT = NLO > 0 && NLO < C::NCB;  // columns hold reordered channels
   const Smem<C> sm{smem};
 
   const int tid = threadIdx.x;
@@ -598,10 +640,32 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
   float* Oh = out + base;
   bf16* Ob = reinterpret_cast<bf16*>(out) + base;
 
-  for (int j = tid; j < C::DV; j += C::NT) {
-    const float bl = beta[h * C::DV + j] * kLog2e;
-    sm.bl()[j] = bl;
-    sm.inv()[j] = 1.f / bl;
+  if (!SPLIT) {
+    for (int j = tid; j < C::DV; j += C::NT) {
+      const float bl = beta[h * C::DV + j] * kLog2e;
+      sm.bl()[j] = bl;
+      sm.inv()[j] = 1.f / bl;
+    }
+  } else if (wave == 0) {
+    // column of channel j: its rank among the channels of its group, after
+    // the nlo channels that need the lo product if it does not
+    int below_lo = 0, below_hi = 0;
+#pragma unroll
+    for (int c0 = 0; c0 < C::DV; c0 += 64) {
+      const int j = c0 + lane;
+      const bool valid = j < C::DV;
+      const float b = valid ? beta[h * C::DV + j] : 1.f;
+      const bool need = valid && !(b >= kLoBeta);
+      const uint64_t mlo = __ballot(need), mhi = __ballot(valid && !need);
+      const int col = need ? below_lo + bits_below(mlo) : nneed + below_hi + bits_below(mhi);
+      if (valid) {
+        sm.chan()[col] = j;
+        sm.bl()[col] = b * kLog2e;
+        sm.inv()[col] = 1.f / (b * kLog2e);
+      }
+      below_lo += __popcll(mlo);
+      below_hi += __popcll(mhi);
+    }
   }
 
   const int wq0 = q0 + wave * 32;  // first query row of this wave
@@ -635,6 +699,8 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
   }
   wait_vmem();
   __syncthreads();
+  // input channel of this lane's tilt column
+  const int vcol = SPLIT ? sm.chan()[wave * C::CPW + lane % C::CPW] : wave * C::CPW + lane % C::CPW;
 
   f32x16 acc[C::NCB];
 #pragma unroll
@@ -718,12 +784,13 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
     for (int w = 1; w < C::NW / 4; ++w) any4 |= uf[w];
     return any4;
   };
-#define FEM_PHASE1(PVA, QKT, PPREV, SIDE) \
-  phase1<C, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, qf, sacc, acc, lacc, PPREV, lsel, SIDE)
+#define FEM_PHASE1(PVA, QKT, PPREV, SIDE)                                                   \
+  phase1<C, NLO, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, vcol, qf, sacc, acc, lacc, PPREV, \
+                           lsel, SIDE)
   const auto none = [](auto...) __attribute__((always_inline)) {};
 #define FEM_PHASE2(PVB, SM, MK, PPREV, PNEXT)                                                    \
-  phase2<C, PVB, SM, MK>(sm, acc, PPREV, PNEXT, sacc, m, apend, k - 1, eofs, k * C::BK, tm, hl, \
-                         scale2)
+  phase2<C, NLO, PVB, SM, MK>(sm, acc, PPREV, PNEXT, sacc, m, apend, k - 1, eofs, k * C::BK, tm, \
+                              hl, scale2)
 
   // Every wave runs the same steps on every tile: past its diagonal tile the
   // softmax masks every key, so P = 0 and PV adds nothing, while the
@@ -779,6 +846,15 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
 #undef FEM_PHASE1
 #undef FEM_PHASE2
 
+  // With reordered channels the outputs go through LDS (the tile buffers are
+  // free once every wave is done with the last tile) so that the rows reach
+  // memory in channel order with whole-row stores.
+  constexpr bool STAGE = SPLIT;
+  constexpr int SROW = C::DV + 4;  // staged row stride (floats)
+  static_assert(!STAGE || C::NW * 32 * SROW * 4 <= C::OFF_F, "staging must not reach the tables");
+  if (STAGE) __syncthreads();
+  float* stage = reinterpret_cast<float*>(smem) + wave * 32 * SROW;
+
   if (!wave_live) return;
 
   if (MODE == kMean) {  // ---- mu = acc / l
@@ -825,6 +901,17 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
         o[e] = ((float)(ea - el - (int)kBias) + (fa - fl) + cw[ch0 + e]) * inv[ch0 + e];
         if (!(a >= kUnderflow) && tq < T) flags |= 1ull << (cb * 16 + g * 4 + e);
       }
+      if (STAGE) {  // into the staged row at the channel's own column
+        const i32x4 oc = SPLIT ? *reinterpret_cast<const i32x4*>(sm.chan() + ch0)
+                               : i32x4{ch0, ch0 + 1, ch0 + 2, ch0 + 3};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          // the gated mix keeps mu where F underflowed (NaN marks those)
+          const bool flagged = (flags >> (cb * 16 + g * 4 + e)) & 1ull;
+          stage[n * SROW + oc[e]] = MODE == kGated && flagged ? __builtin_nanf("") : o[e];
+        }
+        continue;
+      }
       if (tq >= T) continue;
       const size_t at = (size_t)tq * C::DV + ch0;
       if (MODE == kGated) {
@@ -849,6 +936,35 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
     }
   }
 
+  if (STAGE) {
+    // whole rows: lane l stores channels 4 (l % LPR) .. +3 of row l / LPR of
+    // each group of RPI rows
+    constexpr int LPR = C::DV / 4, RPI = 64 / LPR;
+    const int c4 = (lane % LPR) * 4;
+#pragma unroll
+    for (int r0 = 0; r0 < 32; r0 += RPI) {
+      const int r = r0 + lane / LPR, t = wq0 + r;
+      f32x4 o = *reinterpret_cast<const f32x4*>(stage + r * SROW + c4);
+      if (t >= T) continue;
+      const size_t at = (size_t)t * C::DV + c4;
+      if (MODE == kGated) {
+        const f32x4 mu = *reinterpret_cast<const f32x4*>(Oh + at);
+        const f32x4 lm = *reinterpret_cast<const f32x4*>(Lh + at);
+        const f32x4 gg = Gh ? *reinterpret_cast<const f32x4*>(Gh + at) : f32x4{1.f, 1.f, 1.f, 1.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          o[e] = o[e] != o[e] ? mu[e] : gg[e] * fmaf(lm[e], o[e] - mu[e], mu[e]);
+      }
+      if (C::OBF16) {
+        const bf16x2 o01 = to_bf16x2(o[0], o[1]), o23 = to_bf16x2(o[2], o[3]);
+        const u32x2 ob = {__builtin_bit_cast(unsigned, o01), __builtin_bit_cast(unsigned, o23)};
+        *reinterpret_cast<u32x2*>(Ob + at) = ob;
+      } else {
+        *reinterpret_cast<f32x4*>(Oh + at) = o;
+      }
+    }
+  }
+
   // ---- rare path: exact recompute of accumulators that underflowed
   while (true) {
     const uint64_t who = __ballot(flags != 0);
@@ -860,8 +976,9 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
     const int e = __builtin_ctzll(fl64);
     const int t = __builtin_amdgcn_readlane(tq, src);
     const int cb = e >> 4, i = e & 15;
-    const int ch = cb * 32 + (i >> 2) * 8 + (src >> 5) * 4 + (i & 3);
-    const float o = exact_read<C>(Qh, Kh, Vh, t, C::CAUSAL ? t + 1 : T, ch, scale2, sm.bl()[ch]);
+    const int col = cb * 32 + (i >> 2) * 8 + (src >> 5) * 4 + (i & 3);
+    const int ch = SPLIT ? sm.chan()[col] : col;  // input channel
+    const float o = exact_read<C>(Qh, Kh, Vh, t, C::CAUSAL ? t + 1 : T, ch, scale2, sm.bl()[col]);
     if (lane == src) {
       flags &= ~(1ull << e);
       const size_t at = (size_t)t * C::DV + ch;
@@ -874,6 +991,33 @@ __global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
         Oh[at] = o;
       }
     }
+  }
+}
+
+// Dispatch on the number of column blocks that take the lo product.
+template <class C, int N, class... A>
+__device__ __forceinline__ void read_nlo(int nlo, A... a) {
+  if constexpr (N == C::NCB) {
+    read_body<C, N>(a...);
+  } else {
+    if (nlo == N) read_body<C, N>(a...);
+    else read_nlo<C, N + 1>(nlo, a...);
+  }
+}
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void softmax_bf16_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
+    const float* __restrict__ beta, const float* lam, const float* gate, float* out,
+    float* __restrict__ lse, int H, int T, int nqb, int nbh) {
+  __shared__ __align__(16) unsigned char smem[C::LDS];
+  if constexpr (C::MODE == kMean) {
+    read_body<C, 0>(Q, K, V, beta, lam, gate, out, lse, H, T, nqb, nbh, smem, 0);
+  } else {
+    const int h = (int)(blockIdx.x % (unsigned)nbh) % H;
+    const int nneed = lo_channels<C>(beta + h * C::DV, threadIdx.x & 63);
+    read_nlo<C, 0>((nneed + 31) >> 5, Q, K, V, beta, lam, gate, out, lse, H, T, nqb, nbh, smem,
+                   nneed);
   }
 }
 

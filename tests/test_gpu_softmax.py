@@ -145,6 +145,96 @@ def test_bf16_beta_extremes(fem, beta):
     check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, f"beta={beta}")
 
 
+# --------------------------------------------------------------------------
+# channel split: a channel whose beta is at or above 0.5 takes E rounded to
+# bf16 without the lo product (|dF| <= 2^-8 / beta); each workgroup orders its
+# head's channels so that the small-beta ones fill the first column blocks.
+# One head per pattern: every number of lo blocks, block boundaries (32 and
+# 33 small channels), interleaved and reversed orders, beta exactly 0.5.
+# --------------------------------------------------------------------------
+LO_BETA = 0.5
+SPLIT_PATTERNS = ["interleaved", "exactly32", "exactly33", "one_last", "none", "all", "reversed"]
+
+
+def split_beta(d, seed):
+    """[H, d] beta, one pattern per head; small = log-U[0.05, 0.1] (where a
+    missing lo product would show: 2^-8 / 0.05 = 0.078), large = log-U[0.5, 8]
+    with one channel at exactly 0.5."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for pat in SPLIT_PATTERNS:
+        small = np.zeros(d, bool)
+        if pat == "interleaved":
+            small[::2] = True
+        elif pat in ("exactly32", "exactly33"):
+            small[rng.choice(d, min(d, 32 if pat == "exactly32" else 33), replace=False)] = True
+        elif pat == "one_last":
+            small[-1] = True
+        elif pat == "all":
+            small[:] = True
+        elif pat == "reversed":
+            small[d // 3:] = True
+        lo = np.exp(rng.uniform(np.log(0.05), np.log(0.1), d))
+        hi = np.exp(rng.uniform(np.log(LO_BETA), np.log(8.0), d))
+        big = np.flatnonzero(~small)
+        if big.size:
+            hi[big[0]] = LO_BETA
+        out.append(np.where(small, lo, hi))
+    return torch.from_numpy(np.array(out, dtype=np.float32))
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_bf16_channel_split(fem, d):
+    say(f"channel split patterns {SPLIT_PATTERNS}: B1 H{len(SPLIT_PATTERNS)} T333 d{d}, seed {3100 + d}")
+    H = len(SPLIT_PATTERNS)
+    q, k, v, _ = inputs.draw(3100 + d, 1, H, 333, d, dtype="bf16")
+    b = split_beta(d, 3200 + d)
+    got = run(fem, q, k, v, b)
+    want = ref(q, k, v, b)
+    check(got, want, TOL_BF16, f"split d{d}")
+    err = np.abs(got - want).max(axis=(0, 2))        # [H, d]
+    bn = b.double().numpy()
+    small = bn < LO_BETA
+    # small beta: the lo product is there (a rounded E alone would be off by
+    # up to 2^-8 / beta, several times this)
+    assert err[small].max() <= 1e-2, f"small-beta channel error {err[small].max()}"
+    # beta >= 0.5: within the rounding bound of E plus the other rounding
+    bound = 2.0 ** -8 / bn + 5e-3
+    worst = (err - bound)[~small].max()
+    say(f"split d{d}: worst small-beta err {err[small].max():.3e}, worst slack vs 2^-8/beta bound {worst:.3e}")
+    assert worst <= 0, "a channel with beta >= 0.5 exceeds its rounding bound"
+
+
+def test_bf16_channel_split_variants(fem):
+    """The reordered columns with the encoder read, bf16 output, d_v < d_qk and
+    the gated read."""
+    say("channel split variants: encoder / bf16 out / d_qk128 d_v64 / gated, B1 H7 T200, seed 3300")
+    H = len(SPLIT_PATTERNS)
+    dev = torch.device("cuda:0")
+    q, k, v, _ = inputs.draw(3300, 1, H, 200, 128, dtype="bf16")
+    b = split_beta(128, 3301)
+    qd, kd, vd, bd = q.to(dev), k.to(dev), v.to(dev), b.to(dev)
+    enc = fem.fem_softmax_fwd_ex(qd, kd, vd, bd, causal=False)
+    o16 = fem.fem_softmax_fwd_ex(qd, kd, vd, bd, out_dtype=torch.bfloat16)
+    o32 = fem.fem_softmax_fwd(qd, kd, vd, bd)
+    v64, b64 = v[..., :64].contiguous(), b[:, :64].contiguous()
+    half = fem.fem_softmax_fwd_ex(qd, kd, v64.to(dev), b64.to(dev))
+    torch.cuda.synchronize()
+    check(enc.cpu().double().numpy(),
+          oracle.fem_softmax_encoder(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                     b.double().numpy()), TOL_BF16, "split encoder")
+    assert torch.equal(o16.cpu(), o32.cpu().to(torch.bfloat16)), "bf16 output != RNE(fp32 output)"
+    check(half.cpu().double().numpy(), ref(q, k, v64, b64), TOL_BF16, "split d_qk128 d_v64")
+    lam, g = inputs.draw_gates(3302, 1, H, 200, 128)
+    og = fem.fem_softmax_gated_fwd(qd, kd, vd, bd, lam.to(dev), g.to(dev))
+    torch.cuda.synchronize()
+    want = oracle.fem_softmax_ltl(q.double().numpy(), k.double().numpy(), v.double().numpy(),
+                                  b.double().numpy(), lam.double().numpy(), g.double().numpy())
+    errg = (np.abs(og.cpu().double().numpy() - want) / np.maximum(1.0, g.double().numpy())).max()
+    say(f"split gated: max scaled err {errg:.3e}")
+    assert errg <= TOL_BF16
+
+
 def test_bf16_peaked_scores(fem):
     say("bf16 peaked scores q = 8 k_t: B1 H2 T384 d64")
     q, k, v, b = inputs.draw(3001, 1, 2, 384, 64, dtype="bf16")
