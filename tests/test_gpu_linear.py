@@ -2,6 +2,7 @@
 the float64 oracle.  Tolerance: max abs error <= 2e-2 (bf16 inputs)."""
 
 import sys
+import time
 
 import numpy as np
 import pytest
@@ -44,18 +45,22 @@ def test_workload5_full_size_every_row(fem):
     q, k, v, b = inputs.make_inputs(5)
     got = run(fem, q, k, v, b)
     worst = 0.0
+    t_oracle = 0.0
     for bb in range(4):
         for hh in range(16):
+            t0 = time.perf_counter()
             want = oracle.fem_linear(q[bb:bb + 1, hh:hh + 1].double().numpy(),
                                      k[bb:bb + 1, hh:hh + 1].double().numpy(),
                                      v[bb:bb + 1, hh:hh + 1].double().numpy(),
                                      b[hh:hh + 1].double().numpy())[0, 0]
+            t_oracle += time.perf_counter() - t0
             assert np.isfinite(got[bb, hh]).all()
             err = float(np.abs(got[bb, hh] - want).max())
             worst = max(worst, err)
             assert err <= TOL, f"workload 5 b{bb} h{hh}: {err} > {TOL}"
         say(f"workload 5: batch {bb} done, worst max abs err so far {worst:.3e}")
-    say(f"workload 5: all 64 heads, every row: max abs err {worst:.3e} (tol {TOL})")
+    say(f"workload 5: all 64 heads, every row: max abs err {worst:.3e} (tol {TOL}); "
+        f"oracle {t_oracle:.1f} s")
 
 
 def test_workload5_reduced_full(fem):

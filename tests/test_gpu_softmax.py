@@ -6,6 +6,7 @@ the GPU.
 """
 
 import sys
+import time
 
 import numpy as np
 import pytest
@@ -52,13 +53,21 @@ def check(got, want, tol, what):
 def test_workload1_fp32_full(fem):
     say("workload 1: fp32 B1 H1 T128 d32, seed 43")
     q, k, v, b = inputs.make_inputs(1)
-    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_F32, "w1")
+    got = run(fem, q, k, v, b)
+    t0 = time.perf_counter()
+    want = ref(q, k, v, b)
+    say(f"w1: oracle {time.perf_counter() - t0:.2f} s")
+    check(got, want, TOL_F32, "w1")
 
 
 def test_workload2_bf16_full(fem):
     say("workload 2: bf16 B4 H8 T1024 d64, seed 44")
     q, k, v, b = inputs.make_inputs(2)
-    check(run(fem, q, k, v, b), ref(q, k, v, b), TOL_BF16, "w2")
+    got = run(fem, q, k, v, b)
+    t0 = time.perf_counter()
+    want = ref(q, k, v, b)
+    say(f"w2: oracle {time.perf_counter() - t0:.2f} s")
+    check(got, want, TOL_BF16, "w2")
 
 
 def _sampled_rows(T, rng, extra=12):
@@ -75,17 +84,21 @@ def full_compare(got, q, k, v, b, tol, what, fn=None):
     fn = oracle.fem_softmax if fn is None else fn
     B, H = got.shape[:2]
     worst = 0.0
+    t_oracle = 0.0
     for bb in range(B):
         for hh in range(H):
+            t0 = time.perf_counter()
             want = fn(q[bb:bb + 1, hh:hh + 1].double().numpy(), k[bb:bb + 1, hh:hh + 1].double().numpy(),
                       v[bb:bb + 1, hh:hh + 1].double().numpy(), b[hh:hh + 1].double().numpy())[0, 0]
+            t_oracle += time.perf_counter() - t0
             g = got[bb, hh]
             assert np.isfinite(g).all(), f"{what} b{bb} h{hh}: non-finite output"
             err = float(np.abs(g - want).max())
             worst = max(worst, err)
             assert err <= tol, f"{what} b{bb} h{hh}: max abs err {err} > {tol}"
         say(f"{what}: batch {bb} done, worst max abs err so far {worst:.3e}")
-    say(f"{what}: all {B * H} heads, every row: max abs err {worst:.3e} (tol {tol})")
+    say(f"{what}: all {B * H} heads, every row: max abs err {worst:.3e} (tol {tol}); "
+        f"oracle {t_oracle:.1f} s")
     return worst
 
 
