@@ -130,6 +130,10 @@ struct GlaSmem {
 };
 template <int PRIOR, int CH, int NSUB>
 struct ScanSmem : LinSmem<CH, NSUB> {
+  // E fragments passed between the two waves of a channel block (linear
+  // prior, one chunk per tile of at most 64 tokens): [block][k-step][hi, lo][lane]
+  static constexpr bool SPLIT_E = NSUB == 1 && CH <= 64;
+  bf16x8 ex[SPLIT_E ? (DV / 32) * (CH / 16) * 2 * 64 : 1];
   __device__ float* gb() { return nullptr; }
   __device__ float* gbq() { return nullptr; }
   __device__ float* gzr() { return nullptr; }
@@ -137,6 +141,8 @@ struct ScanSmem : LinSmem<CH, NSUB> {
 };
 template <>
 struct ScanSmem<kGla, GCH, 1> : LinSmem<GCH, 1> {
+  static constexpr bool SPLIT_E = false;  // (its LDS is at the two-workgroup limit)
+  bf16x8 ex[1];
   GlaSmem gla;
   __device__ float* gb() { return gla.b; }
   __device__ float* gbq() { return gla.bq; }
@@ -376,11 +382,13 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
   // ---- stage phi(Q), phi(K) and V, row-major; phi in fp32, rounded to bf16.
   // GLA: phi(Q) = q~ e^{B - R}, phi(K) = k~ e^{R - B}, and for the state
   // update k~ e^{B_last - B}.
+  const auto stage = [&](auto partial) __attribute__((always_inline)) {
 #pragma unroll
   for (int i = 0; i < SLOTS; ++i) {
     const int e = tid + NTH * i, r = e >> 3, c8 = (e & 7) * 8;
-    // rows past T: phi of the zeros fetched there, times 0 (no branch)
-    const float okf = t0 + r < T ? 1.f : 0.f;
+    // rows past T (a partial tile only): phi of the zeros fetched there,
+    // times 0
+    const float okf = !decltype(partial)::value || t0 + r < T ? 1.f : 0.f;
     bf16x8 pk, pq;
     if constexpr (PRIOR == kGla) {
       float kx[8], qx[8];
@@ -408,34 +416,50 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
     } else {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        pk[u] = (bf16)(phi((float)cr.k[i][u]) * okf);
-        if (OUT) pq[u] = (bf16)(phi((float)cr.q[i][u]) * okf);
+        if constexpr (decltype(partial)::value) {
+          pk[u] = (bf16)(phi((float)cr.k[i][u]) * okf);
+          if (OUT) pq[u] = (bf16)(phi((float)cr.q[i][u]) * okf);
+        } else {
+          pk[u] = (bf16)phi((float)cr.k[i][u]);
+          if (OUT) pq[u] = (bf16)phi((float)cr.q[i][u]);
+        }
       }
     }
     *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.fk) + swz_off<DK>(r, c8 >> 3)) = pk;
     *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.vs) + swz_off<DV>(r, c8 >> 3)) = cr.v[i];
     if (OUT) *reinterpret_cast<bf16x8*>(sm.fq + r * ROW + c8) = pq;
   }
+  };
+  if (t0 + CH <= T) stage(std::false_type());
+  else stage(std::true_type());
   // the next tile's loads run while this one is processed
   if (tnext < T) fetch_chunk<PRIOR, OUT, CH>(cr, Qh, Kh, Vh, Gh, tnext, T);
   lds_barrier();
 
-  // ---- tilt of the wave's channel block, in registers
+  // ---- tilt of the wave's channel block, in registers.  With one chunk per
+  // tile of at most 64 tokens the two waves of a block split the k-steps:
+  // each forms the E of its half and passes it to the other through LDS
+  // (read back after the next barrier, see take_e).
+  constexpr bool SPLIT_E = ScanSmem<PRIOR, CH, NSUB>::SPLIT_E;
+  constexpr int KSH = SPLIT_E ? NKS / 2 : NKS;  // k-steps whose E this wave forms
   bf16x8 eh[NKS], el[NKS];
   float gj;
   bool rose;
   {
+    // V^T fragments, this wave's half of the k-steps first (split: the
+    // k-step of fragment f is ksof(f))
+    const auto ksof = [&](int f) { return SPLIT_E ? (f + sub * KSH) % NKS : f; };
     bf16x8 vr[NKS];
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) vr[ks] = frag_tr<DV>(sm.vs, dvb * 32, ks * 16);
+    for (int f = 0; f < NKS; ++f) vr[f] = frag_tr<DV>(sm.vs, dvb * 32, ksof(f) * 16);
     // keys at or past T (last tile only) stay out of the max and give E = 0
     const bool full = t0 + CH <= T;
     float vmax = -INFINITY;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
+    for (int f = 0; f < NKS; ++f) {
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        if (full || t0 + e_pos(ks * 16 + hl * 8 + u) < T) vmax = fmaxf(vmax, (float)vr[ks][u]);
+        if (full || t0 + e_pos(ksof(f) * 16 + hl * 8 + u) < T) vmax = fmaxf(vmax, (float)vr[f][u]);
     }
     vmax = fmaxf(vmax, other_half(vmax));  // lanes n and n + 32 hold the same channel
     const float mx = vmax * blj;
@@ -445,25 +469,41 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
     rose = __any(cnew != cj);
     cj = cnew;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
+    for (int kk = 0; kk < KSH; ++kk) {
+      const int ks = ksof(kk);
+      const bf16x8 v = vr[kk];
 #pragma unroll
       for (int u = 0; u < 8; u += 2) {
         float ev[2];
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
           const int key = e_pos(ks * 16 + hl * 8 + u + b);
-          const float x = exp2_hw(fmaf((float)vr[ks][u + b], blj, sh));
+          const float x = exp2_hw(fmaf((float)v[u + b], blj, sh));
           ev[b] = (full || t0 + key < T) ? x : 0.f;
         }
         const bf16x2 h2 = to_bf16x2(ev[0], ev[1]);
         const bf16x2 l2 = to_bf16x2(ev[0] - (float)h2[0], ev[1] - (float)h2[1]);
-        eh[ks][u] = h2[0];
-        eh[ks][u + 1] = h2[1];
-        el[ks][u] = l2[0];
-        el[ks][u + 1] = l2[1];
+        eh[kk][u] = h2[0];
+        eh[kk][u + 1] = h2[1];
+        el[kk][u] = l2[0];
+        el[kk][u + 1] = l2[1];
+      }
+      if constexpr (SPLIT_E) {
+        sm.ex[((dvb * NKS + ks) * 2 + 0) * 64 + lane] = eh[kk];
+        sm.ex[((dvb * NKS + ks) * 2 + 1) * 64 + lane] = el[kk];
       }
     }
   }
+  // every k-step's E of the block, after a barrier that follows the stores
+  auto take_e = [&]() {
+    if constexpr (SPLIT_E) {
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        eh[ks] = sm.ex[((dvb * NKS + ks) * 2 + 0) * 64 + lane];
+        el[ks] = sm.ex[((dvb * NKS + ks) * 2 + 1) * 64 + lane];
+      }
+    }
+  };
   // tile sum of phi(k): thread (column tid & 63, quarter tid >> 6) sums CH/4
   // rows; the four partial sums meet in LDS
   {
@@ -517,6 +557,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
     }
     if (sub == 0 && hl == 0) sm.c[ch] = cj;
     lds_barrier();
+    take_e();
 
     // ---- outputs of channel block dvb for the query blocks of this wave
 #pragma unroll
@@ -541,22 +582,31 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
           const bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + qrow * ROW + ks * 16 + hl * 8);
           at = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, at, 0, 0, 0);
         }
+        // only the diagonal block needs the mask (NSUB = 1: a block below
+        // it holds earlier keys only)
+        const auto round_block = [&](auto masked) __attribute__((always_inline)) {
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int ks = kb * 2 + half, s0 = half * 8;
+          for (int half = 0; half < 2; ++half) {
+            const int ks = kb * 2 + half, s0 = half * 8;
 #pragma unroll
-          for (int u = 0; u < 8; u += 2) {
-            const int i0 = s0 + u, i1 = s0 + u + 1;
-            const int key0 = kb * 32 + (i0 >> 2) * 8 + hl * 4 + (i0 & 3);
-            const int key1 = kb * 32 + (i1 >> 2) * 8 + hl * 4 + (i1 & 3);
-            const bool in0 = key0 <= qrow && (NSUB == 1 || key0 / SUB == qs);
-            const bool in1 = key1 <= qrow && (NSUB == 1 || key1 / SUB == qs);
-            const bf16x2 p2 = to_bf16x2(in0 ? at[i0] : 0.f, in1 ? at[i1] : 0.f);
-            pf[ks][u] = p2[0];
-            pf[ks][u + 1] = p2[1];
-            den = add_bf16x2(p2, den);
+            for (int u = 0; u < 8; u += 2) {
+              const int i0 = s0 + u, i1 = s0 + u + 1;
+              const int key0 = kb * 32 + (i0 >> 2) * 8 + hl * 4 + (i0 & 3);
+              const int key1 = kb * 32 + (i1 >> 2) * 8 + hl * 4 + (i1 & 3);
+              bool in0 = true, in1 = true;
+              if constexpr (decltype(masked)::value) {
+                in0 = key0 <= qrow && (NSUB == 1 || key0 / SUB == qs);
+                in1 = key1 <= qrow && (NSUB == 1 || key1 / SUB == qs);
+              }
+              const bf16x2 p2 = to_bf16x2(in0 ? at[i0] : 0.f, in1 ? at[i1] : 0.f);
+              pf[ks][u] = p2[0];
+              pf[ks][u + 1] = p2[1];
+              den = add_bf16x2(p2, den);
+            }
           }
-        }
+        };
+        if (NSUB == 1 && kb < qb) round_block(std::false_type());
+        else round_block(std::true_type());
       }
       // numerator: E^T A^T (intra) + S^T phi(Q)^T (inter, the state at the
       // start of the query's chunk); the inter-chunk normaliser phi(q)^T z
@@ -646,6 +696,10 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
       const float dcy = exp2_hw(sm.gb()[(CH - 1) * DK + sub * 32 + n] * kLog2e);
 #pragma unroll
       for (int i = 0; i < 16; ++i) st[i] *= dcy;
+    }
+    if (!OUT && SPLIT_E) {
+      lds_barrier();
+      take_e();
     }
     update(OUT ? KS_EARLY : 0, NKS);
   }
