@@ -256,7 +256,7 @@ def main():
         lam, g = inputs.draw_gates(inputs.BASE_SEED + 103, B, H, T, d)
         lamd, gd = lam.to(dev), g.to(dev)
         fng = lambda: binding.fem_softmax_gated_fwd(qd, kd, vd, bd, lamd, gd, out=out)
-        msg, medg = time_calls(fng, args.steps, args.warmup)
+        msg, medg = time_calls(fng, args.steps, args.warmup, args.settle_ms)
         flop_g = 3.0 * B * H * T * (T + 1) * d
         result["gated"] = {
             "workload": w.name + "_gated", "ms": round(msg, 4), "ms_median": round(medg, 4),
@@ -274,7 +274,7 @@ def main():
         wsb = torch.empty(binding.workspace_bytes("bwd", B, H, T, d), device=dev,
                           dtype=torch.uint8)
         fnb = lambda: binding.fem_softmax_bwd(qd, kd, vd, bd, outt, lse, gout, ws=wsb)
-        msb, medb = time_calls(fnb, args.backward_steps, 1)
+        msb, medb = time_calls(fnb, args.backward_steps, 1, args.settle_ms)
         pairs = B * H * T * (T + 1) // 2
         flop_b = 10 * d * pairs
         result["backward"] = {
@@ -293,7 +293,7 @@ def main():
         wsd = torch.empty(binding.workspace_bytes("decode", B, H, T, d, d), device=dev,
                           dtype=torch.uint8)
         fnd = lambda: binding.fem_softmax_decode(q1, kd, vd, bd, out=outd, ws=wsd)
-        msd, medd = time_calls(fnd, args.steps, args.warmup)
+        msd, medd = time_calls(fnd, args.steps, args.warmup, args.settle_ms)
         io = 2 * B * H * T * d * 2 + q1.numel() * 2 + outd.numel() * 4
         result["decode"] = {
             "workload": f"fem_softmax_decode_bf16_B{B}_H{H}_L{T}_d{d}", "ms": round(msd, 4),
@@ -314,7 +314,7 @@ def main():
         wsl = torch.empty(max(1, binding.workspace_bytes("linear", wl.B, wl.H, wl.T, wl.d, wl.dv,
                                                          wl.chunk)), device=dev, dtype=torch.uint8)
         fnl = lambda: binding.fem_linear_fwd(qld, kld, vld, bld, out=outl, chunk=wl.chunk, ws=wsl)
-        msl, medl = time_calls(fnl, args.steps, args.warmup)
+        msl, medl = time_calls(fnl, args.steps, args.warmup, args.settle_ms)
         io = 3 * ql.numel() * 2 + outl.numel() * 4
         result["linear"] = {
             "workload": wl.name, "chunk": wl.chunk, "ms": round(msl, 4), "ms_median": round(medl, 4),
@@ -331,7 +331,7 @@ def main():
                               dtype=torch.uint8)
             fng = lambda: binding.fem_gla_fwd(qld, kld, vld, gld, bld, out=outl, chunk=wl.chunk,
                                               ws=wsg)
-            msg, medg = time_calls(fng, args.steps, args.warmup)
+            msg, medg = time_calls(fng, args.steps, args.warmup, args.settle_ms)
             iog = 3 * ql.numel() * 2 + gld.numel() * 4 + outl.numel() * 4
             result["gla"] = {
                 "workload": wl.name.replace("linear", "gla"), "chunk": wl.chunk,

@@ -171,10 +171,11 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// elu(x) + 1, without a branch: the exponential is evaluated for every x (at
-// min(x, 0), so it stays finite) and selected.
+// elu(x) + 1, without a branch: the exponential is evaluated for every x and
+// selected (for a large positive x it overflows to +inf, which the select
+// discards).
 __device__ __forceinline__ float phi(float x) {
-  const float e = exp2_hw(fminf(x, 0.f) * kLog2e);
+  const float e = exp2_hw(x * kLog2e);
   return x > 0.f ? x + 1.f : e;
 }
 
@@ -452,14 +453,16 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
     bf16x8 vr[NKS];
 #pragma unroll
     for (int f = 0; f < NKS; ++f) vr[f] = frag_tr<DV>(sm.vs, dvb * 32, ksof(f) * 16);
-    // keys at or past T (last tile only) stay out of the max and give E = 0
-    const bool full = t0 + CH <= T;
+    // keys at or past T (a partial last tile only) stay out of the max and
+    // give E = 0
+    const auto tilt = [&](auto partial) __attribute__((always_inline)) {
+    constexpr bool PART = decltype(partial)::value;
     float vmax = -INFINITY;
 #pragma unroll
     for (int f = 0; f < NKS; ++f) {
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        if (full || t0 + e_pos(ksof(f) * 16 + hl * 8 + u) < T) vmax = fmaxf(vmax, (float)vr[f][u]);
+        if (!PART || t0 + e_pos(ksof(f) * 16 + hl * 8 + u) < T) vmax = fmaxf(vmax, (float)vr[f][u]);
     }
     vmax = fmaxf(vmax, other_half(vmax));  // lanes n and n + 32 hold the same channel
     const float mx = vmax * blj;
@@ -479,7 +482,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         for (int b = 0; b < 2; ++b) {
           const int key = e_pos(ks * 16 + hl * 8 + u + b);
           const float x = exp2_hw(fmaf((float)v[u + b], blj, sh));
-          ev[b] = (full || t0 + key < T) ? x : 0.f;
+          ev[b] = (!PART || t0 + key < T) ? x : 0.f;
         }
         const bf16x2 h2 = to_bf16x2(ev[0], ev[1]);
         const bf16x2 l2 = to_bf16x2(ev[0] - (float)h2[0], ev[1] - (float)h2[1]);
@@ -493,6 +496,9 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         sm.ex[((dvb * NKS + ks) * 2 + 1) * 64 + lane] = el[kk];
       }
     }
+    };
+    if (t0 + CH <= T) tilt(std::false_type());
+    else tilt(std::true_type());
   }
   // every k-step's E of the block, after a barrier that follows the stores
   auto take_e = [&]() {
