@@ -141,7 +141,9 @@ struct ScanSmem : LinSmem<CH, NSUB> {
 };
 template <>
 struct ScanSmem<kGla, GCH, 1> : LinSmem<GCH, 1> {
-  static constexpr bool SPLIT_E = false;  // (its LDS is at the two-workgroup limit)
+  // (with the exchange buffer the state pass would lose its second
+  // workgroup per CU; splitting the read's tilt alone measured slower)
+  static constexpr bool SPLIT_E = false;
   bf16x8 ex[1];
   GlaSmem gla;
   __device__ float* gb() { return gla.b; }
@@ -321,8 +323,11 @@ __device__ __forceinline__ void fetch_chunk(ChunkRegs<CH>& cr, const bf16* Qh, c
 // The tilt E^T (32 channels x CH keys of the wave's block) is formed in
 // registers as the MFMA A operand: lane (n, hl) holds channel dvb*32 + n and
 // the keys at MFMA positions ks*16 + hl*8 .. +8 of each k-step ks, read from
-// V^T staged in the same key order.  The two waves of a channel block form
-// the same E; each lane keeps the running shift cj of its channel.
+// V^T staged in the same key order.  Each lane keeps the running shift cj
+// of its channel; the two waves of a channel block compute the same shift
+// and, for the linear prior with one chunk per tile of at most 64 tokens,
+// form the E of half the k-steps each (the halves meet in LDS); otherwise
+// both form all of it.
 template <int PRIOR, bool OUT, int CH, int NSUB>
 __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16& st, float& cj,
                                            float blj, float& ldc, ChunkRegs<CH>& cr,
