@@ -251,7 +251,7 @@ def main():
     if not args.no_extra:
         for no in (2, 4):
             result[f"config{no}"] = softmax_entry(binding, inputs, dev, no, args.steps,
-                                                  args.warmup, 0.0)
+                                                  args.warmup, args.settle_ms)
     if not args.no_gated:
         lam, g = inputs.draw_gates(inputs.BASE_SEED + 103, B, H, T, d)
         lamd, gd = lam.to(dev), g.to(dev)
