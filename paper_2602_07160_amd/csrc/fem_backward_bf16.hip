@@ -25,10 +25,6 @@
 // most 0 up to rounding, so nothing overflows, and no shared shift can
 // underflow an in-support term.  That is T^2 d / 2 exponentials, on the
 // vector units; the contractions around it run on the matrix cores:
-//   kv kernel: one workgroup per (b, h, 64-key tile), over the query tiles
-//              at or after its diagonal: S = Q K^T (MFMA), the posterior loop
-//              (thread = key, channel quarter) accumulates dV and forms dS,
-//              then dK += dS^T Q (MFMA);
 //   q kernel:  one workgroup per (b, h, 64-query tile), over the key tiles up
 //              to its diagonal: S = Q K^T, the posterior loop (thread = query,
 //              channel quarter) forms dS, then dQ += dS K (MFMA).  It also
@@ -38,7 +34,12 @@
 //              F = F^ + ln(Z/P)/beta exactly, E_q[v] - F = X/Z - ln(Z/P)/beta,
 //              in which the forward's rounding of F^ and lse cancels (it would
 //              otherwise swamp the small difference E_q[v] - F ~ beta Var/2
-//              at small beta);
+//              at small beta).  It writes beta log2e F for the kv kernel;
+//   kv kernel: one workgroup per (b, h, 64-key tile), over the query tiles
+//              at or after its diagonal: S = Q K^T (MFMA), the posterior loop
+//              (thread = key, channel quarter) accumulates dV and forms dS
+//              from the posterior at the q kernel's F, which sums to one over
+//              the keys, then dK += dS^T Q (MFMA);
 //   dbeta:     per (h, j), the q kernel's per-tile sums of
 //              G (E_q[v] - F) / beta, added in double precision.
 // No atomics: every output is written by exactly one workgroup.
@@ -176,10 +177,12 @@ __device__ __forceinline__ void block_logp(S& sm, const float* lse2, int q0, int
 
 // ---- kv kernel: dK, dV -----------------------------------------------------
 
+// FB: beta log2e F per (t, j) of the channels it takes, the read with the
+// forward's rounding removed (written by bwd_q_kernel, which runs first).
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
-    const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ lse,
+    const float* __restrict__ beta, const float* __restrict__ FB, const float* __restrict__ lse,
     const float* __restrict__ G, float* __restrict__ dK, float* __restrict__ dV, int H, int T,
     int ntile, const int* __restrict__ flag, const float* __restrict__ splitf) {
   using C = Bw<D>;
@@ -233,9 +236,6 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
       constexpr int N = kTile * D / 4 / kThreads, RPI = kThreads / (D / 4), NB = N >= 4 ? 4 : N;
       static_assert(N * kThreads == kTile * D / 4 && N % NB == 0, "whole rounds");
       const int c4 = (tid % (D / 4)) * 4, t0 = tid / (D / 4);
-      f32x4 bl4;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) bl4[u] = beta[h * D + c4 + u] * kLog2e;
 #pragma unroll
       for (int i0 = 0; i0 < N; i0 += NB) {
         f32x4 g[NB], f[NB];
@@ -246,14 +246,15 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_kernel(
           f[i] = f32x4{};
           if (q0 + t < T) {
             g[i] = *reinterpret_cast<const f32x4*>(G + base + (size_t)(q0 + t) * D + c4);
-            f[i] = *reinterpret_cast<const f32x4*>(F + base + (size_t)(q0 + t) * D + c4);
+            f[i] = *reinterpret_cast<const f32x4*>(FB + base + (size_t)(q0 + t) * D + c4);
           }
         }
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
           const int t = t0 + (i0 + i) * RPI;
           *reinterpret_cast<f32x4*>(sm.gq + t * D + c4) = g[i];
-          *reinterpret_cast<f32x4*>(sm.fb + t * D + c4) = bl4 * f[i];
+          // (channels not taken here hold stale values, never read)
+          *reinterpret_cast<f32x4*>(sm.fb + t * D + c4) = f[i];
         }
       }
     }
@@ -358,8 +359,9 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ K, const bf16* __restrict__ V,
     const float* __restrict__ beta, const float* __restrict__ F, const float* __restrict__ lse,
-    const float* __restrict__ G, float* __restrict__ dQ, float* __restrict__ dbp, int H, int T,
-    int ntile, const int* __restrict__ flag, const float* __restrict__ splitf) {
+    const float* __restrict__ G, float* __restrict__ dQ, float* __restrict__ dbp,
+    float* __restrict__ FB, int H, int T, int ntile, const int* __restrict__ flag,
+    const float* __restrict__ splitf) {
   using C = Bw<D>;
   static_assert(D <= kThreads && C::JPT <= 32, "channel masks");
   const int mode = exact_mode(flag);
@@ -492,6 +494,17 @@ __global__ __launch_bounds__(kThreads) void bwd_q_kernel(
       float* at = dQ + base + (size_t)t * D + cb * 32 + n;
       *at = all ? dq[c][r] * rs : *at + dq[c][r] * rs;  // wide only: add to the matrix-core dQ
     }
+  }
+
+  // The read with the forward's rounding removed, beta log2e F = beta log2e
+  // F^ + log2(Z/P), for the kv kernel: its posterior then sums to one over
+  // the keys, and so do the dV and dS it forms.
+  if (q0 + qi < T) {
+#pragma unroll
+    for (int u = 0; u < C::JPT; ++u)
+      if ((act >> u) & 1)
+        FB[base + (size_t)(q0 + qi) * D + j0 + u] =
+            zs[u] > 0.f ? fb[u] + (log2_hw(zs[u]) - log2_hw(ps)) : fb[u];
   }
 
   // dbeta partial of this tile: sum_t G (X/Z - ln(Z/P)/beta)/beta, with
@@ -1392,15 +1405,19 @@ hipError_t launch_bwd(const void* Q, const void* K, const void* V, const float* 
   }
   // element-wise passes: they return at once unless a wide channel or a
   // failed guard raised a flag; wide channels only add to dQ / dK and write
-  // their own dV columns, a failed guard replaces every gradient
+  // their own dV columns, a failed guard replaces every gradient.  The q
+  // pass runs first: it leaves the normalised beta log2e F of the channels
+  // it takes in the SA / P buffer (free once the fast kv pass has run),
+  // which the kv pass's posterior uses.
+  float* fbn = sap;
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(bwd_kv_kernel<D>, grid, blk, 0, stream, q, k, v, beta, out, lse, dout, dK, dV,
-                       H, T, ntile, flag, splitf);
+    hipLaunchKernelGGL(bwd_q_kernel<D>, grid, blk, 0, stream, q, k, v, beta, out, lse, dout, dQ,
+                       exact, fbn, H, T, ntile, flag, splitf);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(bwd_q_kernel<D>, grid, blk, 0, stream, q, k, v, beta, out, lse, dout, dQ,
-                       exact, H, T, ntile, flag, splitf);
+    hipLaunchKernelGGL(bwd_kv_kernel<D>, grid, blk, 0, stream, q, k, v, beta, fbn, lse, dout, dK, dV,
+                       H, T, ntile, flag, splitf);
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
