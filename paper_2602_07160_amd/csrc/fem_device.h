@@ -105,6 +105,51 @@ __device__ __forceinline__ void dma16s(const void* base_any, unsigned off, void*
       : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_addr(dst)))
       : "memory");
 }
+// The same load with the LDS byte address given as an integer the caller
+// keeps wave-uniform (no pointer conversion per load): with a uniform base
+// and address the block is five scalar instructions and the load.
+__device__ __forceinline__ void dma16u(const void* base_any, unsigned off, unsigned lds) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base_any);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((unsigned)(b >> 32));
+  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((unsigned)b);
+  const uint64_t base = ((uint64_t)hi << 32) | (uint64_t)lo;
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"((unsigned)__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
+}
+// Buffer-resource form: rsrc covers [base, base + bytes) (a raw buffer:
+// stride 0, 32-bit data format), so a lane whose offset falls past its end
+// loads zeros and reads nothing outside the range.  All operands wave-uniform
+// except the lane offset.
+typedef __attribute__((ext_vector_type(4))) int rsrc_t;
+__device__ __forceinline__ rsrc_t buffer_rsrc(const void* base_any, unsigned bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base_any);
+  rsrc_t r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(unsigned)b);
+  r[1] = __builtin_amdgcn_readfirstlane((int)(unsigned)(b >> 32)) & 0xffff;  // stride 0
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;  // data format: 32 bits
+  return r;
+}
+__device__ __forceinline__ void dma16b(rsrc_t rsrc, unsigned off, unsigned lds) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(rsrc), "s"((unsigned)__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
+}
 __device__ __forceinline__ void dma4(const void* src, void* dst) {
   unsigned saved;
   asm volatile(

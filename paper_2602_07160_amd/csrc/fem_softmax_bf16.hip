@@ -244,9 +244,9 @@ __device__ __forceinline__ float max_xor(float x, int o) {
 //             into bf16 hi (truncated) and lo (the rounded remainder), or for
 //             a column without lo product E rounded to bf16, and the store of
 //             run u into the E^T buffers.
-// Keys at or past T (last tile only) hold copies of row T-1 (see load_tile):
-// they leave the column max unchanged and give finite E, which meet P = 0
-// (the causal mask), so the tilt treats every tile as full.
+// Keys at or past T (last tile only) were loaded as zeros (see load_block);
+// read() turns them into -inf, so they leave the column max unchanged and
+// give E = 0, which meets P = 0 (the causal mask).
 // Stores that only one lane of a group should make go to a sink slot from the
 // other lanes, so the code has no branches.
 template <class C>
@@ -257,7 +257,12 @@ struct Tilt {
   float bl, cold, cnew, sh;
   unsigned char* eh;
 
-  __device__ __forceinline__ void read(const Smem<C>& sm, int tt, int wave, int lane, int vcol) {
+  // nvalid: the tile's keys before T.  Rows past it were loaded as zeros;
+  // the read and gated modes take them as -inf, which stays out of the
+  // column max and gives E = 0 (P = 0 there anyway); the mean mode keeps
+  // the zeros as values.
+  __device__ __forceinline__ void read(const Smem<C>& sm, int tt, int nvalid, int wave, int lane,
+                                       int vcol) {
     const int jj = lane % C::CPW, g = lane / C::CPW;
     const int j = wave * C::CPW + jj;
     const unsigned char* sv =
@@ -267,6 +272,14 @@ struct Tilt {
 #pragma unroll
       for (int b = 0; b < 4; ++b)
         v[u][b] = (float)*reinterpret_cast<const bf16*>(sv + (4 * C::G * u + b) * C::VROW * 2);
+    }
+    if (MODE != kMean && nvalid < C::BK) {
+#pragma unroll
+      for (int u = 0; u < C::RPL; ++u) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          if (4 * (g + C::G * u) + b >= nvalid) v[u][b] = -INFINITY;
+      }
     }
     if (MODE == kMean) {
       eh = sm.base + pin(C::OFF_EH + (tt & 1) * C::EB + j * C::EROW * 2 + e_pos(4 * g) * 2);
@@ -420,26 +433,28 @@ struct Softmax {
 // Direct global -> LDS copy of one K or V tile (rows k0 .. k0+63, padded rows).
 // Wave w writes 1 KiB blocks w, w+NW, ...; lane l of a block fills slot
 // 64*blk + l, i.e. row slot/SPR, chunk slot%SPR (the pad chunk re-reads chunk
-// 0).  Rows at or past T are clamped to T-1: their keys are masked anyway.
-// The address is a uniform tile base plus a 32-bit lane offset, so the loads
-// use scalar-base addressing.  The lane offsets are a few integer operations,
-// recomputed per tile inside the MFMA slots of phase 1.
+// 0).  The lane offset inside the tile is the same for every tile and is
+// computed once.
 template <int W, int NW>
-__device__ __forceinline__ unsigned tile_offset(int u, int k0, int T, int wave, int lane) {
+__device__ __forceinline__ unsigned tile_offset(int u, int wave, int lane) {
   constexpr int SPR = (W + 8) / 8;  // 16-byte slots per padded row
   const int slot = (wave + NW * u) * 64 + lane;
-  const int row = min(slot / SPR, T - 1 - k0), chunk = slot % SPR;
+  const int row = slot / SPR, chunk = slot % SPR;
   return (unsigned)(row * W + (chunk < W / 8 ? chunk * 8 : 0)) * 2u;
 }
 
 // Block u of this wave's share of a tile: the direct load, if the tile has it.
+// rsrc covers the rows k0 .. T-1 of the head, so rows at or past T load as
+// zeros (their keys are masked; the tilt leaves them out of the column max).
+// wave_s is the wave index held as a scalar and dst the LDS byte address of
+// the tile buffer, so the block's LDS address and the test are scalar work;
+// off is the lane offset inside the tile, the same for every tile.
 template <int W, int NW>
-__device__ __forceinline__ void load_block(const bf16* __restrict__ src, unsigned char* dst,
-                                           int k0, int wave, int u, unsigned off) {
+__device__ __forceinline__ void load_block(rsrc_t rsrc, unsigned dst, int wave_s, int u,
+                                           unsigned off) {
   constexpr int BLOCKS = 64 * ((W + 8) / 8) / 64;
-  const int blk = wave + NW * u;
-  if (BLOCKS % NW == 0 || blk < BLOCKS)
-    dma16s(src + (size_t)k0 * W, off, dst + blk * 1024);
+  const int blk = wave_s + NW * u;
+  if (BLOCKS % NW == 0 || blk < BLOCKS) dma16b(rsrc, off, dst + (unsigned)blk * 1024u);
 }
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -461,7 +476,7 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // output row 4r, which the 16x16 output layout places in register 0 of lane
 // 16r + l%16.  Hence lacc[0] of every lane is the row sum of its query l%32.
 template <class C, int NLO, bool PVA, bool QKT, class Side>
-__device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, int wave, int lane,
+__device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, int nvalid, int wave, int lane,
                                        int kofs, int eofs, int vcol, const bf16x8 (&qf)[C::NKS],
                                        f32x16 (&s)[2], f32x16 (&acc)[C::NCB], f32x4& lacc,
                                        const bf16x8 (&pp)[4], const bf16x8& lsel, Side&& side) {
@@ -482,7 +497,7 @@ __device__ __forceinline__ void phase1(const Smem<C>& sm, Tilt<C>& tl, int k, in
   constexpr int V0 = CM + 2;
   constexpr int NVS = NV > 0 ? V0 + NV + 2 : 0;
   constexpr int NSLOT = NS > NVS ? NS : NVS;
-  if (QKT) tl.read(sm, k, wave, lane, vcol);
+  if (QKT) tl.read(sm, k, nvalid, wave, lane, vcol);
   const bool lo = wave * C::CPW < 32 * NLO;  // this wave's columns take the lo product
   const unsigned char* kt = sm.base + pin(C::OFF_K + (k & 1) * C::KB + kofs);
   const unsigned char* eb = sm.base + (PVA ? pin(C::OFF_EH + ((k - 1) & 1) * C::EB + eofs) : 0u);
@@ -683,12 +698,33 @@ __device__ __forceinline__ void read_body(
                     : C::CAUSAL ? min((wq0 + 31) / C::BK, ntiles - 1)
                                 : ntiles - 1;
 
+  // the wave index as a scalar and the LDS byte address of the tile
+  // buffers, for the direct loads' addresses
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const unsigned lds0 = lds_addr(smem);
+  // lane offsets of a full K / V tile (the same for every tile)
+  unsigned koff[C::BPWK], voff[C::BPWV];
 #pragma unroll
-  for (int u = 0; u < C::BPWK; ++u)
-    load_block<C::DK, C::NW>(Kh, sm.k(0), 0, wave, u, tile_offset<C::DK, C::NW>(u, 0, T, wave, lane));
+  for (int u = 0; u < C::BPWK; ++u) koff[u] = tile_offset<C::DK, C::NW>(u, wave, lane);
 #pragma unroll
   for (int u = 0; u < C::BPWV; ++u)
-    load_block<C::DV, C::NW>(Vh, sm.v(0), 0, wave, u, tile_offset<C::DV, C::NW>(u, 0, T, wave, lane));
+    voff[u] = C::SAME ? koff[u] : tile_offset<C::DV, C::NW>(u, wave, lane);
+  // rows k0 .. T-1 of the head's K and V
+  auto krsrc = [&](int k0) { return buffer_rsrc(Kh + (size_t)k0 * C::DK, (unsigned)(T - k0) * C::DK * 2u); };
+  auto vrsrc = [&](int k0) { return buffer_rsrc(Vh + (size_t)k0 * C::DV, (unsigned)(T - k0) * C::DV * 2u); };
+  auto kload = [&](int u, const rsrc_t& r, int buf) {
+    load_block<C::DK, C::NW>(r, lds0 + C::OFF_K + buf * C::KB, wave_s, u, koff[u]);
+  };
+  auto vload = [&](int u, const rsrc_t& r, int buf) {
+    load_block<C::DV, C::NW>(r, lds0 + C::OFF_V + buf * C::VB, wave_s, u, voff[u]);
+  };
+  {
+    const rsrc_t rk = krsrc(0), rv = vrsrc(0);
+#pragma unroll
+    for (int u = 0; u < C::BPWK; ++u) kload(u, rk, 0);
+#pragma unroll
+    for (int u = 0; u < C::BPWV; ++u) vload(u, rv, 0);
+  }
   bf16x8 qf[C::NKS];
 #pragma unroll
   for (int ks = 0; ks < C::NKS; ++ks) {
@@ -723,18 +759,14 @@ __device__ __forceinline__ void read_body(
   const int kofs = n * C::KROW * 2 + hl * 16;  // lane part of K fragment addresses
   const int eofs = n * C::EROW * 2 + hl * 16;  // lane part of E fragment addresses
 
-  // Direct loads of tile k+1 into the free K and V buffers; the lane offsets
-  // are a few integer operations each.
+  // Direct loads of tile k+1 into the free K and V buffers.
   auto load_next = [&](int k) {
     const int kn = (k + 1) * C::BK;
+    const rsrc_t rk = krsrc(kn), rv = vrsrc(kn);
 #pragma unroll
-    for (int u = 0; u < C::BPWK; ++u)
-      load_block<C::DK, C::NW>(Kh, sm.k((k + 1) & 1), kn, wave, u,
-                               tile_offset<C::DK, C::NW>(u, kn, T, wave, lane));
+    for (int u = 0; u < C::BPWK; ++u) kload(u, rk, (k + 1) & 1);
 #pragma unroll
-    for (int u = 0; u < C::BPWV; ++u)
-      load_block<C::DV, C::NW>(Vh, sm.v((k + 1) & 1), kn, wave, u,
-                               tile_offset<C::DV, C::NW>(u, kn, T, wave, lane));
+    for (int u = 0; u < C::BPWV; ++u) vload(u, rv, (k + 1) & 1);
   };
   // The same loads spread over the MFMA slots of phase 1, one per slot from
   // slot LD0 on (K blocks, then V blocks), so that the waves of a workgroup
@@ -743,15 +775,12 @@ __device__ __forceinline__ void read_body(
   auto loads_in_slots = [&](int k) {
     const bool more = k + 1 < ntiles;
     const int kn = (k + 1) * C::BK;
+    const rsrc_t rk = krsrc(kn), rv = vrsrc(kn);
     return [=](int st) __attribute__((always_inline)) {
       if (!more) return;
       const int u = st - LD0, w = u - C::BPWK;
-      if (u >= 0 && u < C::BPWK)
-        load_block<C::DK, C::NW>(Kh, sm.k((k + 1) & 1), kn, wave, u,
-                                 tile_offset<C::DK, C::NW>(u, kn, T, wave, lane));
-      if (w >= 0 && w < C::BPWV)
-        load_block<C::DV, C::NW>(Vh, sm.v((k + 1) & 1), kn, wave, w,
-                                 tile_offset<C::DV, C::NW>(w, kn, T, wave, lane));
+      if (u >= 0 && u < C::BPWK) kload(u, rk, (k + 1) & 1);
+      if (w >= 0 && w < C::BPWV) vload(w, rv, (k + 1) & 1);
     };
   };
   // Deferred rescales owed before PV(j): the row factor of softmax(j) and the
@@ -785,7 +814,7 @@ __device__ __forceinline__ void read_body(
     return any4;
   };
 #define FEM_PHASE1(PVA, QKT, PPREV, SIDE)                                                   \
-  phase1<C, NLO, PVA, QKT>(sm, tl, k, wave, lane, kofs, eofs, vcol, qf, sacc, acc, lacc, PPREV, \
+  phase1<C, NLO, PVA, QKT>(sm, tl, k, T - k * C::BK, wave, lane, kofs, eofs, vcol, qf, sacc, acc, lacc, PPREV, \
                            lsel, SIDE)
   const auto none = [](auto...) __attribute__((always_inline)) {};
 #define FEM_PHASE2(PVB, SM, MK, PPREV, PNEXT)                                                    \
