@@ -179,6 +179,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-extra", action="store_true", help="time the headline workload only")
+    ap.add_argument("--no-config24", action="store_true", help="skip the config2 / config4 timings")
     ap.add_argument("--no-linear", action="store_true")
     ap.add_argument("--no-gated", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
@@ -248,7 +249,7 @@ def main():
             "kernel": "softmax_bf16_kernel<128,128,8,kFem>",
         },
     }
-    if not args.no_extra:
+    if not args.no_extra and not args.no_config24:
         for no in (2, 4):
             result[f"config{no}"] = softmax_entry(binding, inputs, dev, no, args.steps,
                                                   args.warmup, args.settle_ms)
