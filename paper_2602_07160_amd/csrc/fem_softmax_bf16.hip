@@ -167,14 +167,19 @@ __device__ __forceinline__ unsigned pin(unsigned x) {
   return x;
 }
 
-// Exact fp32 read of one (t, j) by the whole wave: joint log-sum-exp of
-// (score + tilt) over the keys i < n, minus the log-sum-exp of the scores.
-template <class C>
-__device__ float exact_read(const bf16* __restrict__ Qh, const bf16* __restrict__ Kh,
-                            const bf16* __restrict__ Vh, int t, int n, int j, float scale2,
-                            float bl) {
+// Channels of one row recomputed per pass over its keys by the exact path.
+constexpr int kRepairBatch = 16;
+
+// Exact fp32 read of channels ch[0..nb) (nb <= NB) of row t by the whole
+// wave: per channel the joint log-sum-exp of (score + tilt) over the keys
+// i < n, minus the log-sum-exp of the scores; each key's score is formed
+// once for the whole batch.  Lane c < nb returns channel ch[c]'s value.
+template <class C, int NB>
+__device__ float exact_row(const bf16* __restrict__ Qh, const bf16* __restrict__ Kh,
+                           const bf16* __restrict__ Vh, int t, int n, const int (&ch)[NB],
+                           const float (&bl)[NB], int nb, float scale2) {
   const int lane = threadIdx.x & 63;
-  Lse2 num, den;
+  Lse2 den, num[NB];
   const bf16x8* qrow = reinterpret_cast<const bf16x8*>(Qh + (size_t)t * C::DK);
   for (int i = lane; i < n; i += 64) {
     const bf16x8* krow = reinterpret_cast<const bf16x8*>(Kh + (size_t)i * C::DK);
@@ -187,9 +192,19 @@ __device__ float exact_read(const bf16* __restrict__ Qh, const bf16* __restrict_
     }
     const float s = dot * scale2;
     den.add(s);
-    num.add(s + (float)Vh[(size_t)i * C::DV + j] * bl);
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+      if (c < nb) num[c].add(s + (float)Vh[(size_t)i * C::DV + ch[c]] * bl[c]);
   }
-  return (num.wave_total() - den.wave_total()) / bl;
+  const float d = den.wave_total();
+  float mine = 0.f;
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    if (c >= nb) break;
+    const float o = (num[c].wave_total() - d) / bl[c];
+    if (lane == c) mine = o;
+  }
+  return mine;
 }
 
 template <class C>
@@ -994,32 +1009,58 @@ __device__ __forceinline__ void read_body(
     }
   }
 
-  // ---- rare path: exact recompute of accumulators that underflowed
+  // ---- rare path: exact recompute of accumulators that underflowed, one
+  // row at a time (its flags sit in lanes n and n + 32), up to kRepairBatch
+  // of its channels per pass over the keys, so that a row's scores are
+  // formed once per batch rather than once per channel
+  if (__ballot(flags != 0) == 0) return;
+  wait_vmem();  // the epilogue's stores above (the gated mix reads mu back)
   while (true) {
     const uint64_t who = __ballot(flags != 0);
     if (who == 0) break;
-    const int src = __builtin_ctzll(who);
-    const uint32_t flo = __builtin_amdgcn_readlane((uint32_t)flags, src);
-    const uint32_t fhi = __builtin_amdgcn_readlane((uint32_t)(flags >> 32), src);
-    const uint64_t fl64 = ((uint64_t)fhi << 32) | flo;
-    const int e = __builtin_ctzll(fl64);
-    const int t = __builtin_amdgcn_readlane(tq, src);
-    const int cb = e >> 4, i = e & 15;
-    const int col = cb * 32 + (i >> 2) * 8 + (src >> 5) * 4 + (i & 3);
-    const int ch = SPLIT ? sm.chan()[col] : col;  // input channel
-    const float o = exact_read<C>(Qh, Kh, Vh, t, C::CAUSAL ? t + 1 : T, ch, scale2, sm.bl()[col]);
-    if (lane == src) {
-      flags &= ~(1ull << e);
-      const size_t at = (size_t)t * C::DV + ch;
-      if (MODE == kGated) {
-        const float mu = Oh[at];
-        Oh[at] = (Gh ? Gh[at] : 1.f) * fmaf(Lh[at], o - mu, mu);
-      } else if (C::OBF16) {
-        Ob[at] = (bf16)o;
-      } else {
-        Oh[at] = o;
+    const int r = __builtin_ctzll(who) & 31;
+    const int t = __builtin_amdgcn_readlane(tq, r);
+    uint64_t fw[2];  // the row's flag words: channels of lane half 0 and 1
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t flo = __builtin_amdgcn_readlane((uint32_t)flags, r + 32 * h);
+      const uint32_t fhi = __builtin_amdgcn_readlane((uint32_t)(flags >> 32), r + 32 * h);
+      fw[h] = ((uint64_t)fhi << 32) | flo;
+    }
+    while ((fw[0] | fw[1]) != 0) {
+      int chs[kRepairBatch];
+      float bls[kRepairBatch];
+      int nb = 0, mych = 0;
+#pragma unroll
+      for (int c = 0; c < kRepairBatch; ++c) {
+        chs[c] = 0;
+        bls[c] = 1.f;
+        if ((fw[0] | fw[1]) == 0) continue;
+        const int h = fw[0] != 0 ? 0 : 1;
+        const int e = __builtin_ctzll(fw[h]);
+        fw[h] &= fw[h] - 1;
+        const int cb = e >> 4, i = e & 15;
+        const int col = cb * 32 + (i >> 2) * 8 + h * 4 + (i & 3);
+        chs[c] = SPLIT ? sm.chan()[col] : col;  // input channel
+        bls[c] = sm.bl()[col];
+        nb = c + 1;
+        if (lane == c) mych = chs[c];
+      }
+      const float o = exact_row<C, kRepairBatch>(Qh, Kh, Vh, t, C::CAUSAL ? t + 1 : T, chs, bls, nb,
+                                                 scale2);
+      if (lane < nb) {
+        const size_t at = (size_t)t * C::DV + mych;
+        if (MODE == kGated) {
+          const float mu = Oh[at];
+          Oh[at] = (Gh ? Gh[at] : 1.f) * fmaf(Lh[at], o - mu, mu);
+        } else if (C::OBF16) {
+          Ob[at] = (bf16)o;
+        } else {
+          Oh[at] = o;
+        }
       }
     }
+    if ((lane & 31) == r) flags = 0;
   }
 }
 

@@ -282,6 +282,24 @@ def test_bf16_first_tile_underflow(fem):
     np.testing.assert_allclose(got[0, 0, :32], -5.0, atol=TOL_BF16)
 
 
+@pytest.mark.parametrize("d,T", [(128, 256), (64, 300), (32, 200)])
+def test_bf16_whole_rows_underflow(fem, d, T):
+    """Every channel of every row before the block's last key underflows
+    against that key's value (-5 everywhere, +5 at the last key, beta 16):
+    the exact path repairs whole rows, a batch of channels per pass over the
+    keys, and must agree with the oracle on every element."""
+    say(f"bf16 whole-row underflow: B1 H2 T{T} d{d}, v=-5 then +5 at the last key, beta=16")
+    q, k, _, _ = inputs.draw(3007, 1, 2, T, d, dtype="bf16")
+    v = torch.full((1, 2, T, d), -5.0)
+    v[:, :, T - 1] = 5.0
+    v[:, 1, :, 1::2] = torch.randn(1, T, d // 2, generator=torch.Generator().manual_seed(1))
+    v = v.to(torch.bfloat16)
+    b = torch.full((2, d), 16.0)
+    got = run(fem, q, k, v, b)
+    check(got, ref(q, k, v, b), TOL_BF16, "whole-row underflow repair")
+    np.testing.assert_allclose(got[0, 0, : T - 1], -5.0, atol=TOL_BF16)
+
+
 def test_bf16_scale_law(fem):
     """F(beta; 2v) = 2 F(2beta; v); doubling is exact in bf16."""
     say("bf16 scale law a=2: B1 H2 T400 d128")
