@@ -113,7 +113,7 @@ struct LinSmem {
   bf16 vs[CH * DV];           // V [key][d_v], swizzled; V^T comes from transposing reads
   bf16 sh[NSUB][DV * SROW];   // S^T hi [d_v][d_k] at the start of each sub-chunk
   bf16 sl[NSUB][DV * SROW];   // S^T lo
-  float c[DV];                // running shift (published for the epilogue)
+  float ci[DV];               // (c - kBias) / (beta log2 e): the running shift as the epilogue adds it
   float bl[DV];               // beta log2 e
   float inv[DV];
   float z[DK];                // sum of phi(k) over earlier tiles
@@ -566,7 +566,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
       update(0, KS_EARLY);
       snapshot(1);
     }
-    if (sub == 0 && hl == 0) sm.c[ch] = cj;
+    if (sub == 0 && hl == 0) sm.ci[ch] = (cj - kBias) * sm.inv[ch];
     lds_barrier();
     take_e();
 
@@ -662,25 +662,33 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
       }
       den += (dz[0] + dz[1]) + (dz[2] + dz[3]);
       den += other_half(den);
-      // epilogue
-      int ed;
-      const float fd = log2_hw(frexpf(den, &ed));
-      uint32_t flags = 0;
+      // epilogue: F = (log2(num / den) + c - kBias) / (beta log2 e), one
+      // logarithm per output.  num / den is a weighted mean of E (at most
+      // 2^(kColLag + kBias)); it is flagged below when it or num could have
+      // lost precision (num < 2^-64, or num / den < 2^-100)
+      const float rd = __builtin_amdgcn_rcpf(den);
+      float amin = INFINITY;
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const int ch0 = dvb * 32 + g4 * 8 + hl * 4;
-        const f32x4 cc = *reinterpret_cast<const f32x4*>(sm.c + ch0);
+        const f32x4 ci = *reinterpret_cast<const f32x4*>(sm.ci + ch0);
         const f32x4 iv = *reinterpret_cast<const f32x4*>(sm.inv + ch0);
         f32x4 o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float a = num[g4 * 4 + e];
-          int ea;
-          const float fa = log2_hw(frexpf(a, &ea));
-          o[e] = ((float)(ea - ed - (int)kBias) + (fa - fd) + cc[e]) * iv[e];
-          if (!(a >= kUnderflow) && tq < T) flags |= 1u << (g4 * 4 + e);
+          o[e] = fmaf(log2_hw(a * rd), iv[e], ci[e]);
+          amin = fminf(amin, a);
         }
         if (tq < T) *reinterpret_cast<f32x4*>(Oh + (size_t)tq * DV + ch0) = o;
+      }
+      // outputs whose numerator underflowed (rare): recomputed exactly below
+      uint32_t flags = 0;
+      const auto low = [&](float a) { return !(a >= kUnderflow && a * rd >= 0x1p-100f); };
+      if (__ballot(low(amin) && tq < T) != 0) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (low(num[i]) && tq < T) flags |= 1u << i;
       }
       while (true) {
         const uint64_t who = __ballot(flags != 0);
