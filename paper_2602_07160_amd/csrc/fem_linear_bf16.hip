@@ -327,8 +327,10 @@ __device__ __forceinline__ void fetch_chunk(ChunkRegs<CH>& cr, const bf16* Qh, c
 // of its channel; the two waves of a channel block compute the same shift
 // and, for the linear prior with one chunk per tile of at most 64 tokens,
 // form the E of half the k-steps each (the halves meet in LDS); otherwise
-// both form all of it.
-template <int PRIOR, bool OUT, int CH, int NSUB>
+// both form all of it.  FIXED: the shift is the segment's own, set before
+// the first tile (every value of the segment lies at most kColLag above it),
+// so no tile raises it and only the wave's own k-steps of V^T are read.
+template <int PRIOR, bool OUT, int CH, int NSUB, bool FIXED>
 __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16& st, float& cj,
                                            float blj, float& ldc, ChunkRegs<CH>& cr,
                                            const bf16* Qh, const bf16* Kh, const bf16* Vh,
@@ -455,27 +457,33 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
     // V^T fragments, this wave's half of the k-steps first (split: the
     // k-step of fragment f is ksof(f))
     const auto ksof = [&](int f) { return SPLIT_E ? (f + sub * KSH) % NKS : f; };
-    bf16x8 vr[NKS];
+    constexpr int NVR = FIXED ? KSH : NKS;  // fragments read: FIXED needs no tile max
+    bf16x8 vr[NVR];
 #pragma unroll
-    for (int f = 0; f < NKS; ++f) vr[f] = frag_tr<DV>(sm.vs, dvb * 32, ksof(f) * 16);
+    for (int f = 0; f < NVR; ++f) vr[f] = frag_tr<DV>(sm.vs, dvb * 32, ksof(f) * 16);
     // keys at or past T (a partial last tile only) stay out of the max and
     // give E = 0
     const auto tilt = [&](auto partial) __attribute__((always_inline)) {
     constexpr bool PART = decltype(partial)::value;
-    float vmax = -INFINITY;
+    if constexpr (FIXED) {
+      gj = 1.f;
+      rose = false;
+    } else {
+      float vmax = -INFINITY;
 #pragma unroll
-    for (int f = 0; f < NKS; ++f) {
+      for (int f = 0; f < NKS; ++f) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (!PART || t0 + e_pos(ksof(f) * 16 + hl * 8 + u) < T) vmax = fmaxf(vmax, (float)vr[f][u]);
+        for (int u = 0; u < 8; ++u)
+          if (!PART || t0 + e_pos(ksof(f) * 16 + hl * 8 + u) < T) vmax = fmaxf(vmax, (float)vr[f][u]);
+      }
+      vmax = fmaxf(vmax, other_half(vmax));  // lanes n and n + 32 hold the same channel
+      const float mx = vmax * blj;
+      const float cnew = (mx > cj + kColLag) ? mx : cj;
+      gj = exp2_hw(cj - cnew);
+      rose = __any(cnew != cj);
+      cj = cnew;
     }
-    vmax = fmaxf(vmax, other_half(vmax));  // lanes n and n + 32 hold the same channel
-    const float mx = vmax * blj;
-    const float cnew = (mx > cj + kColLag) ? mx : cj;
-    const float sh = kBias - cnew;
-    gj = exp2_hw(cj - cnew);
-    rose = __any(cnew != cj);
-    cj = cnew;
+    const float sh = kBias - cj;
 #pragma unroll
     for (int kk = 0; kk < KSH; ++kk) {
       const int ks = ksof(kk);
@@ -776,7 +784,226 @@ __global__ __launch_bounds__(NTH) void prefix_kernel(const float* __restrict__ o
   }
 }
 
-template <int PRIOR, bool OUT, int CH, int NSUB>
+// Own state [S | z | c] of one segment, linear prior, with the four waves of
+// the workgroup independent of each other: wave w takes the segment's 32-key
+// tiles w, w + 4, w + 8, ..., streams each into a double-buffered tile pair of
+// its own in LDS by direct buffer loads (no workgroup barrier inside the
+// loop), and accumulates its own S^T (64 x 64 fp32), its own sum of phi(k)
+// (a matrix-core product with rows of ones, from the same rounded phi(k) as
+// S: rows 0-15 of one accumulator sum d_k 0-31, rows 16-31 sum d_k 32-63)
+// and its own lazily raised per-channel shift.  The four partial states
+// meet in LDS at the end, each rescaled to the largest of the four shifts.
+// The sum over a segment does not depend on the order of its keys, so the
+// result is the state the sequential scan leaves, up to rounding.
+constexpr int SKT = 32;  // keys per wave tile
+struct StateTiles {      // one buffer of one wave
+  bf16 k[SKT * DK];      // K [key][d_k], swizzled (see swz_off)
+  bf16 v[SKT * DV];      // V [key][d_v], swizzled
+};
+struct StatePart {       // one wave's state after its tiles
+  float s[DV * DK];      // S [d_v][d_k]
+  float z[DK];
+  float c[DV];
+};
+union StateSmem {
+  StateTiles t[4][2];
+  StatePart p[4];
+};
+
+__global__ __launch_bounds__(NTH, 2) void linear_state_kernel(const bf16* __restrict__ K,
+                                                           const bf16* __restrict__ V,
+                                                           const float* __restrict__ beta,
+                                                           float* __restrict__ ws, int H, int T,
+                                                           int nseg, int segt) {
+  static_assert(DK == 64 && DV == 64, "two 32-wide blocks of each");
+  __shared__ __align__(16) StateSmem sm;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, hl = lane >> 5;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const int seg = blockIdx.x % nseg;
+  const int bh = blockIdx.x / nseg;
+  const int h = bh % H;
+  const bf16* Kh = K + (size_t)bh * T * DK;
+  const bf16* Vh = V + (size_t)bh * T * DV;
+  const int tbeg = seg * segt, tend = min(tbeg + segt, T);
+
+  // lane offsets of the direct loads: LDS slot i * 64 + lane of a tile is
+  // row i * 8 + lane / 8, position lane % 8, which holds 16-byte chunk
+  // (lane % 8) ^ swz(row) of that row
+  unsigned goff[SKT / 8];
+#pragma unroll
+  for (int i = 0; i < SKT / 8; ++i) {
+    const int r = i * 8 + (lane >> 3);
+    goff[i] = (unsigned)(r * DK * 2 + (((lane & 7) ^ swz<DK>(r)) << 4));
+  }
+  const unsigned lds0 = lds_addr(&sm) + (unsigned)wave_s * 2u * (unsigned)sizeof(StateTiles);
+  const auto issue = [&](int t0, int b) {
+    // rows at or past the segment's end load as zeros
+    const unsigned bytes = (unsigned)(min(tend, t0 + SKT) - t0) * DK * 2u;
+    const rsrc_t rk = buffer_rsrc(Kh + (size_t)t0 * DK, bytes);
+    const rsrc_t rv = buffer_rsrc(Vh + (size_t)t0 * DV, bytes);
+    const unsigned lk = lds0 + (unsigned)b * (unsigned)sizeof(StateTiles);
+    const unsigned lv = lk + (unsigned)(SKT * DK * 2);
+#pragma unroll
+    for (int i = 0; i < SKT / 8; ++i) {
+      dma16b(rk, goff[i], lk + i * 1024u);
+      dma16b(rv, goff[i], lv + i * 1024u);
+    }
+  };
+
+  float blj[2], cj[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) blj[cb] = beta[h * DV + cb * 32 + n] * kLog2e;
+  f32x16 st[2][2], zacc = f32x16{};
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) st[a][b] = f32x16{};
+  // A operand rows 0-15 (kb = 0) or 16-31 (kb = 1) all ones, the rest zero
+  bf16x8 ones[2];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    ones[0][u] = (bf16)(n < 16 ? 1.f : 0.f);
+    ones[1][u] = (bf16)(n < 16 ? 0.f : 1.f);
+  }
+
+  // (t0 is held wave-uniform, so the partial last tile is a branch of its own)
+  if (tbeg + wave_s * SKT < tend) issue(tbeg + wave_s * SKT, 0);
+  int it = 0;
+  for (int t0 = tbeg + wave_s * SKT; t0 < tend; t0 += 4 * SKT, ++it) {
+    const int b = it & 1;
+    // the other buffer was read (and its reads waited for) last iteration
+    if (t0 + 4 * SKT < tend) {
+      issue(t0 + 4 * SKT, b ^ 1);
+      static_assert(2 * (SKT / 8) == 8, "loads per tile");
+      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");  // this tile's loads done, the next one's in flight
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    const StateTiles& tl = sm.t[wave][b];
+    const auto tile = [&](auto partial) __attribute__((always_inline)) {
+    constexpr bool part = decltype(partial)::value;
+    // key of element u of a fragment at k-step ks (frag_tr's order)
+    const auto valid = [&](int ks, int u) { return t0 + ppos(ks * 16 + hl * 8 + u) < tend; };
+
+    // phi(K)^T fragments (B operand: column d_k, keys), rounded to bf16;
+    // keys past the segment give 0
+    bf16x8 kf[2][2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8 raw = frag_tr<DK>(tl.k, kb * 32, ks * 16);
+#pragma unroll
+        for (int u = 0; u < 8; u += 2) {
+          float f0 = phi((float)raw[u]), f1 = phi((float)raw[u + 1]);
+          if (part) {
+            f0 = valid(ks, u) ? f0 : 0.f;
+            f1 = valid(ks, u + 1) ? f1 : 0.f;
+          }
+          const bf16x2 p2 = to_bf16x2(f0, f1);
+          kf[kb][ks][u] = p2[0];
+          kf[kb][ks][u + 1] = p2[1];
+        }
+      }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        zacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones[kb], kf[kb][ks], zacc, 0, 0, 0);
+
+    // per channel block: the tile's column max, the lazy shift, the tilt as
+    // E^T fragments (A operand: channel, keys) in bf16 hi + lo, and the update
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      float x[2][8];
+      float vmax = -INFINITY;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x8 raw = frag_tr<DV>(tl.v, cb * 32, ks * 16);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          x[ks][u] = (float)raw[u];
+          if (part && !valid(ks, u)) x[ks][u] = -INFINITY;
+          vmax = fmaxf(vmax, x[ks][u]);
+        }
+      }
+      vmax = fmaxf(vmax, other_half(vmax));
+      const float mx = vmax * blj[cb];
+      const float cnew = (mx > cj[cb] + kColLag) ? mx : cj[cb];
+      if (__any(cnew != cj[cb])) {
+        // S^T rows of this block are channels: lane (i, hl) holds row
+        // 8 (i / 4) + 4 hl + i % 4, whose factor sits in lane of that index
+        const float g = exp2_hw(cj[cb] - cnew);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float gi = __shfl(g, (i >> 2) * 8 + hl * 4 + (i & 3));
+          st[cb][0][i] *= gi;
+          st[cb][1][i] *= gi;
+        }
+      }
+      cj[cb] = cnew;
+      const float sh = kBias - cnew;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        bf16x8 eh, el;
+#pragma unroll
+        for (int u = 0; u < 8; u += 2) {
+          const float e0 = exp2_hw(fmaf(x[ks][u], blj[cb], sh));
+          const float e1 = exp2_hw(fmaf(x[ks][u + 1], blj[cb], sh));
+          const bf16x2 h2 = to_bf16x2(e0, e1);
+          const bf16x2 l2 = to_bf16x2(e0 - (float)h2[0], e1 - (float)h2[1]);
+          eh[u] = h2[0];
+          eh[u + 1] = h2[1];
+          el[u] = l2[0];
+          el[u + 1] = l2[1];
+        }
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          st[cb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eh, kf[kb][ks], st[cb][kb], 0, 0, 0);
+          st[cb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el, kf[kb][ks], st[cb][kb], 0, 0, 0);
+        }
+      }
+    }
+    };
+    if (t0 + SKT <= tend) tile(std::false_type());
+    else tile(std::true_type());
+  }
+
+  // ---- the four partial states meet in LDS (over the tiles: every wave's
+  // reads of them are done after the barrier)
+  __syncthreads();
+  StatePart& P = sm.p[wave];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        P.s[(cb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3)) * DK + kb * 32 + n] = st[cb][kb][i];
+  if (hl == 0) {
+    P.z[n] = zacc[0];        // row 4 hl, below 16
+    P.z[32 + n] = zacc[8];   // row 16 + 4 hl
+    P.c[n] = cj[0];
+    P.c[32 + n] = cj[1];
+  }
+  __syncthreads();
+  float* S = ws + ((size_t)bh * nseg + seg) * STATE;
+  for (int e = tid; e < DV * DK; e += NTH) {
+    const int j = e / DK;
+    const float C = fmaxf(fmaxf(sm.p[0].c[j], sm.p[1].c[j]), fmaxf(sm.p[2].c[j], sm.p[3].c[j]));
+    float acc = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) acc += sm.p[w].s[e] * exp2_hw(sm.p[w].c[j] - C);
+    S[e] = acc;
+  }
+  if (tid < DK) S[DV * DK + tid] = (sm.p[0].z[tid] + sm.p[1].z[tid]) + (sm.p[2].z[tid] + sm.p[3].z[tid]);
+  if (tid < DV)
+    S[DV * DK + DK + tid] =
+        fmaxf(fmaxf(sm.p[0].c[tid], sm.p[1].c[tid]), fmaxf(sm.p[2].c[tid], sm.p[3].c[tid]));
+}
+
+template <int PRIOR, bool OUT, int CH, int NSUB, bool FIXED>
 __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
                                                      const bf16* __restrict__ K,
                                                      const bf16* __restrict__ V,
@@ -818,22 +1045,31 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   ChunkRegs<CH> cr;
   fetch_chunk<PRIOR, OUT, CH>(cr, Qh, Kh, Vh, Gh, tbeg, T);
 
+  // FIXED: the shift is the segment's own (left by the state pass with its
+  // own state), raised to the entering state's where that one is larger
+  const float* cown = wsh + (size_t)seg * SF + DV * DK + DK;
+  if (FIXED) cj = cown[ch];
   if (OUT && seg > 0) {
     // entering state, left by the prefix kernel in the second half of ws
     const float* S = wsh + (size_t)gridDim.x * SF + (size_t)seg * SF;
     if (tid < DK) sm.z[tid] = S[DV * DK + tid];
-    cj = S[DV * DK + DK + ch];
+    cj = FIXED ? fmaxf(cj, S[DV * DK + DK + ch]) : S[DV * DK + DK + ch];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
       const int col = sub * 32 + (lane & 31);
-      st[i] = S[row * DK + col];
+      float v = S[row * DK + col];
+      if (FIXED) {
+        const float ce = S[DV * DK + DK + row];
+        v *= exp2_hw(ce - fmaxf(ce, cown[row]));
+      }
+      st[i] = v;
     }
     __syncthreads();
   }
 
   for (int t0 = tbeg; t0 < tend; t0 += CH)
-    scan_chunk<PRIOR, OUT, CH, NSUB>(sm, st, cj, blj, ldc, cr, Qh, Kh, Vh, Gh, Oh, t0,
+    scan_chunk<PRIOR, OUT, CH, NSUB, FIXED>(sm, st, cj, blj, ldc, cr, Qh, Kh, Vh, Gh, Oh, t0,
                                      t0 + CH < tend ? t0 + CH : T, T);
 
   if (!OUT) {
@@ -892,8 +1128,12 @@ hipError_t launch_scan(const void* Q, const void* K, const void* V, const float*
   const bf16* v = reinterpret_cast<const bf16*>(V);
   hipError_t e = hipSuccess;
   if (nseg > 1) {
-    hipLaunchKernelGGL((linear_kernel<PRIOR, false, CH, NSUB>), dim3((unsigned)(nbh * nseg)),
-                       dim3(NTH), 0, stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
+    if constexpr (PRIOR == kElu)
+      hipLaunchKernelGGL(linear_state_kernel, dim3((unsigned)(nbh * nseg)), dim3(NTH), 0, stream,
+                         k, v, beta, ws, H, T, nseg, segc * CH);
+    else
+      hipLaunchKernelGGL((linear_kernel<PRIOR, false, CH, NSUB, false>), dim3((unsigned)(nbh * nseg)),
+                         dim3(NTH), 0, stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
     e = hipGetLastError();
     if (e == hipSuccess) {
       hipLaunchKernelGGL(prefix_kernel<PRIOR>,
@@ -903,8 +1143,13 @@ hipError_t launch_scan(const void* Q, const void* K, const void* V, const float*
     }
   }
   if (e == hipSuccess) {
-    hipLaunchKernelGGL((linear_kernel<PRIOR, true, CH, NSUB>), dim3((unsigned)(nbh * nseg)),
-                       dim3(NTH), 0, stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
+    // with segment states, each segment reads at its own final shift
+    if (nseg > 1)
+      hipLaunchKernelGGL((linear_kernel<PRIOR, true, CH, NSUB, true>), dim3((unsigned)(nbh * nseg)),
+                         dim3(NTH), 0, stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
+    else
+      hipLaunchKernelGGL((linear_kernel<PRIOR, true, CH, NSUB, false>), dim3((unsigned)(nbh * nseg)),
+                         dim3(NTH), 0, stream, q, k, v, G, beta, out, ws, H, T, nseg, segc);
     e = hipGetLastError();
   }
   return e;

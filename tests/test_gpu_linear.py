@@ -107,6 +107,26 @@ def test_linear_underflow_repair(fem):
     check(got, ref(q, k, v, b), TOL, "linear underflow repair")
 
 
+def test_linear_segment_end_spike(fem):
+    """Values far above the rest of their segment at its last key: the read
+    of a segment shifts by the segment's own maximum, so every earlier row of
+    those channels underflows and is recomputed exactly; rows of other
+    channels and heads are unaffected."""
+    say("linear spikes at segment ends: B2 H64 T1024 (4 segments of 256), beta=16 on 4 channels")
+    q, k, v, b = inputs.draw(4350, 2, 64, 1024, 64, dtype="bf16", beta_lo=0.1, beta_hi=4.0)
+    v = v.float()
+    v[0, 0, :, :4] = -5.0
+    v[0, 0, 255, :4] = 5.0
+    v[0, 0, 767, :4] = 5.0
+    v = v.to(torch.bfloat16)
+    b[0, :4] = 16.0
+    got = run(fem, q, k, v, b)
+    for bb, hh in [(0, 0), (0, 1), (1, 0), (1, 63)]:
+        want = ref(q[bb:bb + 1, hh:hh + 1], k[bb:bb + 1, hh:hh + 1], v[bb:bb + 1, hh:hh + 1],
+                   b[hh:hh + 1])
+        check(got[bb:bb + 1, hh:hh + 1], want, TOL, f"segment-end spikes (b={bb}, h={hh})")
+
+
 def test_linear_deterministic(fem):
     say("linear determinism: B2 H2 T1500")
     q, k, v, b = inputs.draw(4400, 2, 2, 1500, 64, dtype="bf16")
