@@ -58,6 +58,7 @@ constexpr int GCH = 64;          // tokens per chunk of the GLA prior
 constexpr int NTH = 256;         // 4 waves
 constexpr int ROW = 64 + 8;      // padded bf16 row (64 values + 16 B)
 constexpr int SROW = DK + 8;     // padded S^T row (bf16)
+constexpr int OBR = 32 + 4;      // padded row of a staged output block (floats)
 constexpr int STATE = DV * DK + DK + DV;  // floats per saved segment state
 constexpr int kElu = 0, kGla = 1;         // the prior
 // GLA adds the segment's total log-decay per key channel
@@ -117,6 +118,10 @@ struct LinSmem {
   float bl[DV];               // beta log2 e
   float inv[DV];
   float z[DK];                // sum of phi(k) over earlier tiles
+  // the vector whose product with phi(q) is the inter-chunk normaliser (z,
+  // or e^R z for GLA) as bf16 hi + lo: the A operand (all rows equal) of
+  // the matrix-core row sums that form the normaliser
+  bf16 zh[DK], zl[DK];
   float zc[4 * DK];           // partial sums of phi(k) over this tile (four row quarters)
 };
 
@@ -134,6 +139,10 @@ struct ScanSmem : LinSmem<CH, NSUB> {
   // prior, one chunk per tile of at most 64 tokens): [block][k-step][hi, lo][lane]
   static constexpr bool SPLIT_E = NSUB == 1 && CH <= 64;
   bf16x8 ex[SPLIT_E ? (DV / 32) * (CH / 16) * 2 * 64 : 1];
+  // tiles of at most 64 tokens: each wave's 32 x 32 block of outputs, rows
+  // padded to OBR floats, so that the stores leave in whole 128-byte rows
+  static constexpr bool STAGE_OUT = CH <= 64;
+  __align__(16) float ob[STAGE_OUT ? 4 * 32 * OBR : 1];
   __device__ float* gb() { return nullptr; }
   __device__ float* gbq() { return nullptr; }
   __device__ float* gzr() { return nullptr; }
@@ -145,6 +154,7 @@ struct ScanSmem<kGla, GCH, 1> : LinSmem<GCH, 1> {
   // workgroup per CU; splitting the read's tilt alone measured slower)
   static constexpr bool SPLIT_E = false;
   bf16x8 ex[1];
+  static constexpr bool STAGE_OUT = false;
   GlaSmem gla;
   __device__ float* gb() { return gla.b; }
   __device__ float* gbq() { return gla.bq; }
@@ -156,6 +166,14 @@ struct ScanSmem<kGla, GCH, 1> : LinSmem<GCH, 1> {
 __device__ __forceinline__ float swz_elem(const bf16* t, int row, int col) {
   return (float)*reinterpret_cast<const bf16*>(reinterpret_cast<const char*>(t) +
                                                swz_off<DK>(row, col >> 3) + (col & 7) * 2);
+}
+
+// Entry i of the inter-chunk normaliser vector, as bf16 hi + lo.
+template <int CH, int NSUB>
+__device__ __forceinline__ void put_zn(LinSmem<CH, NSUB>& sm, int i, float v) {
+  const bf16 hi = (bf16)v;
+  sm.zh[i] = hi;
+  sm.zl[i] = (bf16)(v - (float)hi);
 }
 
 // Key r of a chunk -> position inside an MFMA-ordered row (see the softmax
@@ -342,7 +360,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
   static_assert(CH == 32 || CH == 64 || CH == 128, "tile length");
   static_assert(NSUB == 1 || (CH == 32 && NSUB == 2), "two 16-token chunks per 32-token tile");
   static_assert(PRIOR != kGla || (CH == GCH && NSUB == 1), "GLA: 64-token chunks");
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, hl = lane >> 5;
   const int dvb = wave >> 1, sub = wave & 1;
   const int ch = dvb * 32 + n;
@@ -534,7 +552,11 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
     sm.zc[q4 * DK + dkc] = s;
     // GLA: the inter-chunk normaliser reads e^{R} z
     if (PRIOR == kGla && q4 == 0)
-      sm.gzr()[dkc] = sm.z[dkc] * exp2_hw(sm.gb()[(CH / 2 - 1) * DK + dkc] * kLog2e);
+    {
+      const float zr = sm.z[dkc] * exp2_hw(sm.gb()[(CH / 2 - 1) * DK + dkc] * kLog2e);
+      sm.gzr()[dkc] = zr;
+      put_zn(sm, dkc, zr);
+    }
   }
 
   // ---- rescale the state rows (d_v) when a shift of the block rose
@@ -590,6 +612,10 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
       bf16x8 pf[NKS];
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) pf[ks] = bf16x8{};
+      // the normaliser: with one chunk per tile, on the matrix cores (every
+      // row of dacc sums the rounded A^T over keys plus zn^T phi(q)); with
+      // two, in the vector units (below)
+      constexpr bool MDEN = NSUB == 1;
       float den = 0.f;
 #pragma unroll
       for (int kb = 0; kb < NQB; ++kb) {
@@ -620,7 +646,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
               const bf16x2 p2 = to_bf16x2(in0 ? at[i0] : 0.f, in1 ? at[i1] : 0.f);
               pf[ks][u] = p2[0];
               pf[ks][u + 1] = p2[1];
-              den = add_bf16x2(p2, den);
+              if (!MDEN) den = add_bf16x2(p2, den);
             }
           }
         };
@@ -631,12 +657,16 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
       // start of the query's chunk); the inter-chunk normaliser phi(q)^T z
       // (this lane's half of d_k) reuses the phi(Q) fragments, with four
       // partial sums
-      f32x16 num = f32x16{};
+      f32x16 num = f32x16{}, dacc = f32x16{};
+      bf16x8 ones;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) ones[u] = (bf16)1.f;
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
         if ((ks >> 1) > qb) continue;
         num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eh[ks], pf[ks], num, 0, 0, 0);
         num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el[ks], pf[ks], num, 0, 0, 0);
+        if (MDEN) dacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[ks], dacc, 0, 0, 0);
       }
       const int soff = (dvb * 32 + n) * SROW + hl * 8;
       float dz[4] = {0.f, 0.f, 0.f, 0.f};
@@ -652,6 +682,13 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
           if (!mine) b = bf16x8{};
           num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
           num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b, num, 0, 0, 0);
+          if (MDEN) {
+            const bf16x8 zh = *reinterpret_cast<const bf16x8*>(sm.zh + ks * 16 + hl * 8);
+            const bf16x8 zl = *reinterpret_cast<const bf16x8*>(sm.zl + ks * 16 + hl * 8);
+            dacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zh, b, dacc, 0, 0, 0);
+            dacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zl, b, dacc, 0, 0, 0);
+            continue;
+          }
           const float* zz = PRIOR == kGla ? sm.gzr() : sm.z;
           f32x4 z0 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8);
           f32x4 z1 = *reinterpret_cast<const f32x4*>(zz + ks * 16 + hl * 8 + 4);
@@ -668,8 +705,12 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
           }
         }
       }
-      den += (dz[0] + dz[1]) + (dz[2] + dz[3]);
-      den += other_half(den);
+      if (MDEN) {
+        den = dacc[0];
+      } else {
+        den += (dz[0] + dz[1]) + (dz[2] + dz[3]);
+        den += other_half(den);
+      }
       // epilogue: F = (log2(num / den) + c - kBias) / (beta log2 e), one
       // logarithm per output.  num / den is a weighted mean of E (at most
       // 2^(kColLag + kBias)); it is flagged below when it or num could have
@@ -688,7 +729,20 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
           o[e] = fmaf(log2_hw(a * rd), iv[e], ci[e]);
           amin = fminf(amin, a);
         }
-        if (tq < T) *reinterpret_cast<f32x4*>(Oh + (size_t)tq * DV + ch0) = o;
+        if constexpr (ScanSmem<PRIOR, CH, NSUB>::STAGE_OUT)
+          *reinterpret_cast<f32x4*>(sm.ob + (wave * 32 + n) * OBR + g4 * 8 + hl * 4) = o;
+        else if (tq < T)
+          *reinterpret_cast<f32x4*>(Oh + (size_t)tq * DV + ch0) = o;
+      }
+      if constexpr (ScanSmem<PRIOR, CH, NSUB>::STAGE_OUT) {
+        // the wave's block back by rows: 8 lanes cover the 32 channels of a row
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = i * 8 + (lane >> 3), c4 = (lane & 7) * 4;
+          const f32x4 x = *reinterpret_cast<const f32x4*>(sm.ob + (wave * 32 + r) * OBR + c4);
+          const int t = t0 + qb * 32 + r;
+          if (t < T) *reinterpret_cast<f32x4*>(Oh + (size_t)t * DV + dvb * 32 + c4) = x;
+        }
       }
       // outputs whose numerator underflowed (rare): recomputed exactly below
       uint32_t flags = 0;
@@ -697,6 +751,8 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
 #pragma unroll
         for (int i = 0; i < 16; ++i)
           if (low(num[i]) && tq < T) flags |= 1u << i;
+        // the repaired values overwrite the stores above
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       }
       while (true) {
         const uint64_t who = __ballot(flags != 0);
@@ -742,6 +798,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
       ldc += blast;  // the segment's total log-decay of channel tid
     } else {
       sm.z[tid] += add;
+      put_zn(sm, tid, sm.z[tid]);
     }
   }
 }
@@ -764,23 +821,36 @@ __global__ __launch_bounds__(NTH) void prefix_kernel(const float* __restrict__ o
   const int j = e < DV * DK ? e / DK : (e >= DV * DK + DK ? e - DV * DK - DK : -1);
   // key channel of an S or z entry (decay), -1 for a shift entry
   const int kc = e < DV * DK ? e % DK : (e < DV * DK + DK ? e - DV * DK : -1);
+  // segments in batches of PB: every load of a batch is issued before the
+  // batch's (sequential) combination
+  constexpr int PB = 8;
   float acc = 0.f, C = -INFINITY;
-  for (int sg = 0; sg + 1 < nseg; ++sg) {
-    const float val = ob[(size_t)sg * SF + e];
-    const float dcy =
-        (PRIOR == kGla && kc >= 0) ? exp2_hw(ob[(size_t)sg * SF + STATE + kc] * kLog2e) : 1.f;
-    if (e < DV * DK) {
-      const float cs = ob[(size_t)sg * SF + DV * DK + DK + j];
-      const float Cn = fmaxf(C, cs);
-      acc = acc * dcy * exp2_hw(C - Cn) + val * exp2_hw(cs - Cn);
-      C = Cn;
-    } else if (e < DV * DK + DK) {
-      acc = acc * dcy + val;
-    } else {
-      acc = fmaxf(C, val);
-      C = acc;
+  for (int s0 = 0; s0 + 1 < nseg; s0 += PB) {
+    float val[PB], cs[PB], lg[PB];
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const size_t o = (size_t)min(s0 + u, nseg - 2) * SF;  // (past the end: unused)
+      val[u] = ob[o + e];
+      cs[u] = j >= 0 ? ob[o + DV * DK + DK + j] : 0.f;
+      lg[u] = (PRIOR == kGla && kc >= 0) ? ob[o + STATE + kc] : 0.f;
     }
-    pb[(size_t)(sg + 1) * SF + e] = acc;
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const int sg = s0 + u;
+      if (sg + 1 >= nseg) break;
+      const float dcy = (PRIOR == kGla && kc >= 0) ? exp2_hw(lg[u] * kLog2e) : 1.f;
+      if (e < DV * DK) {
+        const float Cn = fmaxf(C, cs[u]);
+        acc = acc * dcy * exp2_hw(C - Cn) + val[u] * exp2_hw(cs[u] - Cn);
+        C = Cn;
+      } else if (e < DV * DK + DK) {
+        acc = acc * dcy + val[u];
+      } else {
+        acc = fmaxf(C, val[u]);
+        C = acc;
+      }
+      pb[(size_t)(sg + 1) * SF + e] = acc;
+    }
   }
 }
 
@@ -1004,7 +1074,7 @@ __global__ __launch_bounds__(NTH, 2) void linear_state_kernel(const bf16* __rest
 }
 
 template <int PRIOR, bool OUT, int CH, int NSUB, bool FIXED>
-__global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
+__global__ __launch_bounds__(NTH, PRIOR == kElu && CH <= 64 ? 2 : 1) void linear_kernel(const bf16* __restrict__ Q,
                                                      const bf16* __restrict__ K,
                                                      const bf16* __restrict__ V,
                                                      const float* __restrict__ G,
@@ -1033,7 +1103,10 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
     sm.bl[tid] = bl;
     sm.inv[tid] = 1.f / bl;
   }
-  if (tid < DK) sm.z[tid] = 0.f;
+  if (tid < DK) {
+    sm.z[tid] = 0.f;
+    put_zn(sm, tid, 0.f);
+  }
   f32x16 st = f32x16{};
   const float blj = beta[h * DV + ch] * kLog2e;
   float cj = -INFINITY;  // running shift of channel ch
@@ -1052,7 +1125,10 @@ __global__ __launch_bounds__(NTH) void linear_kernel(const bf16* __restrict__ Q,
   if (OUT && seg > 0) {
     // entering state, left by the prefix kernel in the second half of ws
     const float* S = wsh + (size_t)gridDim.x * SF + (size_t)seg * SF;
-    if (tid < DK) sm.z[tid] = S[DV * DK + tid];
+    if (tid < DK) {
+      sm.z[tid] = S[DV * DK + tid];
+      put_zn(sm, tid, sm.z[tid]);
+    }
     cj = FIXED ? fmaxf(cj, S[DV * DK + DK + ch]) : S[DV * DK + DK + ch];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
