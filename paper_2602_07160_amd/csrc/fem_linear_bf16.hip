@@ -1074,7 +1074,7 @@ __global__ __launch_bounds__(NTH, 2) void linear_state_kernel(const bf16* __rest
 }
 
 template <int PRIOR, bool OUT, int CH, int NSUB, bool FIXED>
-__global__ __launch_bounds__(NTH, PRIOR == kElu && CH <= 64 ? 2 : 1) void linear_kernel(const bf16* __restrict__ Q,
+__global__ __launch_bounds__(NTH, (PRIOR == kElu || FIXED) && CH <= 64 ? 2 : 1) void linear_kernel(const bf16* __restrict__ Q,
                                                      const bf16* __restrict__ K,
                                                      const bf16* __restrict__ V,
                                                      const float* __restrict__ G,
