@@ -127,6 +127,19 @@ def test_linear_segment_end_spike(fem):
         check(got[bb:bb + 1, hh:hh + 1], want, TOL, f"segment-end spikes (b={bb}, h={hh})")
 
 
+def test_linear_one_segment_per_head(fem):
+    """With B*H large enough that every head is one segment, the scan runs
+    without segment states and raises its shift lazily chunk by chunk; a
+    sample of heads is compared with the oracle over every row."""
+    say("linear one segment per head: B4 H128 T700 d64 (no state pass), 4 heads checked")
+    q, k, v, b = inputs.draw(4360, 4, 128, 700, 64, dtype="bf16", beta_lo=0.1, beta_hi=8.0)
+    got = run(fem, q, k, v, b)
+    for bb, hh in [(0, 0), (1, 37), (2, 90), (3, 127)]:
+        want = ref(q[bb:bb + 1, hh:hh + 1], k[bb:bb + 1, hh:hh + 1], v[bb:bb + 1, hh:hh + 1],
+                   b[hh:hh + 1])
+        check(got[bb:bb + 1, hh:hh + 1], want, TOL, f"one segment per head (b={bb}, h={hh})")
+
+
 def test_linear_deterministic(fem):
     say("linear determinism: B2 H2 T1500")
     q, k, v, b = inputs.draw(4400, 2, 2, 1500, 64, dtype="bf16")
