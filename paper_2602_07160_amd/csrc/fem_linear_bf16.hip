@@ -434,7 +434,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         const float b = sm.gb()[r * DK + c8 + u];
         const float R = sm.gb()[(CH / 2 - 1) * DK + c8 + u];
         const float bl = sm.gb()[(CH - 1) * DK + c8 + u];
-        pk[u] = (bf16)(kx[u] * exp2_hw((R - b) * kLog2e) * okf);
+        if (OUT) pk[u] = (bf16)(kx[u] * exp2_hw((R - b) * kLog2e) * okf);
         if (OUT) pq[u] = (bf16)(qx[u] * exp2_hw((b - R) * kLog2e) * okf);
         pu[u] = (bf16)(kx[u] * exp2_hw((bl - b) * kLog2e) * okf);
       }
@@ -451,7 +451,9 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         }
       }
     }
-    *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.fk) + swz_off<DK>(r, c8 >> 3)) = pk;
+    // (the state pass of the GLA prior reads only k~ e^{B_last - B}, above)
+    if (OUT || PRIOR != kGla)
+      *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.fk) + swz_off<DK>(r, c8 >> 3)) = pk;
     *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.vs) + swz_off<DV>(r, c8 >> 3)) = cr.v[i];
     if (OUT) *reinterpret_cast<bf16x8*>(sm.fq + r * ROW + c8) = pq;
   }
