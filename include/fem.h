@@ -148,7 +148,7 @@ int fem_softmax_fwd_ex(const void* Q, const void* K, const void* V,
  *
  * fp32 arithmetic with a per-channel joint log-sum-exp (no shared shift).
  * The keys are split over workgroups: S = ceil(L / (64 n)) splits of n =
- * ceil(ceil(L / 64) / s0) key blocks of 64 each, s0 = min(ceil(1024 / (B H)),
+ * ceil(ceil(L / 64) / s0) key blocks of 64 each, s0 = min(ceil(256 / (B H)),
  * ceil(L / 64)).  Their partial results need a workspace of
  *
  *   fem_softmax_decode_workspace_bytes(B, H, L, d_qk, d_v) = 8 * B * H * S * (d_v + 1)

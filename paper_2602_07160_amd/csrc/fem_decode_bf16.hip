@@ -206,10 +206,12 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(
   }
 }
 
-// Split count of a step: enough (b, h, split) workgroups for about four per
+// Split count of a step: enough (b, h, split) workgroups for about one per
 // compute unit of a 256-CU device, each split a whole number of key blocks.
+// (At B8 H16 L4096 d128: one per CU 45.8 us, two 47.7, three 48.3, four
+// 51.3; fewer, longer splits also shrink the merge.)
 // A function of the sizes only, so that the workspace query needs no device.
-constexpr int kTargetWorkgroups = 1024;
+constexpr int kTargetWorkgroups = 256;
 
 void decode_splits(int B, int H, int L, int* nsplit_out, int* bps_out) {
   const int nbh = B * H;

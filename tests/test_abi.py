@@ -180,7 +180,7 @@ def cdiv(a, b):
 
 def want_decode(B, H, L, dqk, dv):
     blocks = cdiv(L, 64)
-    s0 = max(1, min(cdiv(1024, B * H), blocks))
+    s0 = max(1, min(cdiv(256, B * H), blocks))
     n = cdiv(blocks, s0)
     return 8 * B * H * cdiv(blocks, n) * (dv + 1)
 
