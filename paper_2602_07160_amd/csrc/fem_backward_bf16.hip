@@ -742,12 +742,13 @@ __global__ __launch_bounds__(kThreads) void bwd_prepk_kernel(
     float* __restrict__ cg, float* __restrict__ splitf, bf16* __restrict__ yh,
     bf16* __restrict__ yl, bf16* __restrict__ wh, bf16* __restrict__ wl,
     float* __restrict__ cst, int* __restrict__ flag, int H, int T, int ntile) {
-  __shared__ float c[D], split[D], bl[D];
+  __shared__ float c[D], split[D], bl[D], ib[D];
   constexpr int CPR = D / 8;
   static_assert(kThreads % CPR == 0 && CPR <= 64, "a row's threads share a wave");
   const int kb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
   const int k0 = kb * kTile;
   channel_consts<D>(beta, vmx, vmn, bh, h, ntile, c, split, bl, kb == 0, cg, splitf, flag);
+  for (int j = threadIdx.x; j < D; j += kThreads) ib[j] = 1.f / beta[h * D + j];
   __syncthreads();
   const size_t base = (size_t)bh * T * D;
   const size_t rows = ((size_t)bh * ntile + kb) * kTile;  // first row in the padded [., D] arrays
@@ -781,7 +782,7 @@ __global__ __launch_bounds__(kThreads) void bwd_prepk_kernel(
       split_bf16(y, a, b);
       hi[u] = a;
       lo[u] = b;
-      const float w = on ? g4[u >> 2][u & 3] / beta[h * D + j] : 0.f;
+      const float w = on ? g4[u >> 2][u & 3] * ib[j] : 0.f;
       const float x = on ? c[j] - bl[j] * f4[u >> 2][u & 3] : 0.f;  // log2 U
       const float wu = w * exp2_hw(fminf(x, kGuardU));
       if (!(x <= kGuardU && fabsf(wu) < kGuardW)) bad = true;
@@ -1017,11 +1018,12 @@ __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
     int* __restrict__ flag, int H, int T, int ntile) {
   constexpr int CPR = D / 8, RG = kThreads / CPR;
   static_assert(kThreads % CPR == 0 && CPR <= 64, "a row's threads share a wave");
-  __shared__ float c[D], split[D], bl[D], part[RG][D];
+  __shared__ float c[D], split[D], bl[D], ib[D], part[RG][D];
   const int qb = blockIdx.x % ntile, bh = blockIdx.x / ntile, h = bh % H;
   const int q0 = qb * kTile;
   for (int j = threadIdx.x; j < D; j += kThreads) {
     bl[j] = beta[h * D + j] * kLog2e;
+    ib[j] = 1.f / beta[h * D + j];
     split[j] = splitf[bh * D + j];
     c[j] = cg[bh * D + j];
   }
@@ -1052,7 +1054,7 @@ __global__ __launch_bounds__(kThreads) void bwd_prepq_kernel(
       // a wide channel contributes nothing here (W U' = 0, no G F term)
       const bool sp = split[j] == kSplitForm, on = live && split[j] != kWide;
       const float g = on ? g4[u >> 2][u & 3] : 0.f, f = f4[u >> 2][u & 3], sa = z4[u >> 2][u & 3];
-      const float rb = 1.f / beta[h * D + j], w = g * rb;
+      const float rb = ib[j], w = g * rb;
       const float x = on ? c[j] - bl[j] * f : 0.f;  // log2 U
       float lz = 0.f;                               // ln(Z/P): F = F^ + ln(Z/P)/beta
       if (on) {
