@@ -672,30 +672,48 @@ __global__ __launch_bounds__(kThreads) void bwd_vstats_kernel(const bf16* __rest
                                                               float* __restrict__ vmn,
                                                               int* __restrict__ flag, int T,
                                                               int ntile) {
-  constexpr int RG = kThreads / D;
-  __shared__ float sx[kThreads], sn[kThreads];
-  const int tid = threadIdx.x, j = tid % D, rg = tid / D;
+  // thread: 8 consecutive channels (16-byte loads) of every RG-th row
+  constexpr int CPR = D / 8, RG = kThreads / CPR;
+  static_assert(kThreads % CPR == 0 && kTile % RG == 0, "vstats mapping");
+  __shared__ float sx[RG][D], sn[RG][D];
+  const int tid = threadIdx.x, c8 = (tid % CPR) * 8, rg = tid / CPR;
   const int tb = blockIdx.x % ntile, bh = blockIdx.x / ntile;
   const int r0 = tb * kTile;
   if (blockIdx.x == 0 && tid < 2) flag[tid] = 0;
   const bf16* Vh = V + (size_t)bh * T * D;
-  float a = -INFINITY, b = INFINITY;
-  for (int r = rg; r < kTile; r += RG)
-    if (r0 + r < T) {
-      const float v = (float)Vh[(size_t)(r0 + r) * D + j];
-      a = fmaxf(a, v);
-      b = fminf(b, v);
+  float a[8], b[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    a[u] = -INFINITY;
+    b[u] = INFINITY;
+  }
+  bf16x8 x[kTile / RG];
+#pragma unroll
+  for (int i = 0; i < kTile / RG; ++i) {  // every load first
+    const int r = min(r0 + rg + RG * i, T - 1);  // rows past T repeat row T - 1
+    x[i] = *reinterpret_cast<const bf16x8*>(Vh + (size_t)r * D + c8);
+  }
+#pragma unroll
+  for (int i = 0; i < kTile / RG; ++i)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      a[u] = fmaxf(a[u], (float)x[i][u]);
+      b[u] = fminf(b[u], (float)x[i][u]);
     }
-  sx[tid] = a;
-  sn[tid] = b;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    sx[rg][c8 + u] = a[u];
+    sn[rg][c8 + u] = b[u];
+  }
   __syncthreads();
-  if (rg == 0) {
+  for (int j = tid; j < D; j += kThreads) {
+    float mx = sx[0][j], mn = sn[0][j];
     for (int g = 1; g < RG; ++g) {
-      a = fmaxf(a, sx[g * D + j]);
-      b = fminf(b, sn[g * D + j]);
+      mx = fmaxf(mx, sx[g][j]);
+      mn = fminf(mn, sn[g][j]);
     }
-    vmx[((size_t)bh * ntile + tb) * D + j] = a;
-    vmn[((size_t)bh * ntile + tb) * D + j] = b;
+    vmx[((size_t)bh * ntile + tb) * D + j] = mx;
+    vmn[((size_t)bh * ntile + tb) * D + j] = mn;
   }
 }
 
