@@ -434,9 +434,16 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         const float b = sm.gb()[r * DK + c8 + u];
         const float R = sm.gb()[(CH / 2 - 1) * DK + c8 + u];
         const float bl = sm.gb()[(CH - 1) * DK + c8 + u];
-        if (OUT) pk[u] = (bf16)(kx[u] * exp2_hw((R - b) * kLog2e) * okf);
-        if (OUT) pq[u] = (bf16)(qx[u] * exp2_hw((b - R) * kLog2e) * okf);
-        pu[u] = (bf16)(kx[u] * exp2_hw((bl - b) * kLog2e) * okf);
+        if (OUT) {
+          // k~ e^{B_last - B} = (k~ e^{R - B}) e^{B_last - R}, the second
+          // factor per channel (the same for every slot of the thread)
+          const float kr = kx[u] * exp2_hw((R - b) * kLog2e) * okf;
+          pk[u] = (bf16)kr;
+          pq[u] = (bf16)(qx[u] * exp2_hw((b - R) * kLog2e) * okf);
+          pu[u] = (bf16)(kr * exp2_hw((bl - R) * kLog2e));
+        } else {
+          pu[u] = (bf16)(kx[u] * exp2_hw((bl - b) * kLog2e) * okf);
+        }
       }
       *reinterpret_cast<bf16x8*>(reinterpret_cast<char*>(sm.fku()) + swz_off<DK>(r, c8 >> 3)) = pu;
     } else {
