@@ -918,19 +918,38 @@ __device__ __forceinline__ void read_body(
     return;
   }
 
-  // ---- epilogue: o = (log2 acc - log2 l + c - bias) / (beta log2 e).  The
-  // logarithms are split into exponent and mantissa so the bias and the
-  // integer parts cancel exactly (tiny beta amplifies any error here).
+  // ---- epilogue: o = (log2(acc / l) - bias + c) / (beta log2 e) with one
+  // logarithm per output.  acc / l is a weighted mean of E = 2^(x - c +
+  // bias); it is scaled by 2^-bias (exactly) before the logarithm, so that
+  // the argument lies near 1 and the logarithm keeps its absolute precision
+  // (tiny beta amplifies any error here).  Outputs whose acc fell below
+  // 2^-64, or whose scaled mean is not a normal float, are flagged for the
+  // exact repair below.
+  static_assert(kBias == 64.f, "the scale below is 2^-bias");
   const float lt = lacc[0];
   // the prior's log-normaliser ln sum_i exp(q.k_i / sqrt d), for a backward pass
   if (MODE == kFem && lse && hl == 0 && tq < T) lse[(size_t)bh * T + tq] = (m + log2_hw(lt)) * kLn2;
-  int el;
-  const float fl = log2_hw(frexpf(lt, &el));
+  const float rl = 0x1p-64f / lt;
   const float* cw = sm.c((ntiles - 1) & 1);  // the accumulator's final column frame
   const float* inv = sm.inv();
   const float* Lh = MODE == kGated ? lam + base : nullptr;
   const float* Gh = MODE == kGated && gate ? gate + base : nullptr;
+  const auto low = [&](float a) { return !(a >= kUnderflow && a * rl >= 0x1p-120f); };
   uint64_t flags = 0;
+  {
+    float amin = INFINITY;
+#pragma unroll
+    for (int cb = 0; cb < C::NCB; ++cb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) amin = fminf(amin, acc[cb][i]);
+    if (__ballot(low(amin) && tq < T) != 0) {  // rare: find the flagged outputs
+#pragma unroll
+      for (int cb = 0; cb < C::NCB; ++cb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (low(acc[cb][i]) && tq < T) flags |= 1ull << (cb * 16 + i);
+    }
+  }
 #pragma unroll
   for (int cb = 0; cb < C::NCB; ++cb) {
 #pragma unroll
@@ -938,13 +957,8 @@ __device__ __forceinline__ void read_body(
       const int ch0 = cb * 32 + g * 8 + hl * 4;
       f32x4 o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float a = acc[cb][g * 4 + e];
-        int ea;
-        const float fa = log2_hw(frexpf(a, &ea));
-        o[e] = ((float)(ea - el - (int)kBias) + (fa - fl) + cw[ch0 + e]) * inv[ch0 + e];
-        if (!(a >= kUnderflow) && tq < T) flags |= 1ull << (cb * 16 + g * 4 + e);
-      }
+      for (int e = 0; e < 4; ++e)
+        o[e] = (log2_hw(acc[cb][g * 4 + e] * rl) + cw[ch0 + e]) * inv[ch0 + e];
       if (STAGE) {  // into the staged row at the channel's own column
         const i32x4 oc = SPLIT ? *reinterpret_cast<const i32x4*>(sm.chan() + ch0)
                                : i32x4{ch0, ch0 + 1, ch0 + 2, ch0 + 3};
