@@ -200,9 +200,10 @@ __device__ float exact_row(const bf16* __restrict__ Qh, const bf16* __restrict__
   float mine = 0.f;
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
-    if (c >= nb) break;
-    const float o = (num[c].wave_total() - d) / bl[c];
-    if (lane == c) mine = o;
+    if (c < nb) {
+      const float o = (num[c].wave_total() - d) / bl[c];
+      if (lane == c) mine = o;
+    }
   }
   return mine;
 }
