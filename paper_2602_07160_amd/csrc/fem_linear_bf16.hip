@@ -191,12 +191,12 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// elu(x) + 1, without a branch: the exponential is evaluated for every x and
-// selected (for a large positive x it overflows to +inf, which the select
-// discards).
+// elu(x) + 1 = max(e^min(x, 0), x + 1), without a select: 2^y is increasing
+// with 2^0 = 1, so e^min(x, 0) is 2^(x log2 e) clamped to [0, 1] (the clamp
+// bit of the exponential instruction), and e^x >= x + 1 for every x.
 __device__ __forceinline__ float phi(float x) {
-  const float e = exp2_hw(x * kLog2e);
-  return x > 0.f ? x + 1.f : e;
+  const float e = __builtin_amdgcn_fmed3f(exp2_hw(x * kLog2e), 0.f, 1.f);
+  return fmaxf(e, x + 1.f);
 }
 
 // RoPE of the pair (x0, x1) = dims (2m, 2m+1) at position t, then ReLU + eps.
