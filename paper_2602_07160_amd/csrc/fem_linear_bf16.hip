@@ -57,7 +57,7 @@ constexpr int DK = 64, DV = 64;  // supported widths
 constexpr int GCH = 64;          // tokens per chunk of the GLA prior
 constexpr int NTH = 256;         // 4 waves
 constexpr int ROW = 64 + 8;      // padded bf16 row (64 values + 16 B)
-constexpr int SROW = DK + 8;     // padded S^T row (bf16)
+constexpr int SROW = DV + 8;     // padded row of the state snapshot S [d_k][d_v] (bf16)
 constexpr int OBR = 32 + 4;      // padded row of a staged output block (floats)
 constexpr int STATE = DV * DK + DK + DV;  // floats per saved segment state
 constexpr int kElu = 0, kGla = 1;         // the prior
@@ -112,8 +112,8 @@ struct LinSmem {
   bf16 fq[CH * ROW];          // phi(Q) [token][d_k]
   bf16 fk[CH * DK];           // phi(K) [key][d_k], swizzled; phi(K)^T comes from transposing reads
   bf16 vs[CH * DV];           // V [key][d_v], swizzled; V^T comes from transposing reads
-  bf16 sh[NSUB][DV * SROW];   // S^T hi [d_v][d_k] at the start of each sub-chunk
-  bf16 sl[NSUB][DV * SROW];   // S^T lo
+  bf16 sh[NSUB][DK * SROW];   // S hi [d_k][d_v] at the start of each sub-chunk
+  bf16 sl[NSUB][DK * SROW];   // S lo
   float ci[DV];               // (c - kBias) / (beta log2 e): the running shift as the epilogue adds it
   float bl[DV];               // beta log2 e
   float inv[DV];
@@ -189,6 +189,25 @@ __device__ __forceinline__ int e_pos(int r) {
 // running.  (__syncthreads() would also wait for those.)
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// MFMA A fragment A[m][k] = S[k0 + k][j0 + m] (m < 32, k < 16) of a state
+// snapshot S [d_k][d_v] (row stride SROW): two transposing reads, rows in
+// natural order.  In each 16-lane group g, lane i gives the address of 4
+// columns (j0 + 16 (g & 1) + 4 (i & 3) ...) of row k0 + 8 (g >> 1) + i / 4
+// (then 4 rows further down) and receives column j0 + 16 (g & 1) + i of the
+// 4 rows: lane m + 32 hl holds A[m][8 hl + u], the A layout of
+// v_mfma_f32_32x32x16_bf16.
+__device__ __forceinline__ bf16x8 frag_snap(const bf16* t, int k0, int j0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const int row = k0 + 8 * (g >> 1) + (i >> 2);
+  const int col = j0 + 16 * (g & 1) + 4 * (i & 3);
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(t + row * SROW + col));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(t + (row + 4) * SROW + col));
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 x = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, x);
 }
 
 // elu(x) + 1 = max(e^min(x, 0), x + 1), without a select: 2^y is increasing
@@ -589,15 +608,24 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
   if (OUT) {
     const float eR =
         PRIOR == kGla ? exp2_hw(sm.gb()[(CH / 2 - 1) * DK + sub * 32 + n] * kLog2e) : 1.f;
+    // S^T (dvb, sub) into LDS as S [d_k][d_v] in bf16 hi + lo: entries
+    // 4q..4q+3 of this lane are channels dvb*32 + 8q + 4hl + 0..3 of key dim
+    // sub*32 + n, 8 contiguous bytes of a row
     auto snapshot = [&](int sn) {
+      typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int row = dvb * 32 + (i >> 2) * 8 + hl * 4 + (i & 3);
-        const int col = sub * 32 + n;
-        const float sv = st[i] * eR;
-        const bf16 hi = (bf16)sv;
-        sm.sh[sn][row * SROW + col] = hi;
-        sm.sl[sn][row * SROW + col] = (bf16)(sv - (float)hi);
+      for (int q = 0; q < 4; ++q) {
+        float sv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sv[r] = st[4 * q + r] * eR;
+        const bf16x2 h01 = to_bf16x2(sv[0], sv[1]), h23 = to_bf16x2(sv[2], sv[3]);
+        const bf16x2 l01 = to_bf16x2(sv[0] - (float)h01[0], sv[1] - (float)h01[1]);
+        const bf16x2 l23 = to_bf16x2(sv[2] - (float)h23[0], sv[3] - (float)h23[1]);
+        const int off = (sub * 32 + n) * SROW + dvb * 32 + q * 8 + hl * 4;
+        *reinterpret_cast<u32x2*>(sm.sh[sn] + off) =
+            u32x2{__builtin_bit_cast(unsigned, h01), __builtin_bit_cast(unsigned, h23)};
+        *reinterpret_cast<u32x2*>(sm.sl[sn] + off) =
+            u32x2{__builtin_bit_cast(unsigned, l01), __builtin_bit_cast(unsigned, l23)};
       }
     };
     snapshot(0);
@@ -677,7 +705,6 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el[ks], pf[ks], num, 0, 0, 0);
         if (MDEN) dacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[ks], dacc, 0, 0, 0);
       }
-      const int soff = (dvb * 32 + n) * SROW + hl * 8;
       float dz[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int sn = 0; sn < NSUB; ++sn) {
@@ -685,8 +712,8 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         const bool mine = NSUB == 1 || qs == sn;
 #pragma unroll
         for (int ks = 0; ks < DK / 16; ++ks) {
-          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sm.sh[sn] + soff + ks * 16);
-          const bf16x8 al = *reinterpret_cast<const bf16x8*>(sm.sl[sn] + soff + ks * 16);
+          const bf16x8 ah = frag_snap(sm.sh[sn], ks * 16, dvb * 32);
+          const bf16x8 al = frag_snap(sm.sl[sn], ks * 16, dvb * 32);
           bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + qrow * ROW + ks * 16 + hl * 8);
           if (!mine) b = bf16x8{};
           num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
