@@ -57,7 +57,16 @@ constexpr int DK = 64, DV = 64;  // supported widths
 constexpr int GCH = 64;          // tokens per chunk of the GLA prior
 constexpr int NTH = 256;         // 4 waves
 constexpr int ROW = 64 + 8;      // padded bf16 row (64 values + 16 B)
-constexpr int SROW = DV + 8;     // padded row of the state snapshot S [d_k][d_v] (bf16)
+// State snapshot S [d_k][d_v] in LDS (bf16): a row is 16 eight-byte chunks of
+// 4 channels, chunk k of row r stored at position k ^ snap_swz(r), so that
+// 16 consecutive rows written at one chunk, and 4 consecutive rows read at 4
+// consecutive chunks, each meet every bank once.
+constexpr int SROW = DV;
+static_assert(DV == 64, "16 chunks per snapshot row");
+__host__ __device__ constexpr int snap_swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int snap_off(int r, int j) {  // j a multiple of 4
+  return r * SROW + ((((j >> 2) ^ snap_swz(r))) << 2);
+}
 constexpr int OBR = 32 + 4;      // padded row of a staged output block (floats)
 constexpr int STATE = DV * DK + DK + DV;  // floats per saved segment state
 constexpr int kElu = 0, kGla = 1;         // the prior
@@ -191,24 +200,35 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// MFMA A fragment A[m][k] = S[k0 + k][j0 + m] (m < 32, k < 16) of a state
-// snapshot S [d_k][d_v] (row stride SROW): two transposing reads, rows in
+// MFMA A fragments A[m][k] = S[k0 + k][j0 + m] (m < 32, k < 16) of a state
+// snapshot S [d_k][d_v] (layout at snap_off): two transposing reads, rows in
 // natural order.  In each 16-lane group g, lane i gives the address of 4
 // columns (j0 + 16 (g & 1) + 4 (i & 3) ...) of row k0 + 8 (g >> 1) + i / 4
 // (then 4 rows further down) and receives column j0 + 16 (g & 1) + i of the
 // 4 rows: lane m + 32 hl holds A[m][8 hl + u], the A layout of
-// v_mfma_f32_32x32x16_bf16.
-__device__ __forceinline__ bf16x8 frag_snap(const bf16* t, int k0, int j0) {
-  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
-  const int row = k0 + 8 * (g >> 1) + (i >> 2);
-  const int col = j0 + 16 * (g & 1) + 4 * (i & 3);
-  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(t + row * SROW + col));
-  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(t + (row + 4) * SROW + col));
-  typedef short s16x8 __attribute__((ext_vector_type(8)));
-  const s16x8 x = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-  return __builtin_bit_cast(bf16x8, x);
-}
+// v_mfma_f32_32x32x16_bf16.  With k0 a multiple of 16 the swizzle does not
+// depend on k0, so the lane's two offsets are formed once (SnapFrag) and k0
+// is a constant displacement.
+struct SnapFrag {
+  int lo, hi;  // element offsets of the lane's two reads at k0 = 0
+  __device__ __forceinline__ explicit SnapFrag(int j0) {
+    const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+    const int row = 8 * (g >> 1) + (i >> 2);
+    const int col = j0 + 16 * (g & 1) + 4 * (i & 3);
+    lo = snap_off(row, col);
+    hi = snap_off(row + 4, col);
+  }
+  // k0: a multiple of 16 (the swizzle repeats every 16 rows)
+  __device__ __forceinline__ bf16x8 read(const bf16* t, int k0) const {
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    const bf16* b = t + k0 * SROW;
+    const s16x4 l = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(b + lo));
+    const s16x4 h = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(b + hi));
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const s16x8 x = {l[0], l[1], l[2], l[3], h[0], h[1], h[2], h[3]};
+    return __builtin_bit_cast(bf16x8, x);
+  }
+};
 
 // elu(x) + 1 = max(e^min(x, 0), x + 1), without a select: 2^y is increasing
 // with 2^0 = 1, so e^min(x, 0) is 2^(x log2 e) clamped to [0, 1] (the clamp
@@ -621,7 +641,7 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         const bf16x2 h01 = to_bf16x2(sv[0], sv[1]), h23 = to_bf16x2(sv[2], sv[3]);
         const bf16x2 l01 = to_bf16x2(sv[0] - (float)h01[0], sv[1] - (float)h01[1]);
         const bf16x2 l23 = to_bf16x2(sv[2] - (float)h23[0], sv[3] - (float)h23[1]);
-        const int off = (sub * 32 + n) * SROW + dvb * 32 + q * 8 + hl * 4;
+        const int off = snap_off(sub * 32 + n, dvb * 32 + q * 8 + hl * 4);
         *reinterpret_cast<u32x2*>(sm.sh[sn] + off) =
             u32x2{__builtin_bit_cast(unsigned, h01), __builtin_bit_cast(unsigned, h23)};
         *reinterpret_cast<u32x2*>(sm.sl[sn] + off) =
@@ -706,14 +726,15 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
         if (MDEN) dacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, pf[ks], dacc, 0, 0, 0);
       }
       float dz[4] = {0.f, 0.f, 0.f, 0.f};
+      const SnapFrag sf(dvb * 32);
 #pragma unroll
       for (int sn = 0; sn < NSUB; ++sn) {
         // NSUB = 2: snapshot sn feeds only the query columns of chunk sn
         const bool mine = NSUB == 1 || qs == sn;
 #pragma unroll
         for (int ks = 0; ks < DK / 16; ++ks) {
-          const bf16x8 ah = frag_snap(sm.sh[sn], ks * 16, dvb * 32);
-          const bf16x8 al = frag_snap(sm.sl[sn], ks * 16, dvb * 32);
+          const bf16x8 ah = sf.read(sm.sh[sn], ks * 16);
+          const bf16x8 al = sf.read(sm.sl[sn], ks * 16);
           bf16x8 b = *reinterpret_cast<const bf16x8*>(sm.fq + qrow * ROW + ks * 16 + hl * 8);
           if (!mine) b = bf16x8{};
           num = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b, num, 0, 0, 0);
