@@ -171,12 +171,6 @@ struct ScanSmem<kGla, GCH, 1> : LinSmem<GCH, 1> {
   __device__ bf16* fku() { return gla.fk2; }
 };
 
-// Element (row, col) of a swizzled [64][64] tile.
-__device__ __forceinline__ float swz_elem(const bf16* t, int row, int col) {
-  return (float)*reinterpret_cast<const bf16*>(reinterpret_cast<const char*>(t) +
-                                               swz_off<DK>(row, col >> 3) + (col & 7) * 2);
-}
-
 // Entry i of the inter-chunk normaliser vector, as bf16 hi + lo.
 template <int CH, int NSUB>
 __device__ __forceinline__ void put_zn(LinSmem<CH, NSUB>& sm, int i, float v) {
@@ -589,18 +583,30 @@ __device__ __forceinline__ void scan_chunk(ScanSmem<PRIOR, CH, NSUB>& sm, f32x16
       }
     }
   };
-  // tile sum of phi(k): thread (column tid & 63, quarter tid >> 6) sums CH/4
-  // rows; the four partial sums meet in LDS
+  // tile sum of phi(k): wave q4 takes a quarter of the rows, lane (pair cp,
+  // half h) sums columns 2cp and 2cp + 1 over CH/8 of them with 4-byte reads;
+  // the two halves meet by a lane swap, the four quarters in LDS
   {
-    const int dkc = tid & 63, q4 = tid >> 6;
-    float s = 0.f;
+    const int q4 = tid >> 6, cp = lane & 31, h = lane >> 5;
+    float s0 = 0.f, s1 = 0.f;
 #pragma unroll
-    for (int r = 0; r < CH / 4; ++r)
-      s += swz_elem(sm.fku(), q4 * (CH / 4) + r, dkc);
-    sm.zc[q4 * DK + dkc] = s;
+    for (int r = 0; r < CH / 8; ++r) {
+      const int row = q4 * (CH / 4) + h * (CH / 8) + r;
+      const bf16x2 p = *reinterpret_cast<const bf16x2*>(
+          reinterpret_cast<const char*>(sm.fku()) + swz_off<DK>(row, cp >> 2) + (cp & 3) * 4);
+      s0 += (float)p[0];
+      s1 += (float)p[1];
+    }
+    s0 += other_half(s0);
+    s1 += other_half(s1);
+    if (h == 0) {
+      sm.zc[q4 * DK + 2 * cp] = s0;
+      sm.zc[q4 * DK + 2 * cp + 1] = s1;
+    }
     // GLA: the inter-chunk normaliser reads e^{R} z
     if (PRIOR == kGla && q4 == 0)
     {
+      const int dkc = lane;
       const float zr = sm.z[dkc] * exp2_hw(sm.gb()[(CH / 2 - 1) * DK + dkc] * kLog2e);
       sm.gzr()[dkc] = zr;
       put_zn(sm, dkc, zr);
